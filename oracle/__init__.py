@@ -1,0 +1,26 @@
+"""CPU oracle for Windowed-MTP draft decode attention.
+
+TEST INFRASTRUCTURE ONLY.  This package is the plain, slow, float64 statement
+of what the draft-attention hot path computes.  Only the test suite, the smoke
+check and the CPU-baseline leg of the benchmark may import it; the product
+path (the HIP library and its Python binding) never does, and shares no code
+with it.
+
+Modules
+  attention  -- key selection (sink + recent window), exact masked-softmax
+                GQA decode attention (Windowed-MTP paper, Section 4
+                "Mechanism" and the Appendix A pseudocode of the windowing
+                change).
+  ring       -- the compact ring-buffer draft KV store: the slot map and an
+                operational replay of appends (Section 4 "Memory", Section 6
+                "Memory", the ring comment of the Appendix A pseudocode).
+
+Every function states the passage it follows.  Readings of points where the
+paper is silent are listed in the module docstrings.  No function here is
+"parity unpinned": each is pinned by the CPU tests in tests/test_oracle_*.py
+against closed forms, brute force, invariants, a library routine
+(torch scaled_dot_product_attention in float64) and the facts the paper prints
+(tests/golden/).
+"""
+
+from . import attention, ring  # noqa: F401
