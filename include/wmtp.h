@@ -1,0 +1,184 @@
+/*
+ * wmtp.h -- C ABI of the Windowed-MTP draft decode attention library
+ * (libwmtp.so, AMD Instinct MI355X / gfx950).
+ *
+ * The library computes the MTP draft head's single-token GQA decode attention
+ * over its KV cache, as described in "Windowed-MTP: Removing the Full-Context
+ * Draft-KV Tax at Million-Token Context":
+ *   - full-context: the native draft attends every cached key (Section 3,
+ *     per-step latency model; Figure "window", native row);
+ *   - windowed: the draft attends the first `sink` keys plus the most recent
+ *     `W` keys, and all keys while S <= sink + W (Section 4 "Mechanism";
+ *     Appendix A, pseudocode of the windowing change);
+ *   - ring: the same windowed attention over a compact per-request ring that
+ *     stores only the sink and a circular window region (Section 4 and
+ *     Section 6 "Memory"; the ring comment of the Appendix A pseudocode).
+ *
+ * Common conventions
+ *   - All tensor pointers are DEVICE pointers owned by the caller.  The
+ *     library allocates nothing, keeps no state between calls, never
+ *     synchronises and only enqueues work on `stream` (a hipStream_t; NULL is
+ *     the default stream).  Calls are safe to capture in a HIP graph.
+ *   - bf16 tensors are raw bfloat16 bit patterns (uint16), row-major, and must
+ *     be 16-byte aligned; int32 arrays must be 4-byte aligned.
+ *   - Shapes: q and out [B, Hq, d]; a dense cache [B, S_max, Hkv, d]; a ring
+ *     [B, sink + R_w, Hkv, d]; lens [B].  Query head h reads KV head
+ *     h / (Hq / Hkv) (consecutive GQA grouping).
+ *   - d must be 64, 128 or 256 and G = Hq / Hkv at most 16, otherwise
+ *     WMTP_EUNSUPPORTED.  Other invalid arguments give WMTP_EINVAL; both are
+ *     detected on the host before anything is enqueued.
+ *   - Lengths live on the device (so a captured graph can replay a growing
+ *     sequence).  lens[b] is the number of cached keys of sequence b, counting
+ *     the current draft token's row.  A length outside its valid range is
+ *     clamped on the device and WMTP_DERR_* bits are OR-ed into *err when
+ *     `err` is not NULL.
+ *   - Arithmetic: bf16 inputs, fp32 logits / softmax / accumulation, bf16
+ *     output rounded to nearest even; lse (optional) is the natural-log
+ *     log-sum-exp of the scaled logits in fp32.  An empty sequence (no keys)
+ *     gives out = 0 and lse = -inf.
+ *   - Results are deterministic: no atomics take part in any reduction.
+ */
+#ifndef WMTP_H
+#define WMTP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Host-side status codes. */
+typedef enum {
+  WMTP_OK = 0,
+  WMTP_EINVAL = 1,        /* bad argument (null pointer, misalignment, bad size) */
+  WMTP_EUNSUPPORTED = 2,  /* head size or GQA group outside the built kernels */
+  WMTP_EWORKSPACE = 3,    /* ws_bytes smaller than wmtp_workspace_bytes() */
+  WMTP_ELAUNCH = 4        /* the HIP runtime rejected a kernel launch */
+} wmtp_status;
+
+/* Device error bits, OR-ed into *err by the kernels. */
+#define WMTP_DERR_LEN_RANGE 0x1  /* lens[b] < 0, or > S_max for a dense cache: clamped */
+#define WMTP_DERR_NNEW_RANGE 0x2 /* n_new[b] outside [0, n_max]: clamped */
+#define WMTP_DERR_CAPACITY 0x4   /* dense-cache append past S_max: extra rows dropped */
+
+/* Attention variants, for wmtp_workspace_bytes(). */
+typedef enum {
+  WMTP_VARIANT_FULL = 0,
+  WMTP_VARIANT_WINDOWED = 1,
+  WMTP_VARIANT_RING = 2
+} wmtp_variant;
+
+/*
+ * Workspace (device bytes) that one attention call of the given variant and
+ * shape needs for its split-K partial results (per split and query head: the
+ * running maximum, the softmax denominator and the unnormalised output row).
+ * S_max is the dense cache capacity (ignored for the ring); W and sink are
+ * ignored for the full variant.  Returns 0 for arguments the attention calls
+ * would reject.  The workspace needs no initialisation and may be reused by
+ * successive calls on one stream.
+ */
+size_t wmtp_workspace_bytes(int variant, int B, int Hq, int Hkv, int d, int64_t S_max, int W,
+                            int sink);
+
+/*
+ * Full-context draft decode attention (the native MTP draft; Section 3 and
+ * the Figure "window" native row): every query token attends all keys
+ * [0, lens[b]) of its sequence.
+ *   q      [B, Hq, d] bf16           one draft query token per sequence
+ *   k, v   [B, S_max, Hkv, d] bf16   dense draft KV cache, rows in position order
+ *   lens   [B] int32 device          0 <= lens[b] <= S_max
+ *   out    [B, Hq, d] bf16           attention output
+ *   lse    [B, Hq] fp32 or NULL      natural-log log-sum-exp of the logits
+ *   scale  logit scale (usually 1/sqrt(d)); must be finite
+ *   ws, ws_bytes  workspace, see wmtp_workspace_bytes(WMTP_VARIANT_FULL, ...)
+ *   err    device int32 error word or NULL
+ */
+int wmtp_draft_attn_full(const void* q, const void* k, const void* v, const int32_t* lens,
+                         void* out, float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
+                         float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream);
+
+/*
+ * Windowed draft decode attention over the dense cache (Section 4
+ * "Mechanism"; Appendix A pseudocode): with S = lens[b], the kept keys are
+ * [0, sink) and [S - W, S) when S > sink + W, and [0, S) otherwise -- at most
+ * sink + W keys, whatever S is.  No other mask is applied.  Arguments as for
+ * wmtp_draft_attn_full, plus
+ *   W     recent-window length, >= 1 (the current token is always attended)
+ *   sink  number of attention-sink keys, >= 0
+ * Workspace: wmtp_workspace_bytes(WMTP_VARIANT_WINDOWED, ...).
+ */
+int wmtp_draft_attn_windowed(const void* q, const void* k, const void* v, const int32_t* lens,
+                             void* out, float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
+                             int W, int sink, float scale, void* ws, size_t ws_bytes,
+                             int32_t* err, void* stream);
+
+/*
+ * Windowed draft decode attention over the compact ring store (Section 4 and
+ * Section 6 "Memory": the draft KV pool shrinks to a fixed sink + window +
+ * headroom footprint per request).  Logical position p of sequence b lives
+ * in slot
+ *     p                          if p < sink
+ *     sink + ((p - sink) % R_w)  otherwise
+ * of k_ring/v_ring [B, sink + R_w, Hkv, d]; lens[b] is the logical length
+ * (any value >= 0).  R_w >= W keeps the whole window resident; the paper's
+ * chain setting is R_w = W + gamma + 1 so rows of rejected draft tokens
+ * never overwrite the live window.  The kept keys and their order are those
+ * of wmtp_draft_attn_windowed, so the two calls give bit-identical outputs
+ * for the same logical content.
+ * Workspace: wmtp_workspace_bytes(WMTP_VARIANT_RING, ...).
+ */
+int wmtp_ring_attn(const void* q, const void* k_ring, const void* v_ring, const int32_t* lens,
+                   void* out, float* lse, int B, int Hq, int Hkv, int d, int W, int sink, int R_w,
+                   float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream);
+
+/*
+ * Append draft KV rows to the ring store (the draft forward writes the K/V
+ * row of each draft token it processes; Section 3 "Per-step latency model").
+ * For each sequence b, rows k_new[b, i], v_new[b, i] for i < n_new[b] take
+ * logical positions lens[b] + i and are written to their ring slots; then
+ * lens[b] += n_new[b] on the device.  When n_new[b] exceeds the ring, only
+ * rows that stay resident are written (the sink and the last R_w positions),
+ * which equals writing every row in order.
+ *   k_new, v_new  [B, n_max, Hkv, d] bf16;  n_new [B] int32 device, 0..n_max
+ * One call must not run concurrently with an attention call on the same ring.
+ */
+int wmtp_ring_append(void* k_ring, void* v_ring, const void* k_new, const void* v_new,
+                     const int32_t* n_new, int32_t* lens, int B, int Hkv, int d, int sink, int R_w,
+                     int n_max, int32_t* err, void* stream);
+
+/*
+ * Append draft KV rows to a dense cache [B, S_max, Hkv, d]: rows go to
+ * positions lens[b] .. lens[b] + n_new[b] - 1, then lens[b] += n_new[b].
+ * Rows past S_max are dropped, lens[b] is clamped to S_max and
+ * WMTP_DERR_CAPACITY is raised.  Other arguments as for wmtp_ring_append.
+ */
+int wmtp_cache_append(void* k, void* v, const void* k_new, const void* v_new,
+                      const int32_t* n_new, int32_t* lens, int B, int Hkv, int d, int64_t S_max,
+                      int n_max, int32_t* err, void* stream);
+
+/*
+ * Export of the windowed key selection and ring slot map that the attention
+ * kernels use (for tests and debugging).  For each b and virtual key index
+ * j < sink + W: pos_out[b, j] is the logical position of the j-th kept key
+ * (ascending), or -1 for j >= n_sel; slot_out[b, j] (may be NULL) its ring
+ * slot for ring window R_w (-1 past n_sel); n_sel_out[b] = min(lens[b],
+ * sink + W).  lens[b] < 0 is clamped to 0 and flagged.  R_w is only used for
+ * slot_out and must then be >= W.
+ */
+int wmtp_select_indices(const int32_t* lens, int B, int W, int sink, int R_w, int32_t* pos_out,
+                        int32_t* slot_out, int32_t* n_sel_out, int32_t* err, void* stream);
+
+/* Human-readable name of a wmtp_status value (static string). */
+const char* wmtp_status_string(int status);
+
+/* ABI version of this header, (major << 16) | minor. */
+int wmtp_abi_version(void);
+
+#define WMTP_ABI_VERSION ((1 << 16) | 0)
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WMTP_H */

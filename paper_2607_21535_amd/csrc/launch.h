@@ -1,0 +1,64 @@
+// Internal launch interface between the C-ABI layer and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wmtp {
+
+// One attention call, already validated on the host.
+struct AttnLaunch {
+  int variant;  // wmtp_variant
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* lens;
+  uint16_t* out;
+  float* lse;
+  int32_t* err;
+  int B, Hq, Hkv, d;
+  int64_t rows;     // storage rows per sequence: S_max, or sink + R_w for the ring
+  int64_t len_cap;  // largest valid lens[b]
+  int W, sink, R_w;
+  float scale;
+  // split plan (from plan_split)
+  int chunk;
+  int max_items;  // work items per KV head, upper bound over all lengths
+  float* pm;
+  float* pl;
+  float* po;
+};
+
+struct SplitPlan {
+  int chunk;       // keys per work item (multiple of kChunkQuantum)
+  int max_items;   // B * ceil(n_keys_max / chunk)
+  size_t bytes;    // workspace bytes
+  size_t off_pl;   // byte offsets of the partial arrays inside the workspace
+  size_t off_po;
+};
+
+// Split plan for a validated shape; n_keys_max = most keys one sequence attends.
+SplitPlan plan_split(int B, int Hq, int Hkv, int d, int64_t n_keys_max);
+
+hipError_t launch_attention(const AttnLaunch& a, hipStream_t stream);
+
+struct AppendLaunch {
+  bool ring;
+  uint16_t* k;
+  uint16_t* v;
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  const int32_t* n_new;
+  int32_t* lens;
+  int32_t* err;
+  int B, Hkv, d;
+  int64_t rows;     // dense: S_max; ring: sink + R_w
+  int sink, R_w, n_max;
+};
+
+hipError_t launch_append(const AppendLaunch& a, hipStream_t stream);
+
+hipError_t launch_select(const int32_t* lens, int B, int W, int sink, int R_w, int32_t* pos_out,
+                         int32_t* slot_out, int32_t* n_sel_out, int32_t* err, hipStream_t stream);
+
+}  // namespace wmtp

@@ -1,0 +1,227 @@
+// C ABI of libwmtp.so: host-side validation and launch of the kernels.
+// Every check runs before anything is enqueued; nothing here allocates,
+// synchronises or keeps state.
+
+#include "../../include/wmtp.h"
+#include "launch.h"
+
+#include <climits>
+#include <cmath>
+#include <cstdint>
+
+#define WMTP_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+using wmtp::AttnLaunch;
+using wmtp::SplitPlan;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Head shape: EINVAL for malformed values, EUNSUPPORTED for well-formed
+// shapes without a kernel (d not 64/128/256, more than 16 query heads per KV
+// head).
+int check_heads(int B, int Hq, int Hkv, int d) {
+  if (B < 0 || Hkv < 1 || Hq < 1 || d < 1 || Hq % Hkv != 0) return WMTP_EINVAL;
+  if (d != 64 && d != 128 && d != 256) return WMTP_EUNSUPPORTED;
+  if (Hq / Hkv > 16) return WMTP_EUNSUPPORTED;
+  return WMTP_OK;
+}
+
+int check_window(int W, int sink) {
+  if (W < 1 || sink < 0 || static_cast<int64_t>(W) + sink > INT_MAX / 2) return WMTP_EINVAL;
+  return WMTP_OK;
+}
+
+// Most keys one sequence attends, for the split plan.  The windowed and ring
+// variants plan for sink + W whatever the cache capacity, so both split the
+// same key set identically (bit-identical results).
+int64_t keys_max(int variant, int64_t S_max, int W, int sink) {
+  return variant == WMTP_VARIANT_FULL ? S_max : static_cast<int64_t>(W) + sink;
+}
+
+bool plan_fits(const SplitPlan& p, int Hkv) {
+  return static_cast<int64_t>(p.max_items) * Hkv < INT_MAX;
+}
+
+int attention_common(int variant, const void* q, const void* k, const void* v,
+                     const int32_t* lens, void* out, float* lse, int B, int Hq, int Hkv, int d,
+                     int64_t S_max, int W, int sink, int R_w, float scale, void* ws,
+                     size_t ws_bytes, int32_t* err, void* stream) {
+  int st = check_heads(B, Hq, Hkv, d);
+  if (st != WMTP_OK) return st;
+  if (variant != WMTP_VARIANT_FULL) {
+    st = check_window(W, sink);
+    if (st != WMTP_OK) return st;
+  }
+  if (variant == WMTP_VARIANT_RING && R_w < W) return WMTP_EINVAL;
+  if (S_max < 0) return WMTP_EINVAL;
+  if (!std::isfinite(scale)) return WMTP_EINVAL;
+  if (B == 0) return WMTP_OK;
+  if (q == nullptr || k == nullptr || v == nullptr || lens == nullptr || out == nullptr)
+    return WMTP_EINVAL;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(lens, 4) || (lse != nullptr && !aligned(lse, 4)) ||
+      (err != nullptr && !aligned(err, 4)))
+    return WMTP_EINVAL;
+
+  const SplitPlan plan = wmtp::plan_split(B, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
+  if (!plan_fits(plan, Hkv)) return WMTP_EUNSUPPORTED;
+  if (ws_bytes < plan.bytes) return WMTP_EWORKSPACE;
+  if (plan.bytes > 0 && (ws == nullptr || !aligned(ws, 256))) return WMTP_EINVAL;
+
+  AttnLaunch L{};
+  L.variant = variant;
+  L.q = static_cast<const uint16_t*>(q);
+  L.k = static_cast<const uint16_t*>(k);
+  L.v = static_cast<const uint16_t*>(v);
+  L.lens = lens;
+  L.out = static_cast<uint16_t*>(out);
+  L.lse = lse;
+  L.err = err;
+  L.B = B;
+  L.Hq = Hq;
+  L.Hkv = Hkv;
+  L.d = d;
+  if (variant == WMTP_VARIANT_RING) {
+    L.rows = static_cast<int64_t>(sink) + R_w;
+    L.len_cap = INT_MAX;
+  } else {
+    L.rows = S_max;
+    L.len_cap = S_max < INT_MAX ? S_max : INT_MAX;
+  }
+  L.W = W;
+  L.sink = sink;
+  L.R_w = R_w;
+  L.scale = scale;
+  L.chunk = plan.chunk;
+  L.max_items = plan.max_items;
+  char* base = static_cast<char*>(ws);
+  L.pm = reinterpret_cast<float*>(base);
+  L.pl = reinterpret_cast<float*>(base + plan.off_pl);
+  L.po = reinterpret_cast<float*>(base + plan.off_po);
+  if (wmtp::launch_attention(L, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return WMTP_ELAUNCH;
+  return WMTP_OK;
+}
+
+int append_common(bool ring, void* k, void* v, const void* k_new, const void* v_new,
+                  const int32_t* n_new, int32_t* lens, int B, int Hkv, int d, int64_t rows,
+                  int sink, int R_w, int n_max, int32_t* err, void* stream) {
+  if (B < 0 || Hkv < 1 || d < 1 || n_max < 0) return WMTP_EINVAL;
+  if (d != 64 && d != 128 && d != 256) return WMTP_EUNSUPPORTED;
+  if (ring && (sink < 0 || R_w < 1 || static_cast<int64_t>(sink) + R_w > INT_MAX))
+    return WMTP_EINVAL;
+  if (!ring && (rows < 0 || rows > INT_MAX)) return WMTP_EINVAL;
+  if (B == 0) return WMTP_OK;
+  if (k == nullptr || v == nullptr || lens == nullptr || n_new == nullptr) return WMTP_EINVAL;
+  if (n_max > 0 && (k_new == nullptr || v_new == nullptr)) return WMTP_EINVAL;
+  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) ||
+      !aligned(n_new, 4) || !aligned(lens, 4) || (err != nullptr && !aligned(err, 4)))
+    return WMTP_EINVAL;
+  wmtp::AppendLaunch L{};
+  L.ring = ring;
+  L.k = static_cast<uint16_t*>(k);
+  L.v = static_cast<uint16_t*>(v);
+  L.k_new = static_cast<const uint16_t*>(k_new);
+  L.v_new = static_cast<const uint16_t*>(v_new);
+  L.n_new = n_new;
+  L.lens = lens;
+  L.err = err;
+  L.B = B;
+  L.Hkv = Hkv;
+  L.d = d;
+  L.rows = ring ? static_cast<int64_t>(sink) + R_w : rows;
+  L.sink = ring ? sink : 0;
+  L.R_w = ring ? R_w : 1;
+  L.n_max = n_max;
+  if (wmtp::launch_append(L, static_cast<hipStream_t>(stream)) != hipSuccess) return WMTP_ELAUNCH;
+  return WMTP_OK;
+}
+
+}  // namespace
+
+WMTP_EXPORT size_t wmtp_workspace_bytes(int variant, int B, int Hq, int Hkv, int d, int64_t S_max,
+                                        int W, int sink) {
+  if (variant != WMTP_VARIANT_FULL && variant != WMTP_VARIANT_WINDOWED &&
+      variant != WMTP_VARIANT_RING)
+    return 0;
+  if (check_heads(B, Hq, Hkv, d) != WMTP_OK || B == 0) return 0;
+  if (variant != WMTP_VARIANT_FULL && check_window(W, sink) != WMTP_OK) return 0;
+  if (variant == WMTP_VARIANT_FULL && S_max < 0) return 0;
+  const SplitPlan plan = wmtp::plan_split(B, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
+  if (!plan_fits(plan, Hkv)) return 0;
+  return plan.bytes;
+}
+
+WMTP_EXPORT int wmtp_draft_attn_full(const void* q, const void* k, const void* v,
+                                     const int32_t* lens, void* out, float* lse, int B, int Hq,
+                                     int Hkv, int d, int64_t S_max, float scale, void* ws,
+                                     size_t ws_bytes, int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_FULL, q, k, v, lens, out, lse, B, Hq, Hkv, d, S_max, 1, 0,
+                          1, scale, ws, ws_bytes, err, stream);
+}
+
+WMTP_EXPORT int wmtp_draft_attn_windowed(const void* q, const void* k, const void* v,
+                                         const int32_t* lens, void* out, float* lse, int B,
+                                         int Hq, int Hkv, int d, int64_t S_max, int W, int sink,
+                                         float scale, void* ws, size_t ws_bytes, int32_t* err,
+                                         void* stream) {
+  return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, out, lse, B, Hq, Hkv, d, S_max, W,
+                          sink, W, scale, ws, ws_bytes, err, stream);
+}
+
+WMTP_EXPORT int wmtp_ring_attn(const void* q, const void* k_ring, const void* v_ring,
+                               const int32_t* lens, void* out, float* lse, int B, int Hq, int Hkv,
+                               int d, int W, int sink, int R_w, float scale, void* ws,
+                               size_t ws_bytes, int32_t* err, void* stream) {
+  if (check_window(W, sink) == WMTP_OK && (R_w < W || static_cast<int64_t>(sink) + R_w > INT_MAX))
+    return WMTP_EINVAL;
+  return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, out, lse, B, Hq, Hkv, d,
+                          static_cast<int64_t>(sink) + R_w, W, sink, R_w, scale, ws, ws_bytes,
+                          err, stream);
+}
+
+WMTP_EXPORT int wmtp_ring_append(void* k_ring, void* v_ring, const void* k_new,
+                                 const void* v_new, const int32_t* n_new, int32_t* lens, int B,
+                                 int Hkv, int d, int sink, int R_w, int n_max, int32_t* err,
+                                 void* stream) {
+  return append_common(true, k_ring, v_ring, k_new, v_new, n_new, lens, B, Hkv, d, 0, sink, R_w,
+                       n_max, err, stream);
+}
+
+WMTP_EXPORT int wmtp_cache_append(void* k, void* v, const void* k_new, const void* v_new,
+                                  const int32_t* n_new, int32_t* lens, int B, int Hkv, int d,
+                                  int64_t S_max, int n_max, int32_t* err, void* stream) {
+  return append_common(false, k, v, k_new, v_new, n_new, lens, B, Hkv, d, S_max, 0, 1, n_max, err,
+                       stream);
+}
+
+WMTP_EXPORT int wmtp_select_indices(const int32_t* lens, int B, int W, int sink, int R_w,
+                                    int32_t* pos_out, int32_t* slot_out, int32_t* n_sel_out,
+                                    int32_t* err, void* stream) {
+  if (B < 0 || check_window(W, sink) != WMTP_OK) return WMTP_EINVAL;
+  if (slot_out != nullptr && R_w < W) return WMTP_EINVAL;
+  if (B == 0) return WMTP_OK;
+  if (lens == nullptr || pos_out == nullptr || n_sel_out == nullptr) return WMTP_EINVAL;
+  if (!aligned(lens, 4) || !aligned(pos_out, 4) || !aligned(n_sel_out, 4) ||
+      (slot_out != nullptr && !aligned(slot_out, 4)) || (err != nullptr && !aligned(err, 4)))
+    return WMTP_EINVAL;
+  if (wmtp::launch_select(lens, B, W, sink, slot_out != nullptr ? R_w : W, pos_out, slot_out,
+                          n_sel_out, err, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return WMTP_ELAUNCH;
+  return WMTP_OK;
+}
+
+WMTP_EXPORT const char* wmtp_status_string(int status) {
+  switch (status) {
+    case WMTP_OK: return "WMTP_OK";
+    case WMTP_EINVAL: return "WMTP_EINVAL: invalid argument";
+    case WMTP_EUNSUPPORTED: return "WMTP_EUNSUPPORTED: shape without a built kernel";
+    case WMTP_EWORKSPACE: return "WMTP_EWORKSPACE: workspace too small";
+    case WMTP_ELAUNCH: return "WMTP_ELAUNCH: kernel launch failed";
+    default: return "unknown wmtp status";
+  }
+}
+
+WMTP_EXPORT int wmtp_abi_version(void) { return WMTP_ABI_VERSION; }

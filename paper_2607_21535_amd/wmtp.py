@@ -1,0 +1,262 @@
+"""Python binding of libwmtp.so (ctypes): argument marshalling only.
+
+Every function here checks tensor dtypes, devices and shapes, allocates
+outputs/workspace with torch when the caller passes none, and calls the C ABI
+(include/wmtp.h) with raw device pointers on torch's current HIP stream.
+All computation happens in the library's HIP kernels; there is no fallback:
+if libwmtp.so is missing or fails to load, every call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+__all__ = [
+    "WmtpError",
+    "VARIANT_FULL",
+    "VARIANT_WINDOWED",
+    "VARIANT_RING",
+    "DERR_LEN_RANGE",
+    "DERR_NNEW_RANGE",
+    "DERR_CAPACITY",
+    "lib_path",
+    "load_library",
+    "workspace_bytes",
+    "draft_attn_full",
+    "draft_attn_windowed",
+    "ring_attn",
+    "ring_append",
+    "cache_append",
+    "select_indices",
+    "status_string",
+    "EXPORTED_SYMBOLS",
+]
+
+VARIANT_FULL, VARIANT_WINDOWED, VARIANT_RING = 0, 1, 2
+DERR_LEN_RANGE, DERR_NNEW_RANGE, DERR_CAPACITY = 0x1, 0x2, 0x4
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, ELAUNCH = 0, 1, 2, 3, 4
+
+EXPORTED_SYMBOLS = (
+    "wmtp_workspace_bytes",
+    "wmtp_draft_attn_full",
+    "wmtp_draft_attn_windowed",
+    "wmtp_ring_attn",
+    "wmtp_ring_append",
+    "wmtp_cache_append",
+    "wmtp_select_indices",
+    "wmtp_status_string",
+    "wmtp_abi_version",
+)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_I64 = ctypes.c_int64
+_F = ctypes.c_float
+_SZ = ctypes.c_size_t
+
+_SIGNATURES = {
+    "wmtp_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I64, _I, _I]),
+    "wmtp_draft_attn_full": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _F, _P, _SZ, _P, _P]),
+    "wmtp_draft_attn_windowed": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _F, _P, _SZ, _P, _P]),
+    "wmtp_ring_attn": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P, _SZ, _P, _P]),
+    "wmtp_ring_append": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
+    "wmtp_cache_append": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I64, _I, _P, _P]),
+    "wmtp_select_indices": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
+    "wmtp_status_string": (ctypes.c_char_p, [_I]),
+    "wmtp_abi_version": (_I, []),
+}
+
+
+class WmtpError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+def lib_path() -> str:
+    return os.environ.get("WMTP_LIB", os.path.join(_HERE, "libwmtp.so"))
+
+
+def load_library():
+    """Load libwmtp.so (once).  Raises OSError when it is missing."""
+    global _LIB
+    if _LIB is None:
+        path = lib_path()
+        if not os.path.exists(path):
+            raise OSError(f"{path} not found: build it with `python -m paper_2607_21535_amd.build`")
+        lib = ctypes.CDLL(path)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = lib
+    return _LIB
+
+
+def status_string(status: int) -> str:
+    return load_library().wmtp_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise WmtpError(status, where)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _need(t, name, dtype, ndim=None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on a HIP device")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+
+
+def workspace_bytes(variant, B, Hq, Hkv, d, S_max=0, W=1, sink=0) -> int:
+    return int(load_library().wmtp_workspace_bytes(variant, B, Hq, Hkv, d, S_max, W, sink))
+
+
+def _workspace(ws, nbytes, device):
+    if ws is None:
+        if nbytes == 0:
+            return None
+        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    if ws.numel() * ws.element_size() < nbytes:
+        raise WmtpError(EWORKSPACE, "workspace")
+    return ws
+
+
+def _attn_io(q, k, v, lens, out, lse):
+    _need(q, "q", torch.bfloat16, 3)
+    dev = q.device
+    _need(k, "k", torch.bfloat16, 4, dev)
+    _need(v, "v", torch.bfloat16, 4, dev)
+    _need(lens, "lens", torch.int32, 1, dev)
+    B, Hq, d = q.shape
+    if k.shape != v.shape or k.shape[0] != B or k.shape[3] != d or lens.shape[0] != B:
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)} lens {tuple(lens.shape)}")
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need(out, "out", torch.bfloat16, 3, dev)
+        if out.shape != q.shape:
+            raise ValueError("out must have q's shape")
+    if lse is not None:
+        _need(lse, "lse", torch.float32, 2, dev)
+        if tuple(lse.shape) != (B, Hq):
+            raise ValueError("lse must be [B, Hq]")
+    return dev, B, Hq, d, out
+
+
+def draft_attn_full(q, k, v, lens, out=None, lse=None, scale=None, ws=None, err=None):
+    """Full-context draft decode attention; returns out [B, Hq, d] bf16."""
+    dev, B, Hq, d, out = _attn_io(q, k, v, lens, out, lse)
+    S_max, Hkv = k.shape[1], k.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    nb = workspace_bytes(VARIANT_FULL, B, Hq, Hkv, d, S_max)
+    ws = _workspace(ws, nb, dev)
+    st = load_library().wmtp_draft_attn_full(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, S_max, scale,
+        _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_attn_full")
+    return out
+
+
+def draft_attn_windowed(q, k, v, lens, W, sink, out=None, lse=None, scale=None, ws=None, err=None):
+    """Sink + recent-window draft decode attention over a dense cache."""
+    dev, B, Hq, d, out = _attn_io(q, k, v, lens, out, lse)
+    S_max, Hkv = k.shape[1], k.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    nb = workspace_bytes(VARIANT_WINDOWED, B, Hq, Hkv, d, S_max, W, sink)
+    ws = _workspace(ws, nb, dev)
+    st = load_library().wmtp_draft_attn_windowed(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, S_max, W, sink,
+        scale, _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_attn_windowed")
+    return out
+
+
+def ring_attn(q, k_ring, v_ring, lens, W, sink, R_w, out=None, lse=None, scale=None, ws=None, err=None):
+    """Windowed draft decode attention over the compact ring [B, sink+R_w, Hkv, d]."""
+    dev, B, Hq, d, out = _attn_io(q, k_ring, v_ring, lens, out, lse)
+    if k_ring.shape[1] != sink + R_w:
+        raise ValueError(f"ring must hold sink + R_w = {sink + R_w} rows, has {k_ring.shape[1]}")
+    Hkv = k_ring.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    nb = workspace_bytes(VARIANT_RING, B, Hq, Hkv, d, sink + R_w, W, sink)
+    ws = _workspace(ws, nb, dev)
+    st = load_library().wmtp_ring_attn(
+        _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, W, sink,
+        R_w, scale, _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _ptr(err), _stream(dev))
+    _check(st, "wmtp_ring_attn")
+    return out
+
+
+def _append_io(k, v, k_new, v_new, n_new, lens):
+    _need(k, "k", torch.bfloat16, 4)
+    dev = k.device
+    _need(v, "v", torch.bfloat16, 4, dev)
+    _need(k_new, "k_new", torch.bfloat16, 4, dev)
+    _need(v_new, "v_new", torch.bfloat16, 4, dev)
+    _need(n_new, "n_new", torch.int32, 1, dev)
+    _need(lens, "lens", torch.int32, 1, dev)
+    B, _, Hkv, d = k.shape
+    if (v.shape != k.shape or k_new.shape != v_new.shape or k_new.shape[0] != B
+            or tuple(k_new.shape[2:]) != (Hkv, d) or n_new.shape[0] != B or lens.shape[0] != B):
+        raise ValueError("append shape mismatch")
+    return dev, B, Hkv, d, k_new.shape[1]
+
+
+def ring_append(k_ring, v_ring, k_new, v_new, n_new, lens, sink, R_w, err=None):
+    """Append n_new[b] rows per sequence to the ring; lens += n_new on the device."""
+    dev, B, Hkv, d, n_max = _append_io(k_ring, v_ring, k_new, v_new, n_new, lens)
+    if k_ring.shape[1] != sink + R_w:
+        raise ValueError("ring must hold sink + R_w rows")
+    st = load_library().wmtp_ring_append(
+        _ptr(k_ring), _ptr(v_ring), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(lens), B, Hkv, d, sink,
+        R_w, n_max, _ptr(err), _stream(dev))
+    _check(st, "wmtp_ring_append")
+
+
+def cache_append(k, v, k_new, v_new, n_new, lens, err=None):
+    """Append n_new[b] rows per sequence to a dense cache; lens += n_new on the device."""
+    dev, B, Hkv, d, n_max = _append_io(k, v, k_new, v_new, n_new, lens)
+    st = load_library().wmtp_cache_append(
+        _ptr(k), _ptr(v), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(lens), B, Hkv, d, k.shape[1],
+        n_max, _ptr(err), _stream(dev))
+    _check(st, "wmtp_cache_append")
+
+
+def select_indices(lens, W, sink, R_w=None, err=None):
+    """Kept positions [B, sink+W] (-1 padded), ring slots (if R_w) and counts [B]."""
+    _need(lens, "lens", torch.int32, 1)
+    dev = lens.device
+    B = lens.shape[0]
+    pos = torch.empty((B, sink + W), dtype=torch.int32, device=dev)
+    slot = None if R_w is None else torch.empty_like(pos)
+    n_sel = torch.empty(B, dtype=torch.int32, device=dev)
+    st = load_library().wmtp_select_indices(
+        _ptr(lens), B, W, sink, W if R_w is None else R_w, _ptr(pos), _ptr(slot), _ptr(n_sel),
+        _ptr(err), _stream(dev))
+    _check(st, "wmtp_select_indices")
+    return pos, slot, n_sel

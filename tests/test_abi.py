@@ -1,0 +1,208 @@
+"""The C ABI on the host: symbols, status codes, workspace sizing and every
+argument check that fires before anything is enqueued.
+
+No compute call is made here (no GPU is needed): every call below is
+rejected by host-side validation, so fake but well-aligned pointer values
+are enough.
+"""
+
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2607_21535_amd import wmtp as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "wmtp.h")
+
+P = 0x10000  # a fake, 256-byte aligned "device pointer" (never dereferenced)
+
+
+def _gpu_present():
+    import torch
+    return torch.cuda.is_available()
+
+
+# The fake pointers above must never reach a real device: if a check were
+# missing, a GPU would run a kernel on them.  These host-validation tests
+# therefore only run where no GPU is visible.
+fake_pointers = pytest.mark.skipif(_gpu_present(), reason="fake-pointer validation tests run without a GPU")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return W.load_library()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(wmtp_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_symbols():
+    assert _declared_functions() == sorted(W.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", W.lib_path()], capture_output=True, text=True)
+    exported = set(re.findall(r"\sT\s+(wmtp_\w+)", out.stdout))
+    for name in _declared_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_abi_version_and_status_strings(lib):
+    assert lib.wmtp_abi_version() == (1 << 16)
+    for code in range(5):
+        assert W.status_string(code).startswith("WMTP_")
+    assert "unknown" in W.status_string(99)
+
+
+def test_workspace_bytes_shapes():
+    full = W.workspace_bytes(W.VARIANT_FULL, 1, 32, 2, 256, 1 << 20)
+    win = W.workspace_bytes(W.VARIANT_WINDOWED, 1, 32, 2, 256, 1 << 20, 2048, 4)
+    ring = W.workspace_bytes(W.VARIANT_RING, 1, 32, 2, 256, 0, 2048, 4)
+    assert full > win > 0
+    assert win == ring  # windowed and ring share one split plan
+    # windowed workspace does not grow with the cache length
+    assert W.workspace_bytes(W.VARIANT_WINDOWED, 1, 32, 2, 256, 1 << 17, 2048, 4) == win
+    assert W.workspace_bytes(W.VARIANT_FULL, 1, 32, 2, 256, 0) == 0
+    assert W.workspace_bytes(W.VARIANT_FULL, 0, 32, 2, 256, 1000) == 0
+    # invalid shapes size to 0
+    assert W.workspace_bytes(W.VARIANT_FULL, 1, 32, 3, 256, 1000) == 0
+    assert W.workspace_bytes(W.VARIANT_FULL, 1, 32, 2, 96, 1000) == 0
+    assert W.workspace_bytes(7, 1, 32, 2, 256, 1000) == 0
+    assert W.workspace_bytes(W.VARIANT_WINDOWED, 1, 32, 2, 256, 1000, 0, 4) == 0
+
+
+def _full(lib, **kw):
+    a = dict(q=P, k=P, v=P, lens=P, out=P, lse=None, B=1, Hq=16, Hkv=2, d=128, S_max=100,
+             scale=0.1, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_draft_attn_full(*a.values())
+
+
+def _win(lib, **kw):
+    a = dict(q=P, k=P, v=P, lens=P, out=P, lse=None, B=1, Hq=16, Hkv=2, d=128, S_max=100, W=8,
+             sink=4, scale=0.1, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_draft_attn_windowed(*a.values())
+
+
+def _ring(lib, **kw):
+    a = dict(q=P, k=P, v=P, lens=P, out=P, lse=None, B=1, Hq=16, Hkv=2, d=128, W=8, sink=4, R_w=8,
+             scale=0.1, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_ring_attn(*a.values())
+
+
+@fake_pointers
+@pytest.mark.parametrize("call", [_full, _win, _ring])
+def test_attention_argument_checks(lib, call):
+    assert call(lib, d=96) == W.EUNSUPPORTED
+    assert call(lib, d=512) == W.EUNSUPPORTED
+    assert call(lib, Hq=64, Hkv=2) == W.EUNSUPPORTED  # G = 32 > 16
+    assert call(lib, d=0) == W.EINVAL
+    assert call(lib, Hq=16, Hkv=3) == W.EINVAL
+    assert call(lib, Hkv=0) == W.EINVAL
+    assert call(lib, B=-1) == W.EINVAL
+    assert call(lib, q=None) == W.EINVAL
+    assert call(lib, k=None) == W.EINVAL
+    assert call(lib, lens=None) == W.EINVAL
+    assert call(lib, out=None) == W.EINVAL
+    assert call(lib, q=P + 2) == W.EINVAL  # bf16 tensors need 16-byte alignment
+    assert call(lib, out=P + 8) == W.EINVAL
+    assert call(lib, lens=P + 2) == W.EINVAL
+    assert call(lib, ws=P + 64) == W.EINVAL  # workspace needs 256-byte alignment
+    assert call(lib, ws=None) == W.EINVAL
+    assert call(lib, ws_bytes=1) == W.EWORKSPACE
+    assert call(lib, scale=float("nan")) == W.EINVAL
+    assert call(lib, scale=float("inf")) == W.EINVAL
+    assert call(lib, B=0, q=None, k=None, v=None, lens=None, out=None) == W.OK  # nothing to do
+
+
+@fake_pointers
+def test_full_specific_checks(lib):
+    assert _full(lib, S_max=-1) == W.EINVAL
+    assert W.workspace_bytes(W.VARIANT_FULL, 1, 16, 2, 128, 0) == 0
+
+
+@fake_pointers
+@pytest.mark.parametrize("call", [_win, _ring])
+def test_window_argument_checks(lib, call):
+    assert call(lib, W=0) == W.EINVAL
+    assert call(lib, W=-3) == W.EINVAL
+    assert call(lib, sink=-1) == W.EINVAL
+
+
+@fake_pointers
+def test_ring_specific_checks(lib):
+    assert _ring(lib, R_w=7) == W.EINVAL  # R_w < W cannot hold the window
+    assert _ring(lib, R_w=0) == W.EINVAL
+
+
+def _rapp(lib, **kw):
+    a = dict(k=P, v=P, kn=P, vn=P, n_new=P, lens=P, B=2, Hkv=2, d=256, sink=4, R_w=16, n_max=8,
+             err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_ring_append(*a.values())
+
+
+def _capp(lib, **kw):
+    a = dict(k=P, v=P, kn=P, vn=P, n_new=P, lens=P, B=2, Hkv=2, d=256, S_max=100, n_max=8,
+             err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_cache_append(*a.values())
+
+
+@fake_pointers
+@pytest.mark.parametrize("call", [_rapp, _capp])
+def test_append_argument_checks(lib, call):
+    assert call(lib, d=96) == W.EUNSUPPORTED
+    assert call(lib, d=-1) == W.EINVAL
+    assert call(lib, Hkv=0) == W.EINVAL
+    assert call(lib, n_max=-1) == W.EINVAL
+    assert call(lib, k=None) == W.EINVAL
+    assert call(lib, lens=None) == W.EINVAL
+    assert call(lib, n_new=None) == W.EINVAL
+    assert call(lib, kn=None) == W.EINVAL
+    assert call(lib, kn=P + 4) == W.EINVAL
+    assert call(lib, lens=P + 1) == W.EINVAL
+    assert call(lib, B=0, k=None, v=None, kn=None, vn=None, n_new=None, lens=None) == W.OK
+
+
+@fake_pointers
+def test_ring_append_specific_checks(lib):
+    assert _rapp(lib, R_w=0) == W.EINVAL
+    assert _rapp(lib, sink=-2) == W.EINVAL
+
+
+@fake_pointers
+def test_cache_append_specific_checks(lib):
+    assert _capp(lib, S_max=-1) == W.EINVAL
+    assert _capp(lib, S_max=1 << 40) == W.EINVAL
+
+
+@fake_pointers
+def test_select_argument_checks(lib):
+    sel = lib.wmtp_select_indices
+    assert sel(P, 2, 0, 4, 8, P, P, P, None, None) == W.EINVAL  # W < 1
+    assert sel(P, 2, 8, -1, 8, P, P, P, None, None) == W.EINVAL
+    assert sel(P, 2, 8, 4, 7, P, P, P, None, None) == W.EINVAL  # slots need R_w >= W
+    assert sel(None, 2, 8, 4, 8, P, P, P, None, None) == W.EINVAL
+    assert sel(P, 2, 8, 4, 8, None, P, P, None, None) == W.EINVAL
+    assert sel(P, 2, 8, 4, 8, P, P, None, None, None) == W.EINVAL
+    assert sel(P + 2, 2, 8, 4, 8, P, P, P, None, None) == W.EINVAL
+    assert sel(P, 0, 8, 4, 8, None, None, None, None, None) == W.OK
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    q = torch.zeros(1, 16, 128, dtype=torch.bfloat16)
+    k = torch.zeros(1, 10, 2, 128, dtype=torch.bfloat16)
+    lens = torch.zeros(1, dtype=torch.int32)
+    with pytest.raises(ValueError, match="HIP device"):
+        W.draft_attn_full(q, k, k, lens)
