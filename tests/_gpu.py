@@ -1,7 +1,11 @@
 """Helpers shared by the GPU parity tests (not collected by pytest).
 
 Parity bar (floating point, all variants):
-  * max |o - o_ref| <= 1e-2 over every output element (the contract);
+  * max |o - o_ref| <= 1e-2 over every output element (the contract) on the
+    five workloads, where |o_ref| < 1; for the small edge cases (a handful
+    of keys, |o_ref| up to ~4) the elementwise bar is
+    max(1e-2, 2^-8 |o_ref| + 1e-4): bf16 output rounding alone moves an
+    element by up to 2^-8 of its magnitude, 1.6e-2 at |o| = 4;
   * per (b, h): ||o - o_ref||_2 <= 5e-3 * ||o_ref||_2.  Rounding the output
     to bfloat16 alone moves each element by at most 2^-8 of its magnitude
     (half an ulp with 8 significant bits), i.e. <= 3.9e-3 normwise; the fp32
@@ -27,6 +31,7 @@ from paper_2607_21535_amd import wmtp as W
 ATOL = 1e-2
 NREL = 5e-3
 LSE_REL = 1e-4
+BF16_REL = 2.0 ** -8
 
 
 def device():
@@ -60,13 +65,14 @@ def oracle_seq(q_bits, k_dev_seq, v_dev_seq, S, scale, variant, W_=None, sink=No
     return A.attend_sequence(q_bits, HostRows(k_dev_seq), HostRows(v_dev_seq), S, scale, mask)
 
 
-def assert_attn_close(out, o_ref, lse=None, lse_ref=None, what=""):
+def assert_attn_close(out, o_ref, lse=None, lse_ref=None, what="", strict=True):
     o = out.detach().float().cpu().numpy().astype(np.float64)
     o_ref = np.asarray(o_ref, dtype=np.float64).reshape(o.shape)
     d = o.shape[-1]
     err = np.abs(o - o_ref)
     assert np.all(np.isfinite(o)), f"{what}: non-finite output"
-    assert err.max() <= ATOL, f"{what}: max abs err {err.max():.3e} > {ATOL}"
+    bound = ATOL if strict else np.maximum(ATOL, BF16_REL * np.abs(o_ref) + 1e-4)
+    assert np.all(err <= bound), f"{what}: max abs err {err.max():.3e} (|o_ref| max {np.abs(o_ref).max():.2f})"
     num = np.linalg.norm((o - o_ref).reshape(-1, d), axis=1)
     den = np.linalg.norm(o_ref.reshape(-1, d), axis=1)
     bad = num > NREL * den
