@@ -36,10 +36,17 @@
 #include "launch.h"
 
 #include <algorithm>
+#include <atomic>
 #include <cstdlib>
+
+#ifndef WMTP_CHUNK_MAX_DEFAULT
+#define WMTP_CHUNK_MAX_DEFAULT 9216
+#endif
 
 namespace wmtp {
 namespace {
+
+constexpr int kMergeThreads = 1024;
 
 struct SplitArgs {
   const uint16_t* q;
@@ -48,13 +55,15 @@ struct SplitArgs {
   const int32_t* lens;
   float* pm;
   float* pl;
+  float* pz;
   float* po;
   int32_t* err;
   int B, Hq, Hkv, G;
   int64_t rows;
   int64_t len_cap;
   int W, sink, R_w;
-  int chunk;
+  int target;     // work items per KV head to aim for
+  int chunk_cap;  // largest item, in keys
   float scale_log2;
 };
 
@@ -62,13 +71,14 @@ struct MergeArgs {
   const int32_t* lens;
   const float* pm;
   const float* pl;
+  const float* pz;
   const float* po;
   uint16_t* out;
   float* lse;
   int32_t* err;
   int B, Hq, Hkv, G;
   int64_t len_cap;
-  int W, sink, chunk;
+  int W, sink, target, chunk_cap;
 };
 
 __device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap, int32_t* err,
@@ -81,22 +91,52 @@ __device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap,
   return S;
 }
 
-// Sequence b owns ceil(n_sel(b) / chunk) consecutive work items.  Wave 0
-// scans the lengths; the result is broadcast through LDS.  Returns false
-// (for the whole workgroup) when `item` lies past the last sequence's items.
+// Work decomposition, derived the same way by every split and merge
+// workgroup from the device-resident lengths (so a captured graph adapts to
+// the lengths of each replay): the item size is the batch's total number of
+// selected keys per KV head divided by `target`, rounded up to a multiple of
+// kChunkQuantum and clamped to [kChunkQuantum, chunk_cap]; sequence b owns
+// ceil(n_sel(b) / chunk) consecutive items.  Runs on one whole wave; every
+// lane returns the same value.
 template <KeyMap M>
-__device__ bool locate_item(const SplitArgs& a, int item, int& b_out, int& c_out, int& S_out) {
-  __shared__ int s_b, s_c, s_S;
+__device__ int wave_chunk(const int32_t* lens, int B, int64_t len_cap, int W, int sink, int target,
+                          int chunk_cap, int32_t* err, bool report) {
+  const int lane = threadIdx.x & (kWave - 1);
+  long long total = 0;
+  for (int base = 0; base < B; base += kWave) {
+    const int b = base + lane;
+    if (b < B) total += selected_count<M>(read_len(lens, b, len_cap, err, report), W, sink);
+  }
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) total += __shfl_xor(total, off);
+  long long c = (total + target - 1) / target;
+  c = (c + kChunkQuantum - 1) / kChunkQuantum * kChunkQuantum;
+  c = c < kChunkQuantum ? kChunkQuantum : (c > chunk_cap ? chunk_cap : c);
+  return static_cast<int>(c);
+}
+
+// Finds the sequence b and local chunk c of work item `item` (wave 0 scans
+// the lengths; the result is broadcast through LDS).  Returns false for the
+// whole workgroup when `item` lies past the last sequence's items.
+template <KeyMap M>
+__device__ bool locate_item(const SplitArgs& a, int item, int& b_out, int& c_out, int& S_out,
+                            int& chunk_out) {
+  __shared__ int s_b, s_c, s_S, s_chunk;
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
-    if (lane == 0) s_b = -1;
+    const int chunk =
+        wave_chunk<M>(a.lens, a.B, a.len_cap, a.W, a.sink, a.target, a.chunk_cap, a.err, true);
+    if (lane == 0) {
+      s_b = -1;
+      s_chunk = chunk;
+    }
     int carry = 0;
     for (int base = 0; base < a.B; base += kWave) {
       const int b = base + lane;
       int S = 0, cnt = 0;
       if (b < a.B) {
-        S = read_len(a.lens, b, a.len_cap, a.err, true);
-        cnt = ceil_div_i(selected_count<M>(S, a.W, a.sink), a.chunk);
+        S = read_len(a.lens, b, a.len_cap, a.err, false);
+        cnt = ceil_div_i(selected_count<M>(S, a.W, a.sink), chunk);
       }
       int incl = cnt;
 #pragma unroll
@@ -118,45 +158,56 @@ __device__ bool locate_item(const SplitArgs& a, int item, int& b_out, int& c_out
   b_out = s_b;
   c_out = s_c;
   S_out = s_S;
+  chunk_out = s_chunk;
   return b_out >= 0;
 }
 
-template <int VW>
-__device__ __forceinline__ void load_words(uint32_t (&dst)[VW], const uint16_t* p) {
-  if constexpr (VW == 8) {
-    const u32x4 x = reinterpret_cast<const u32x4*>(p)[0];
-    const u32x4 y = reinterpret_cast<const u32x4*>(p)[1];
-    dst[0] = x[0]; dst[1] = x[1]; dst[2] = x[2]; dst[3] = x[3];
-    dst[4] = y[0]; dst[5] = y[1]; dst[6] = y[2]; dst[7] = y[3];
-  } else if constexpr (VW == 4) {
-    const u32x4 x = *reinterpret_cast<const u32x4*>(p);
-    dst[0] = x[0]; dst[1] = x[1]; dst[2] = x[2]; dst[3] = x[3];
-  } else {
-    static_assert(VW == 2, "d must be 64, 128 or 256");
-    const u32x2 x = *reinterpret_cast<const u32x2*>(p);
-    dst[0] = x[0]; dst[1] = x[1];
-  }
+#ifndef WMTP_NT_LOADS
+#define WMTP_NT_LOADS 1
+#endif
+
+// Streaming loads of the KV cache (read once per call).
+template <typename T>
+__device__ __forceinline__ T stream_load(const uint16_t* p) {
+#if WMTP_NT_LOADS
+  return __builtin_nontemporal_load(reinterpret_cast<const T*>(p));
+#else
+  return *reinterpret_cast<const T*>(p);
+#endif
 }
 
+// Two waves per SIMD at d = 256 (the kernel fits 256 registers per lane):
+// two workgroups share a CU, so one waits on memory while the other computes.
 template <int D, KeyMap M>
-__global__ __launch_bounds__(kThreads) void split_kernel(SplitArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void split_kernel(SplitArgs a) {
   constexpr int VEC = D / 16;  // d values of one key per lane in the PV operand
   constexpr int VW = VEC / 2;  // ... as 32-bit words
+  // A lane's VEC values come in pieces of SEG contiguous d values (16 bytes at
+  // most); piece s of lane col starts at d = s*16*SEG + SEG*col, so the 16
+  // lanes of one key read 16*SEG contiguous values per load instruction.
+  constexpr int SEG = VEC < 8 ? VEC : 8;
+  constexpr int NSEG = VEC / SEG;
   constexpr int KCH = D / 32;  // 16x16x32 steps over d for the logits
   constexpr int OPAD = kWave + 1;
 
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x / kWave;
+  // Wave-uniform values are moved to scalar registers so that the tile loop
+  // is scalar control flow (exact load/wait accounting, no exec masking).
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int grp = lane >> 4;  // 0..3
   const int col = lane & 15;  // query head (within the group) owned by this lane
   const int g = blockIdx.x % a.Hkv;
   const int item = blockIdx.x / a.Hkv;
 
-  int b, c, S;
-  if (!locate_item<M>(a, item, b, c, S)) return;
+  int b, c, S, chunk;
+  if (!locate_item<M>(a, item, b, c, S, chunk)) return;
+  b = __builtin_amdgcn_readfirstlane(b);
+  c = __builtin_amdgcn_readfirstlane(c);
+  S = __builtin_amdgcn_readfirstlane(S);
+  chunk = __builtin_amdgcn_readfirstlane(chunk);
   const int n_sel = selected_count<M>(S, a.W, a.sink);
-  const int j0 = c * a.chunk;
-  const int j1 = min(j0 + a.chunk, n_sel);
+  const int j0 = c * chunk;
+  const int j1 = min(j0 + chunk, n_sel);
   const RowMap<M> map(S, a.W, a.sink, a.R_w);
   const int64_t rs = static_cast<int64_t>(a.Hkv) * D;  // elements between rows
   const int64_t seq_off = (static_cast<int64_t>(b) * a.rows * a.Hkv + g) * D;
@@ -179,24 +230,41 @@ __global__ __launch_bounds__(kThreads) void split_kernel(SplitArgs a) {
 
   struct Tile {
     u32x4 kx[KCH];       // key (col) : d chunk kk*32 + grp*8
-    uint32_t vx[4][VW];  // key 4*grp + i : d values col*VEC ..
+    uint32_t vx[4][VW];  // key 4*grp + i : NSEG pieces of SEG values
   };
 
-  // Keys past j1 read a valid row (j0) and are masked out of the softmax.
+  const int n_tiles = (j1 - j0 + kTileKeys - 1) / kTileKeys;
+
+  // Keys past j1 read a valid row (j0) and are masked out of the softmax.  A
+  // tile index past the end re-reads the last tile (a cached read): the
+  // pipeline then issues the same loads on every path, so the compiler's
+  // wait counts cover exactly the tile being computed.
   auto load_tile = [&](Tile& T, int t) {
-    const int jt = j0 + t * kTileKeys;
+    const int jt = j0 + min(t, n_tiles - 1) * kTileKeys;
     {
       const int j = jt + col;
       const int r = map.row(j < j1 ? j : j0);
       const uint16_t* p = kbase + static_cast<int64_t>(r) * rs + grp * 8;
 #pragma unroll
-      for (int kk = 0; kk < KCH; ++kk) T.kx[kk] = *reinterpret_cast<const u32x4*>(p + kk * 32);
+      for (int kk = 0; kk < KCH; ++kk) T.kx[kk] = stream_load<u32x4>(p + kk * 32);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = jt + 4 * grp + i;
       const int r = map.row(j < j1 ? j : j0);
-      load_words<VW>(T.vx[i], vbase + static_cast<int64_t>(r) * rs + col * VEC);
+      const uint16_t* p = vbase + static_cast<int64_t>(r) * rs + SEG * col;
+#pragma unroll
+      for (int sg = 0; sg < NSEG; ++sg) {
+        if constexpr (SEG == 8) {
+          const u32x4 x = stream_load<u32x4>(p + sg * 16 * SEG);
+#pragma unroll
+          for (int w = 0; w < 4; ++w) T.vx[i][sg * 4 + w] = x[w];
+        } else {
+          const u32x2 x = stream_load<u32x2>(p + sg * 16 * SEG);
+          T.vx[i][sg * 2] = x[0];
+          T.vx[i][sg * 2 + 1] = x[1];
+        }
+      }
     }
   };
 
@@ -204,7 +272,8 @@ __global__ __launch_bounds__(kThreads) void split_kernel(SplitArgs a) {
 #pragma unroll
   for (int e = 0; e < VEC; ++e) acc[e] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = neg_inf();
-  float l_run = 0.f;
+  float l_run = 0.f;  // sum of the bf16-rounded weights (normalises the output)
+  float z_run = 0.f;  // sum of the fp32 weights (the log-sum-exp)
   const float sl2 = a.scale_log2;
 
   auto compute_tile = [&](const Tile& T, int t) {
@@ -229,53 +298,65 @@ __global__ __launch_bounds__(kThreads) void split_kernel(SplitArgs a) {
     if (__any(m_new > m_run)) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
+      z_run *= alpha;
 #pragma unroll
       for (int e = 0; e < VEC; ++e) acc[e] *= alpha;
     }
     m_run = m_new;
-    float pv[4];
+    // P^T operand: the weights of keys 4*grp + i for head col, rounded to
+    // bf16; the denominator sums the same rounded weights.
+    uint32_t pb[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      pv[i] = __builtin_amdgcn_exp2f(sv[i] - m_run);
-      l_run += pv[i];
+    for (int i = 0; i < 2; ++i) {
+      const float p0 = __builtin_amdgcn_exp2f(sv[2 * i] - m_run);
+      const float p1 = __builtin_amdgcn_exp2f(sv[2 * i + 1] - m_run);
+      pb[i] = uint32_t(f32_to_bf16_rne(p0)) | (uint32_t(f32_to_bf16_rne(p1)) << 16);
+      l_run += bf16_lo(pb[i]) + bf16_hi(pb[i]);
+      z_run += p0 + p1;
     }
+    const bf16x4 pop = __builtin_bit_cast(bf16x4, u32x2{pb[0], pb[1]});
+    // V^T operand for output tile e: this lane's four keys at its value
+    // column e, packed from the loaded rows (low or high halves of a word).
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        const uint32_t w = T.vx[i][e >> 1];
-        const float vf = (e & 1) ? bf16_hi(w) : bf16_lo(w);
-        acc[e] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf, pv[i], acc[e], 0, 0, 0);
-      }
+    for (int e = 0; e < VEC; ++e) {
+      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+      const uint32_t a01 = __builtin_amdgcn_perm(T.vx[1][e >> 1], T.vx[0][e >> 1], sel);
+      const uint32_t a23 = __builtin_amdgcn_perm(T.vx[3][e >> 1], T.vx[2][e >> 1], sel);
+      acc[e] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, u32x2{a01, a23}),
+                                                        pop, acc[e], 0, 0, 0);
     }
   };
 
-  // Two register buffers: the next tile's loads are in flight while the
-  // current tile is computed.
-  const int n_tiles = (j1 - j0 + kTileKeys - 1) / kTileKeys;
+  // Two register buffers: the loads of this wave's next tile are in flight
+  // while the current one is computed.  The loop body is straight-line (a
+  // past-the-end prefetch re-reads the last tile), so the wait before each
+  // tile covers exactly that tile's loads.
+  const int my_tiles = n_tiles > wave ? (n_tiles - wave + kWaves - 1) / kWaves : 0;
   Tile T0, T1;
-  int t = wave;
-  if (t < n_tiles) load_tile(T0, t);
-  while (t < n_tiles) {
-    const int t1 = t + kWaves;
-    if (t1 < n_tiles) load_tile(T1, t1);
+  load_tile(T0, wave);
+  int i = 0;
+  for (; i + 2 <= my_tiles; i += 2) {
+    const int t = wave + i * kWaves;
+    load_tile(T1, t + kWaves);
     compute_tile(T0, t);
-    if (t1 >= n_tiles) break;
-    const int t2 = t1 + kWaves;
-    if (t2 < n_tiles) load_tile(T0, t2);
-    compute_tile(T1, t1);
-    t = t2;
+    load_tile(T0, t + 2 * kWaves);
+    compute_tile(T1, t + kWaves);
   }
+  if (i < my_tiles) compute_tile(T0, wave + i * kWaves);
 
   // ---- combine the four waves: (m, l) per head, then O in wave order ----
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
+  z_run += __shfl_xor(z_run, 16);
+  z_run += __shfl_xor(z_run, 32);
   __shared__ float s_m[kWaves][16];
   __shared__ float s_l[kWaves][16];
+  __shared__ float s_z[kWaves][16];
   __shared__ float s_o[(D / 4) * OPAD];
   if (grp == 0) {
     s_m[wave][col] = m_run;
     s_l[wave][col] = l_run;
+    s_z[wave][col] = z_run;
   }
   __syncthreads();
   float Mx = neg_inf();
@@ -284,6 +365,9 @@ __global__ __launch_bounds__(kThreads) void split_kernel(SplitArgs a) {
   float Lx = 0.f;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) Lx += s_l[w][col] * __builtin_amdgcn_exp2f(s_m[w][col] - Mx);
+  float Zx = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) Zx += s_z[w][col] * __builtin_amdgcn_exp2f(s_m[w][col] - Mx);
   const float f = __builtin_amdgcn_exp2f(m_run - Mx);  // 0 for a wave with no tile
   for (int w = 0; w < kWaves; ++w) {
     if (wave == w) {
@@ -300,48 +384,65 @@ __global__ __launch_bounds__(kThreads) void split_kernel(SplitArgs a) {
     __syncthreads();
   }
 
-  // Partial row of (item, g): pm/pl [G], po [G, D].  Lane l of any wave held
-  // head l&15, d = VEC*(4*(l>>4) + jj) + e.
+  // Partial row (item, g) = blockIdx.x: pm/pl/pz [G], po [G, D].  acc[e][jj] of
+  // lane l in any wave held head l&15 and
+  // d = (e/SEG)*16*SEG + SEG*(4*(l>>4) + jj) + e%SEG.
   const int64_t pidx = blockIdx.x;
   if (threadIdx.x < 16 && col < a.G) {
     a.pm[pidx * a.G + col] = Mx;
     a.pl[pidx * a.G + col] = Lx;
+    a.pz[pidx * a.G + col] = Zx;
   }
   float* po = a.po + pidx * a.G * D;
   for (int idx = threadIdx.x; idx < a.G * D; idx += kThreads) {
     const int h = idx / D;
     const int d = idx % D;
-    const int gq = d / (4 * VEC);
-    const int rem = d % (4 * VEC);
-    const int jj = rem / VEC;
-    const int e = rem % VEC;
+    const int sg = d / (16 * SEG);
+    const int rem = d % (16 * SEG);
+    const int r = rem / SEG;  // MFMA output row: r = 4*gq + jj
+    const int e = sg * SEG + rem % SEG;
+    const int gq = r / 4;
+    const int jj = r % 4;
     po[idx] = s_o[(e * 4 + jj) * OPAD + gq * 16 + h];
   }
 }
 
-// One workgroup per (b, h, 64-wide slice of d).  Items of sequence b are
-// combined in a fixed order: wave w takes items w, w+4, ...; then waves 0..3.
-template <int D, KeyMap M>
-__global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x / kWave;
+// One workgroup of NT threads per (b, h, SLICE-wide slice of d).  Thread t
+// owns float4 column q4 = t % (SLICE/4) of the slice and item slot
+// t / (SLICE/4); the slots walk the sequence's items (several loads in flight
+// per thread), then are summed by a fixed-order tree in LDS, so the result
+// does not depend on timing.  Two shapes: 1024 threads on 64-wide slices for
+// sequences with many items (one long sequence), 256 threads on whole rows
+// when items per sequence are few (many short windows).
+template <int D, KeyMap M, int NT, int SLICE>
+__global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
+  constexpr int Q = SLICE / 4;  // float4 columns per slice
+  constexpr int NS = NT / Q;    // item slots
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int q4 = tid % Q;
+  const int slot = tid / Q;
   const int b = blockIdx.x / a.Hq;
   const int h = blockIdx.x % a.Hq;
   const int g = h / a.G;
   const int hl = h % a.G;
-  const int d = blockIdx.y * kWave + lane;
+  const int d0 = blockIdx.y * SLICE + 4 * q4;
 
   __shared__ int s_base, s_cnt;
-  __shared__ float s_red[4];
-  __shared__ float s_o[4][kWave];
-  __shared__ float s_L[4];
-  if (threadIdx.x < kWave) {
+  __shared__ float s_red[NT / kWave];
+  __shared__ floatx4 s_o[NS][Q];
+  __shared__ float s_L[NS];
+  __shared__ float s_Z[NS];
+  if (tid < kWave) {
+    const int chunk =
+        wave_chunk<M>(a.lens, a.B, a.len_cap, a.W, a.sink, a.target, a.chunk_cap, a.err, false);
     int before = 0, mine = 0;
     for (int base = 0; base <= b; base += kWave) {
       const int bb = base + lane;
       if (bb <= b) {
         const int S = read_len(a.lens, bb, a.len_cap, a.err, false);
-        const int cnt = ceil_div_i(selected_count<M>(S, a.W, a.sink), a.chunk);
+        const int cnt = ceil_div_i(selected_count<M>(S, a.W, a.sink), chunk);
         if (bb < b) before += cnt; else mine = cnt;
       }
     }
@@ -358,34 +459,58 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
   __syncthreads();
   const int base = s_base;
   const int n = s_cnt;
+  auto prow = [&](int c) { return (static_cast<int64_t>(base + c) * a.Hkv + g) * a.G + hl; };
 
   // Largest partial maximum.
   float mx = neg_inf();
-  for (int c = threadIdx.x; c < n; c += 256)
-    mx = fmaxf(mx, a.pm[(static_cast<int64_t>(base + c) * a.Hkv + g) * a.G + hl]);
+  for (int c = tid; c < n; c += NT) mx = fmaxf(mx, a.pm[prow(c)]);
 #pragma unroll
   for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
   if (lane == 0) s_red[wave] = mx;
   __syncthreads();
-  const float Mx = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
+  float Mx = s_red[0];
+#pragma unroll
+  for (int w = 1; w < NT / kWave; ++w) Mx = fmaxf(Mx, s_red[w]);
 
-  float o = 0.f, L = 0.f;
-  for (int c = wave; c < n; c += 4) {
-    const int64_t pr = (static_cast<int64_t>(base + c) * a.Hkv + g) * a.G + hl;
+  floatx4 o = {0.f, 0.f, 0.f, 0.f};
+  float L = 0.f, Z = 0.f;
+#pragma unroll 8
+  for (int c = slot; c < n; c += NS) {
+    const int64_t pr = prow(c);
     const float w = __builtin_amdgcn_exp2f(a.pm[pr] - Mx);
-    o += w * a.po[pr * D + d];
+    const floatx4 v = *reinterpret_cast<const floatx4*>(a.po + pr * D + d0);
+    o += w * v;
     L += w * a.pl[pr];
+    Z += w * a.pz[pr];
   }
-  s_o[wave][lane] = o;
-  if (lane == 0) s_L[wave] = L;
+  s_o[slot][q4] = o;
+  if (q4 == 0) {
+    s_L[slot] = L;
+    s_Z[slot] = Z;
+  }
   __syncthreads();
-  if (wave == 0) {
-    const float ot = ((s_o[0][lane] + s_o[1][lane]) + s_o[2][lane]) + s_o[3][lane];
-    const float Lt = ((s_L[0] + s_L[1]) + s_L[2]) + s_L[3];
-    const float r = n > 0 ? ot / Lt : 0.f;
-    a.out[(static_cast<int64_t>(b) * a.Hq + h) * D + d] = f32_to_bf16_rne(r);
-    if (a.lse != nullptr && blockIdx.y == 0 && lane == 0)
-      a.lse[static_cast<int64_t>(b) * a.Hq + h] = n > 0 ? (Mx + log2f(Lt)) * kLn2 : neg_inf();
+#pragma unroll
+  for (int half = NS / 2; half > 0; half >>= 1) {
+    if (slot < half) {
+      s_o[slot][q4] += s_o[slot + half][q4];
+      if (q4 == 0) {
+        s_L[slot] += s_L[slot + half];
+        s_Z[slot] += s_Z[slot + half];
+      }
+    }
+    __syncthreads();
+  }
+  if (slot == 0) {
+    const float Lt = s_L[0];
+    const floatx4 ot = s_o[0][q4];
+    float r[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = n > 0 ? ot[i] / Lt : 0.f;
+    const uint32_t lo = f32_to_bf16_rne(r[0]) | (uint32_t(f32_to_bf16_rne(r[1])) << 16);
+    const uint32_t hi = f32_to_bf16_rne(r[2]) | (uint32_t(f32_to_bf16_rne(r[3])) << 16);
+    *reinterpret_cast<u32x2*>(a.out + (static_cast<int64_t>(b) * a.Hq + h) * D + d0) = u32x2{lo, hi};
+    if (a.lse != nullptr && blockIdx.y == 0 && q4 == 0)
+      a.lse[static_cast<int64_t>(b) * a.Hq + h] = n > 0 ? (Mx + log2f(s_Z[0])) * kLn2 : neg_inf();
   }
 }
 
@@ -395,21 +520,29 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   if (L.max_items > 0) {
     SplitArgs a;
     a.q = L.q; a.k = L.k; a.v = L.v; a.lens = L.lens;
-    a.pm = L.pm; a.pl = L.pl; a.po = L.po; a.err = L.err;
+    a.pm = L.pm; a.pl = L.pl; a.pz = L.pz; a.po = L.po; a.err = L.err;
     a.B = L.B; a.Hq = L.Hq; a.Hkv = L.Hkv; a.G = G;
     a.rows = L.rows; a.len_cap = L.len_cap;
-    a.W = L.W; a.sink = L.sink; a.R_w = L.R_w; a.chunk = L.chunk;
+    a.W = L.W; a.sink = L.sink; a.R_w = L.R_w;
+    a.target = L.target; a.chunk_cap = L.chunk_cap;
     a.scale_log2 = L.scale * kLog2e;
     const dim3 grid(static_cast<unsigned>(L.max_items) * static_cast<unsigned>(L.Hkv));
     hipLaunchKernelGGL((split_kernel<D, M>), grid, dim3(kThreads), 0, st, a);
   }
+  // Items per sequence the plan allows decide the merge shape.
+  const bool wide = L.max_items >= 32 * L.B;
   MergeArgs m;
-  m.lens = L.lens; m.pm = L.pm; m.pl = L.pl; m.po = L.po;
+  m.lens = L.lens; m.pm = L.pm; m.pl = L.pl; m.pz = L.pz; m.po = L.po;
   m.out = L.out; m.lse = L.lse; m.err = L.err;
   m.B = L.B; m.Hq = L.Hq; m.Hkv = L.Hkv; m.G = G;
-  m.len_cap = L.len_cap; m.W = L.W; m.sink = L.sink; m.chunk = L.chunk;
-  const dim3 grid2(static_cast<unsigned>(L.B) * static_cast<unsigned>(L.Hq), D / kWave);
-  hipLaunchKernelGGL((merge_kernel<D, M>), grid2, dim3(256), 0, st, m);
+  m.len_cap = L.len_cap; m.W = L.W; m.sink = L.sink;
+  m.target = L.target; m.chunk_cap = L.chunk_cap;
+  const unsigned bh = static_cast<unsigned>(L.B) * static_cast<unsigned>(L.Hq);
+  if (wide)
+    hipLaunchKernelGGL((merge_kernel<D, M, kMergeThreads, 64>), dim3(bh, D / 64), dim3(kMergeThreads), 0,
+                       st, m);
+  else
+    hipLaunchKernelGGL((merge_kernel<D, M, 256, D>), dim3(bh, 1), dim3(256), 0, st, m);
   return hipGetLastError();
 }
 
@@ -431,25 +564,73 @@ int env_int(const char* name, int dflt) {
 
 }  // namespace
 
+// Split workgroups the current device keeps resident at once: CUs times the
+// workgroups per CU the compiled kernel for head size d allows.  Queried once
+// per device and head size; without a visible device, the MI355X figure
+// (256 CUs, two workgroups each at d = 256).
+constexpr int kMaxDevices = 64;
+
+template <int D>
+int query_resident_groups(int dev) {
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, split_kernel<D, KeyMap::Full>, kThreads,
+                                                   0) != hipSuccess)
+    return 0;
+  return cus * per_cu;
+}
+
+int resident_split_groups(int d) {
+  static std::atomic<int> cache[kMaxDevices][3];
+  const int fallback = 256 * (d == 256 ? 2 : d == 128 ? 3 : 6);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return fallback;
+  }
+  const int k = d == 64 ? 0 : (d == 128 ? 1 : 2);
+  int v = cache[dev][k].load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  v = d == 64 ? query_resident_groups<64>(dev)
+              : (d == 128 ? query_resident_groups<128>(dev) : query_resident_groups<256>(dev));
+  if (v <= 0) {
+    (void)hipGetLastError();
+    v = fallback;
+  }
+  cache[dev][k].store(v, std::memory_order_relaxed);
+  return v;
+}
+
 SplitPlan plan_split(int B, int Hq, int Hkv, int d, int64_t n_keys_max) {
-  // Aim for about kTargetItems workgroups in total (several per CU on a
-  // 256-CU part) with items of at most kChunkMax keys, so that long sequences
-  // get many items and short ones still spread over the chip.
-  static const int target = env_int("WMTP_TARGET_ITEMS", 1024);
-  static const int chunk_max =
-      std::max(kChunkQuantum, env_int("WMTP_CHUNK_MAX", 2048) / kChunkQuantum * kChunkQuantum);
+  // Aim for as many workgroups as the device keeps resident (one balanced
+  // round: 512 on MI355X at d = 256) with items of at most `chunk_max`
+  // keys, so that a long single
+  // sequence runs in one balanced round and many or variable-length
+  // sequences are cut finely enough to pack without a long tail.  Fewer
+  // items also mean fewer partials for the merge.  The kernels pick the item
+  // size from the actual lengths; the workspace covers every choice they can
+  // make: with per-head target T and chunk in [quantum, chunk_max], the item
+  // count is at most min(B*ceil(n/quantum), max(T + B, B*ceil(n/chunk_max))).
+  static const int target_env = env_int("WMTP_TARGET_ITEMS", 0);
+  static const int chunk_max = std::max(
+      kChunkQuantum, env_int("WMTP_CHUNK_MAX", WMTP_CHUNK_MAX_DEFAULT) / kChunkQuantum * kChunkQuantum);
   SplitPlan p{};
-  const int64_t groups = std::max<int64_t>(1, static_cast<int64_t>(B) * Hkv);
-  const int64_t per_seq = std::max<int64_t>(1, (target + groups - 1) / groups);
-  int64_t chunk = (std::max<int64_t>(n_keys_max, 1) + per_seq - 1) / per_seq;
-  chunk = (chunk + kChunkQuantum - 1) / kChunkQuantum * kChunkQuantum;
-  chunk = std::min<int64_t>(std::max<int64_t>(chunk, kChunkQuantum), chunk_max);
-  p.chunk = static_cast<int>(chunk);
-  p.max_items = n_keys_max > 0 ? static_cast<int>(B * ((n_keys_max + chunk - 1) / chunk)) : 0;
+  const int64_t wgs = target_env > 0 ? target_env : resident_split_groups(d);
+  const int64_t T = std::max<int64_t>(1, wgs / std::max(Hkv, 1));
+  p.target = static_cast<int>(std::min<int64_t>(T, INT32_MAX / 2));
+  p.chunk_cap = chunk_max;
+  int64_t items = 0;
+  if (n_keys_max > 0) {
+    const int64_t fine = static_cast<int64_t>(B) * ((n_keys_max + kChunkQuantum - 1) / kChunkQuantum);
+    const int64_t coarse = static_cast<int64_t>(B) * ((n_keys_max + chunk_max - 1) / chunk_max);
+    items = std::min(fine, std::max(T + B, coarse));
+  }
+  p.max_items = static_cast<int>(std::min<int64_t>(items, INT32_MAX));
   const size_t rows = static_cast<size_t>(p.max_items) * Hkv * (Hq / Hkv);
   auto up = [](size_t x) { return (x + 255) / 256 * 256; };
   p.off_pl = up(rows * sizeof(float));
-  p.off_po = p.off_pl + up(rows * sizeof(float));
+  p.off_pz = p.off_pl + up(rows * sizeof(float));
+  p.off_po = p.off_pz + up(rows * sizeof(float));
   p.bytes = rows ? p.off_po + up(rows * static_cast<size_t>(d) * sizeof(float)) : 0;
   return p;
 }

@@ -22,18 +22,22 @@ struct AttnLaunch {
   int W, sink, R_w;
   float scale;
   // split plan (from plan_split)
-  int chunk;
+  int target;     // work items per KV head to aim for
+  int chunk_cap;  // largest work item, in keys
   int max_items;  // work items per KV head, upper bound over all lengths
   float* pm;
   float* pl;
+  float* pz;
   float* po;
 };
 
 struct SplitPlan {
-  int chunk;       // keys per work item (multiple of kChunkQuantum)
-  int max_items;   // B * ceil(n_keys_max / chunk)
+  int target;      // work items per KV head to aim for
+  int chunk_cap;   // largest work item, in keys (multiple of kChunkQuantum)
+  int max_items;   // most work items per KV head for any lengths
   size_t bytes;    // workspace bytes
   size_t off_pl;   // byte offsets of the partial arrays inside the workspace
+  size_t off_pz;
   size_t off_po;
 };
 

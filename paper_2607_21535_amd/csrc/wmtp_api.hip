@@ -94,11 +94,13 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   L.sink = sink;
   L.R_w = R_w;
   L.scale = scale;
-  L.chunk = plan.chunk;
+  L.target = plan.target;
+  L.chunk_cap = plan.chunk_cap;
   L.max_items = plan.max_items;
   char* base = static_cast<char*>(ws);
   L.pm = reinterpret_cast<float*>(base);
   L.pl = reinterpret_cast<float*>(base + plan.off_pl);
+  L.pz = reinterpret_cast<float*>(base + plan.off_pz);
   L.po = reinterpret_cast<float*>(base + plan.off_po);
   if (wmtp::launch_attention(L, static_cast<hipStream_t>(stream)) != hipSuccess)
     return WMTP_ELAUNCH;
