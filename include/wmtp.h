@@ -32,9 +32,11 @@
  *     the current draft token's row.  A length outside its valid range is
  *     clamped on the device and WMTP_DERR_* bits are OR-ed into *err when
  *     `err` is not NULL.
- *   - Arithmetic: bf16 inputs, fp32 logits / softmax / accumulation, bf16
+ *   - Arithmetic: bf16 inputs, fp32 logits, softmax and accumulation; the
+ *     softmax weights enter the weight-times-value product rounded to bf16
+ *     and the output is normalised by the sum of those rounded weights; bf16
  *     output rounded to nearest even; lse (optional) is the natural-log
- *     log-sum-exp of the scaled logits in fp32.  An empty sequence (no keys)
+ *     log-sum-exp of the scaled logits from the fp32 weights.  An empty sequence (no keys)
  *     gives out = 0 and lse = -inf.
  *   - Results are deterministic: no atomics take part in any reduction.
  */
@@ -71,8 +73,9 @@ typedef enum {
 
 /*
  * Workspace (device bytes) that one attention call of the given variant and
- * shape needs for its split-K partial results (per split and query head: the
- * running maximum, the softmax denominator and the unnormalised output row).
+ * shape needs for its split-K partial results (per work item and query head:
+ * the running maximum, two softmax denominators and the unnormalised output
+ * row, in fp32), sized for the current device.
  * S_max is the dense cache capacity (ignored for the ring); W and sink are
  * ignored for the full variant.  Returns 0 for arguments the attention calls
  * would reject.  The workspace needs no initialisation and may be reused by

@@ -8,23 +8,27 @@
 // index_map.h; no index table is built.
 //
 // Work decomposition.  Sequence b attends n_sel(b) keys, cut into work items
-// of `chunk` keys; the items of all sequences are numbered consecutively (a
-// prefix sum over the device-resident lengths, so variable-length batches
-// pack without holes) and one 256-thread workgroup handles one (item, KV
-// head).  The four waves of a workgroup take interleaved 16-key tiles, so the
-// group streams one contiguous key range.
+// whose size the kernels derive on the device from the batch's total
+// selected keys (so a captured graph adapts to the lengths of each replay);
+// the items of all sequences are numbered consecutively (a prefix sum over
+// the device-resident lengths, so variable-length batches pack without
+// holes) and one 256-thread workgroup handles one (item, KV head).  The four
+// waves of a workgroup take interleaved 16-key tiles, so the group streams
+// one contiguous key range.
 //
 // Per 16-key tile, on one wave:
 //   S^T[16 keys, 16 heads] = K_tile . Q^T   v_mfma_f32_16x16x32_bf16, d/32 steps
 //   online softmax per head in the exp2 domain (scale * log2 e folded into the
-//   fp32 logits); the head's running maximum is shared by the four lanes that
-//   hold its 16 scores (two xor shuffles)
-//   O^T[d, heads] += V^T . P^T              v_mfma_f32_16x16x4f32, P kept in fp32
-// The orientation puts a query head on the same lane in the scores and in the
-// output accumulator, so rescaling by exp2(m_old - m_new) is lane-local, and
-// it lets every lane read its V operand as one contiguous run of d/16
-// values of a single key (16 lanes cover one 2*d-byte row: coalesced).
-// The four waves combine their (m, l, O) through LDS in a fixed order, and the
+//   fp32 logits); a head's 16 scores sit in four lanes (two xor shuffles)
+//   O^T[d, heads] += V^T . P^T              v_mfma_f32_16x16x16_bf16, d/16 steps
+// In this orientation a query head sits on the same lane in the scores and
+// in the output accumulator (rescaling is lane-local), and each lane already
+// holds, for every value column it loaded, the four keys its lane group
+// contributes to the PV product: two byte permutes build the MFMA operand,
+// with no transpose through LDS.  P is rounded to bf16 for that product; the
+// output is normalised by the sum of the same rounded weights, and the
+// log-sum-exp uses the fp32 weights.
+// The four waves combine their state through LDS in a fixed order, and the
 // merge kernel combines the items of a sequence in a fixed order: results are
 // bitwise reproducible.
 //
