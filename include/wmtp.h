@@ -60,8 +60,8 @@ typedef enum {
 } wmtp_status;
 
 /* Device error bits, OR-ed into *err by the kernels. */
-#define WMTP_DERR_LEN_RANGE 0x1  /* lens[b] < 0, or > S_max for a dense cache: clamped */
-#define WMTP_DERR_NNEW_RANGE 0x2 /* n_new[b] outside [0, n_max]: clamped */
+#define WMTP_DERR_LEN_RANGE 0x1  /* lens[b] < 0, > S_max for a dense cache, or < n_q[b]: clamped */
+#define WMTP_DERR_NNEW_RANGE 0x2 /* n_new[b] outside [0, n_max] (n_q[b] outside [0, q_max]): clamped */
 #define WMTP_DERR_CAPACITY 0x4   /* dense-cache append past S_max: extra rows dropped */
 
 /* Attention variants, for wmtp_workspace_bytes(). */
@@ -76,8 +76,9 @@ typedef enum {
  * shape needs for its split-K partial results (per work item and query head:
  * the running maximum, two softmax denominators and the unnormalised output
  * row, in fp32), sized for the current device.
- * S_max is the dense cache capacity (ignored for the ring); W and sink are
- * ignored for the full variant.  Returns 0 for arguments the attention calls
+ * B counts query rows: the batch for the single-row calls, B * q_max for the
+ * extend calls.  S_max is the dense cache capacity (ignored for the ring); W
+ * and sink are ignored for the full variant.  Returns 0 for arguments the attention calls
  * would reject.  The workspace needs no initialisation and may be reused by
  * successive calls on one stream.
  */
@@ -134,6 +135,36 @@ int wmtp_draft_attn_windowed(const void* q, const void* k, const void* v, const 
 int wmtp_ring_attn(const void* q, const void* k_ring, const void* v_ring, const int32_t* lens,
                    void* out, float* lse, int B, int Hq, int Hkv, int d, int W, int sink, int R_w,
                    float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream);
+
+/*
+ * Draft-extend attention: several new query rows per sequence, attending
+ * causally (the draft forward over the accepted tokens after a verify step;
+ * "draft-extend attn" in the kernel attribution table, Appendix B, and the
+ * discussion of ragged extend in Section 6 "The backend is not the confound").
+ *   q, out  [B, q_max, Hq, d] bf16;  lse [B, q_max, Hq] fp32 or NULL
+ *   lens    [B] int32 device: cached rows of sequence b INCLUDING its new rows
+ *   n_q     [B] int32 device, 1..q_max: new rows of sequence b (NULL: q_max)
+ * Row t < n_q[b] of sequence b attends the first lens[b] - n_q[b] + t + 1
+ * cached rows -- the full context, or under the window rule applied at that
+ * length (its own sink + last W); rows t >= n_q[b] give out = 0 and
+ * lse = -inf.  A draft decode step is the case q_max = 1.  The ring variant
+ * needs R_w >= W + q_max - 1 so that the earliest row's window is resident
+ * (the paper's chain sizing R_w = W + gamma + 1 covers q_max = gamma + 1).
+ * Workspace: wmtp_workspace_bytes(variant, B * q_max, ...).  Other arguments
+ * and conventions as for the single-row calls.
+ */
+int wmtp_draft_extend_full(const void* q, const void* k, const void* v, const int32_t* lens,
+                           const int32_t* n_q, void* out, float* lse, int B, int q_max, int Hq,
+                           int Hkv, int d, int64_t S_max, float scale, void* ws, size_t ws_bytes,
+                           int32_t* err, void* stream);
+int wmtp_draft_extend_windowed(const void* q, const void* k, const void* v, const int32_t* lens,
+                               const int32_t* n_q, void* out, float* lse, int B, int q_max, int Hq,
+                               int Hkv, int d, int64_t S_max, int W, int sink, float scale,
+                               void* ws, size_t ws_bytes, int32_t* err, void* stream);
+int wmtp_ring_extend(const void* q, const void* k_ring, const void* v_ring, const int32_t* lens,
+                     const int32_t* n_q, void* out, float* lse, int B, int q_max, int Hq, int Hkv,
+                     int d, int W, int sink, int R_w, float scale, void* ws, size_t ws_bytes,
+                     int32_t* err, void* stream);
 
 /*
  * Append draft KV rows to the ring store (the draft forward writes the K/V

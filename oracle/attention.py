@@ -15,6 +15,11 @@ What is computed (Windowed-MTP paper):
     keys per step.
   * The native (full-context) draft attends all S cached keys (Section 3,
     "Per-step latency model"; Figure "window").
+  * Draft-extend (the draft forward over several accepted tokens after a
+    verify step; Appendix B kernel attribution table, Section 6 "The backend
+    is not the confound"): each new row is an autoregressive decode step of
+    its own -- the token at position p sees positions [0, p] -- with the
+    selection rule applied at that row's length.
 
 Everything else is the textbook single-query softmax attention, written out:
     z_p = scale * <q_h, k_p>            for kept positions p
@@ -50,6 +55,8 @@ __all__ = [
     "n_selected",
     "attend_sequence",
     "attend_batch",
+    "extend_lengths",
+    "attend_extend",
 ]
 
 # Keys processed per chunk when forming logits and the value sum.
@@ -173,3 +180,35 @@ def attend_batch(q, K, V, lens, scale: float, variant: str = "full",
         outs.append(o)
         lses.append(lse)
     return np.stack(outs), np.stack(lses)
+
+
+def extend_lengths(S: int, n: int, q_max: int):
+    """Visible length of each new query row in a draft-extend call.
+
+    Autoregressive attention over n new rows appended at the end of a
+    sequence that now holds S rows: row t (0-based among the new rows) is
+    the token at position S - n + t and sees positions [0, S - n + t + 1).
+    Rows t >= n (padding up to q_max) see nothing.
+    """
+    return [S - n + t + 1 if t < n else 0 for t in range(q_max)]
+
+
+def attend_extend(q_rows, K, V, S: int, n: int, scale: float, variant: str = "full",
+                  W: int | None = None, sink: int | None = None):
+    """Draft-extend attention of one sequence: q_rows [q_max, Hq, d].
+
+    Each new row attends causally; under the windowed variant each row
+    applies the sink + window rule at its own length (Section 4 "Mechanism",
+    Appendix A pseudocode, with S the row's own length).
+    Returns (o [q_max, Hq, d], lse [q_max, Hq]); padding rows give 0 / -inf.
+    """
+    q_rows = np.asarray(q_rows)
+    q_max, Hq, d = q_rows.shape
+    o = np.zeros((q_max, Hq, d))
+    lse = np.full((q_max, Hq), -np.inf)
+    for t, L in enumerate(extend_lengths(S, n, q_max)):
+        if L <= 0:
+            continue
+        mask = None if variant == "full" else window_mask(L, W, sink)
+        o[t], lse[t] = attend_sequence(q_rows[t], K, V, L, scale, mask)
+    return o, lse

@@ -62,7 +62,9 @@ struct SplitArgs {
   float* pz;
   float* po;
   int32_t* err;
+  const int32_t* n_q;  // new query rows per sequence (NULL: all qps rows)
   int B, Hq, Hkv, G;
+  int qps;             // query rows per sequence; NV = B * qps query rows in all
   int64_t rows;
   int64_t len_cap;
   int W, sink, R_w;
@@ -80,7 +82,9 @@ struct MergeArgs {
   uint16_t* out;
   float* lse;
   int32_t* err;
+  const int32_t* n_q;
   int B, Hq, Hkv, G;
+  int qps;
   int64_t len_cap;
   int W, sink, target, chunk_cap;
 };
@@ -95,21 +99,55 @@ __device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap,
   return S;
 }
 
+// Query row v = b * qps + t is row t of sequence b.  lens[b] counts every
+// cached row, including the n new rows of this call (n = n_q[b], or qps when
+// n_q is NULL); row t attends causally: it sees the first lens[b] - n + t + 1
+// rows (the draft decode step is the case qps = n = 1).  Rows t >= n, and
+// every row of an empty sequence, have no keys; a non-empty sequence with
+// fewer rows than n is flagged.  Returns that length; `b_out` receives the
+// sequence.
+__device__ __forceinline__ int visible_len(const int32_t* lens, const int32_t* n_q, int qps,
+                                           int64_t cap, int32_t* err, int v, bool report,
+                                           int& b_out) {
+  const int b = qps == 1 ? v : v / qps;
+  const int t = v - b * qps;
+  b_out = b;
+  const int S = read_len(lens, b, cap, err, report);
+  int n = qps;
+  if (n_q != nullptr) {
+    n = n_q[b];
+    if (n < 0 || n > qps) {
+      if (report) raise_error(err, WMTP_DERR_NNEW_RANGE);
+      n = n < 0 ? 0 : qps;
+    }
+  }
+  if (t >= n || S == 0) return 0;  // padding row, or an empty (padding) sequence
+  const int L = S - n + t + 1;
+  if (L < 1) {  // fewer cached rows than new query rows
+    if (report) raise_error(err, WMTP_DERR_LEN_RANGE);
+    return 0;
+  }
+  return L;
+}
+
 // Work decomposition, derived the same way by every split and merge
 // workgroup from the device-resident lengths (so a captured graph adapts to
 // the lengths of each replay): the item size is the batch's total number of
 // selected keys per KV head divided by `target`, rounded up to a multiple of
 // kChunkQuantum and clamped to [kChunkQuantum, chunk_cap]; sequence b owns
-// ceil(n_sel(b) / chunk) consecutive items.  Runs on one whole wave; every
+// ceil(n_sel(b) / chunk) consecutive items (per query row, see
+// visible_len).  Runs on one whole wave; every
 // lane returns the same value.
 template <KeyMap M>
-__device__ int wave_chunk(const int32_t* lens, int B, int64_t len_cap, int W, int sink, int target,
-                          int chunk_cap, int32_t* err, bool report) {
+__device__ int wave_chunk(const int32_t* lens, const int32_t* n_q, int qps, int NV, int64_t len_cap,
+                          int W, int sink, int target, int chunk_cap, int32_t* err, bool report) {
   const int lane = threadIdx.x & (kWave - 1);
   long long total = 0;
-  for (int base = 0; base < B; base += kWave) {
-    const int b = base + lane;
-    if (b < B) total += selected_count<M>(read_len(lens, b, len_cap, err, report), W, sink);
+  for (int base = 0; base < NV; base += kWave) {
+    const int v = base + lane;
+    int b;
+    if (v < NV)
+      total += selected_count<M>(visible_len(lens, n_q, qps, len_cap, err, v, report, b), W, sink);
   }
 #pragma unroll
   for (int off = kWave / 2; off > 0; off >>= 1) total += __shfl_xor(total, off);
@@ -119,27 +157,29 @@ __device__ int wave_chunk(const int32_t* lens, int B, int64_t len_cap, int W, in
   return static_cast<int>(c);
 }
 
-// Finds the sequence b and local chunk c of work item `item` (wave 0 scans
+// Finds the query row v and local chunk c of work item `item` (wave 0 scans
 // the lengths; the result is broadcast through LDS).  Returns false for the
-// whole workgroup when `item` lies past the last sequence's items.
+// whole workgroup when `item` lies past the last query row's items.
 template <KeyMap M>
-__device__ bool locate_item(const SplitArgs& a, int item, int& b_out, int& c_out, int& S_out,
+__device__ bool locate_item(const SplitArgs& a, int item, int& v_out, int& c_out, int& S_out,
                             int& chunk_out) {
-  __shared__ int s_b, s_c, s_S, s_chunk;
+  __shared__ int s_v, s_c, s_S, s_chunk;
+  const int NV = a.B * a.qps;
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
-    const int chunk =
-        wave_chunk<M>(a.lens, a.B, a.len_cap, a.W, a.sink, a.target, a.chunk_cap, a.err, true);
+    const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, NV, a.len_cap, a.W, a.sink, a.target,
+                                    a.chunk_cap, a.err, true);
     if (lane == 0) {
-      s_b = -1;
+      s_v = -1;
       s_chunk = chunk;
     }
     int carry = 0;
-    for (int base = 0; base < a.B; base += kWave) {
-      const int b = base + lane;
+    for (int base = 0; base < NV; base += kWave) {
+      const int v = base + lane;
       int S = 0, cnt = 0;
-      if (b < a.B) {
-        S = read_len(a.lens, b, a.len_cap, a.err, false);
+      if (v < NV) {
+        int b;
+        S = visible_len(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, false, b);
         cnt = ceil_div_i(selected_count<M>(S, a.W, a.sink), chunk);
       }
       int incl = cnt;
@@ -150,7 +190,7 @@ __device__ bool locate_item(const SplitArgs& a, int item, int& b_out, int& c_out
       }
       const int lo = carry + incl - cnt;
       if (cnt > 0 && item >= lo && item < lo + cnt) {
-        s_b = b;
+        s_v = v;
         s_c = item - lo;
         s_S = S;
       }
@@ -159,11 +199,11 @@ __device__ bool locate_item(const SplitArgs& a, int item, int& b_out, int& c_out
     }
   }
   __syncthreads();
-  b_out = s_b;
+  v_out = s_v;
   c_out = s_c;
   S_out = s_S;
   chunk_out = s_chunk;
-  return b_out >= 0;
+  return v_out >= 0;
 }
 
 #ifndef WMTP_NT_LOADS
@@ -203,9 +243,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int g = blockIdx.x % a.Hkv;
   const int item = blockIdx.x / a.Hkv;
 
-  int b, c, S, chunk;
-  if (!locate_item<M>(a, item, b, c, S, chunk)) return;
-  b = __builtin_amdgcn_readfirstlane(b);
+  int v, c, S, chunk;
+  if (!locate_item<M>(a, item, v, c, S, chunk)) return;
+  v = __builtin_amdgcn_readfirstlane(v);
+  const int b = a.qps == 1 ? v : v / a.qps;  // the sequence whose KV row v reads
   c = __builtin_amdgcn_readfirstlane(c);
   S = __builtin_amdgcn_readfirstlane(S);
   chunk = __builtin_amdgcn_readfirstlane(chunk);
@@ -223,7 +264,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   {
     const bool live = col < a.G;
     const uint16_t* qp =
-        a.q + (static_cast<int64_t>(b) * a.Hq + g * a.G + (live ? col : 0)) * D + grp * 8;
+        a.q + (static_cast<int64_t>(v) * a.Hq + g * a.G + (live ? col : 0)) * D + grp * 8;
 #pragma unroll
     for (int kk = 0; kk < KCH; ++kk) {
       u32x4 w = *reinterpret_cast<const u32x4*>(qp + kk * 32);
@@ -427,7 +468,7 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
   const int wave = tid / kWave;
   const int q4 = tid % Q;
   const int slot = tid / Q;
-  const int b = blockIdx.x / a.Hq;
+  const int v = blockIdx.x / a.Hq;  // query row
   const int h = blockIdx.x % a.Hq;
   const int g = h / a.G;
   const int hl = h % a.G;
@@ -439,15 +480,16 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
   __shared__ float s_L[NS];
   __shared__ float s_Z[NS];
   if (tid < kWave) {
-    const int chunk =
-        wave_chunk<M>(a.lens, a.B, a.len_cap, a.W, a.sink, a.target, a.chunk_cap, a.err, false);
+    const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, a.B * a.qps, a.len_cap, a.W, a.sink,
+                                    a.target, a.chunk_cap, a.err, false);
     int before = 0, mine = 0;
-    for (int base = 0; base <= b; base += kWave) {
-      const int bb = base + lane;
-      if (bb <= b) {
-        const int S = read_len(a.lens, bb, a.len_cap, a.err, false);
+    for (int base = 0; base <= v; base += kWave) {
+      const int vv = base + lane;
+      if (vv <= v) {
+        int bb;
+        const int S = visible_len(a.lens, a.n_q, a.qps, a.len_cap, a.err, vv, false, bb);
         const int cnt = ceil_div_i(selected_count<M>(S, a.W, a.sink), chunk);
-        if (bb < b) before += cnt; else mine = cnt;
+        if (vv < v) before += cnt; else mine = cnt;
       }
     }
 #pragma unroll
@@ -512,9 +554,9 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
     for (int i = 0; i < 4; ++i) r[i] = n > 0 ? ot[i] / Lt : 0.f;
     const uint32_t lo = f32_to_bf16_rne(r[0]) | (uint32_t(f32_to_bf16_rne(r[1])) << 16);
     const uint32_t hi = f32_to_bf16_rne(r[2]) | (uint32_t(f32_to_bf16_rne(r[3])) << 16);
-    *reinterpret_cast<u32x2*>(a.out + (static_cast<int64_t>(b) * a.Hq + h) * D + d0) = u32x2{lo, hi};
+    *reinterpret_cast<u32x2*>(a.out + (static_cast<int64_t>(v) * a.Hq + h) * D + d0) = u32x2{lo, hi};
     if (a.lse != nullptr && blockIdx.y == 0 && q4 == 0)
-      a.lse[static_cast<int64_t>(b) * a.Hq + h] = n > 0 ? (Mx + log2f(s_Z[0])) * kLn2 : neg_inf();
+      a.lse[static_cast<int64_t>(v) * a.Hq + h] = n > 0 ? (Mx + log2f(s_Z[0])) * kLn2 : neg_inf();
   }
 }
 
@@ -523,7 +565,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   const int G = L.Hq / L.Hkv;
   if (L.max_items > 0) {
     SplitArgs a;
-    a.q = L.q; a.k = L.k; a.v = L.v; a.lens = L.lens;
+    a.q = L.q; a.k = L.k; a.v = L.v; a.lens = L.lens; a.n_q = L.n_q; a.qps = L.qps;
     a.pm = L.pm; a.pl = L.pl; a.pz = L.pz; a.po = L.po; a.err = L.err;
     a.B = L.B; a.Hq = L.Hq; a.Hkv = L.Hkv; a.G = G;
     a.rows = L.rows; a.len_cap = L.len_cap;
@@ -534,14 +576,15 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
     hipLaunchKernelGGL((split_kernel<D, M>), grid, dim3(kThreads), 0, st, a);
   }
   // Items per sequence the plan allows decide the merge shape.
-  const bool wide = L.max_items >= 32 * L.B;
+  const int64_t NV = static_cast<int64_t>(L.B) * L.qps;
+  const bool wide = L.max_items >= 32 * NV;
   MergeArgs m;
-  m.lens = L.lens; m.pm = L.pm; m.pl = L.pl; m.pz = L.pz; m.po = L.po;
+  m.lens = L.lens; m.n_q = L.n_q; m.qps = L.qps; m.pm = L.pm; m.pl = L.pl; m.pz = L.pz; m.po = L.po;
   m.out = L.out; m.lse = L.lse; m.err = L.err;
   m.B = L.B; m.Hq = L.Hq; m.Hkv = L.Hkv; m.G = G;
   m.len_cap = L.len_cap; m.W = L.W; m.sink = L.sink;
   m.target = L.target; m.chunk_cap = L.chunk_cap;
-  const unsigned bh = static_cast<unsigned>(L.B) * static_cast<unsigned>(L.Hq);
+  const unsigned bh = static_cast<unsigned>(NV) * static_cast<unsigned>(L.Hq);
   if (wide)
     hipLaunchKernelGGL((merge_kernel<D, M, kMergeThreads, 64>), dim3(bh, D / 64), dim3(kMergeThreads), 0,
                        st, m);

@@ -13,6 +13,8 @@ struct AttnLaunch {
   const uint16_t* k;
   const uint16_t* v;
   const int32_t* lens;
+  const int32_t* n_q;  // new query rows per sequence, or NULL (all qps rows)
+  int qps;             // query rows per sequence (1 for a draft decode step)
   uint16_t* out;
   float* lse;
   int32_t* err;
@@ -41,7 +43,8 @@ struct SplitPlan {
   size_t off_po;
 };
 
-// Split plan for a validated shape; n_keys_max = most keys one sequence attends.
+// Split plan for a validated shape; B counts query rows (sequences x rows per
+// sequence); n_keys_max = most keys one query row attends.
 SplitPlan plan_split(int B, int Hq, int Hkv, int d, int64_t n_keys_max);
 
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t stream);

@@ -44,17 +44,24 @@ bool plan_fits(const SplitPlan& p, int Hkv) {
   return static_cast<int64_t>(p.max_items) * Hkv < INT_MAX;
 }
 
+// Largest number of query rows per sequence an extend call accepts.
+constexpr int kMaxQueryRows = 4096;
+
 int attention_common(int variant, const void* q, const void* k, const void* v,
-                     const int32_t* lens, void* out, float* lse, int B, int Hq, int Hkv, int d,
-                     int64_t S_max, int W, int sink, int R_w, float scale, void* ws,
-                     size_t ws_bytes, int32_t* err, void* stream) {
+                     const int32_t* lens, const int32_t* n_q, int q_max, void* out, float* lse,
+                     int B, int Hq, int Hkv, int d, int64_t S_max, int W, int sink, int R_w,
+                     float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream) {
   int st = check_heads(B, Hq, Hkv, d);
   if (st != WMTP_OK) return st;
+  if (q_max < 1 || q_max > kMaxQueryRows) return WMTP_EINVAL;
+  if (static_cast<int64_t>(B) * q_max > INT_MAX / 64) return WMTP_EINVAL;
   if (variant != WMTP_VARIANT_FULL) {
     st = check_window(W, sink);
     if (st != WMTP_OK) return st;
   }
-  if (variant == WMTP_VARIANT_RING && R_w < W) return WMTP_EINVAL;
+  // The ring must hold the window of the earliest new row as well.
+  if (variant == WMTP_VARIANT_RING && static_cast<int64_t>(R_w) < static_cast<int64_t>(W) + q_max - 1)
+    return WMTP_EINVAL;
   if (S_max < 0) return WMTP_EINVAL;
   if (!std::isfinite(scale)) return WMTP_EINVAL;
   if (B == 0) return WMTP_OK;
@@ -62,10 +69,11 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
     return WMTP_EINVAL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
       !aligned(lens, 4) || (lse != nullptr && !aligned(lse, 4)) ||
-      (err != nullptr && !aligned(err, 4)))
+      (err != nullptr && !aligned(err, 4)) || (n_q != nullptr && !aligned(n_q, 4)))
     return WMTP_EINVAL;
 
-  const SplitPlan plan = wmtp::plan_split(B, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
+  const int rows_q = B * q_max;
+  const SplitPlan plan = wmtp::plan_split(rows_q, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
   if (!plan_fits(plan, Hkv)) return WMTP_EUNSUPPORTED;
   if (ws_bytes < plan.bytes) return WMTP_EWORKSPACE;
   if (plan.bytes > 0 && (ws == nullptr || !aligned(ws, 256))) return WMTP_EINVAL;
@@ -76,6 +84,8 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   L.k = static_cast<const uint16_t*>(k);
   L.v = static_cast<const uint16_t*>(v);
   L.lens = lens;
+  L.n_q = n_q;
+  L.qps = q_max;
   L.out = static_cast<uint16_t*>(out);
   L.lse = lse;
   L.err = err;
@@ -160,8 +170,8 @@ WMTP_EXPORT int wmtp_draft_attn_full(const void* q, const void* k, const void* v
                                      const int32_t* lens, void* out, float* lse, int B, int Hq,
                                      int Hkv, int d, int64_t S_max, float scale, void* ws,
                                      size_t ws_bytes, int32_t* err, void* stream) {
-  return attention_common(WMTP_VARIANT_FULL, q, k, v, lens, out, lse, B, Hq, Hkv, d, S_max, 1, 0,
-                          1, scale, ws, ws_bytes, err, stream);
+  return attention_common(WMTP_VARIANT_FULL, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv, d,
+                          S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream);
 }
 
 WMTP_EXPORT int wmtp_draft_attn_windowed(const void* q, const void* k, const void* v,
@@ -169,8 +179,8 @@ WMTP_EXPORT int wmtp_draft_attn_windowed(const void* q, const void* k, const voi
                                          int Hq, int Hkv, int d, int64_t S_max, int W, int sink,
                                          float scale, void* ws, size_t ws_bytes, int32_t* err,
                                          void* stream) {
-  return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, out, lse, B, Hq, Hkv, d, S_max, W,
-                          sink, W, scale, ws, ws_bytes, err, stream);
+  return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv,
+                          d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream);
 }
 
 WMTP_EXPORT int wmtp_ring_attn(const void* q, const void* k_ring, const void* v_ring,
@@ -179,9 +189,39 @@ WMTP_EXPORT int wmtp_ring_attn(const void* q, const void* k_ring, const void* v_
                                size_t ws_bytes, int32_t* err, void* stream) {
   if (check_window(W, sink) == WMTP_OK && (R_w < W || static_cast<int64_t>(sink) + R_w > INT_MAX))
     return WMTP_EINVAL;
-  return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, out, lse, B, Hq, Hkv, d,
-                          static_cast<int64_t>(sink) + R_w, W, sink, R_w, scale, ws, ws_bytes,
-                          err, stream);
+  return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, nullptr, 1, out, lse, B, Hq,
+                          Hkv, d, static_cast<int64_t>(sink) + R_w, W, sink, R_w, scale, ws,
+                          ws_bytes, err, stream);
+}
+
+WMTP_EXPORT int wmtp_draft_extend_full(const void* q, const void* k, const void* v,
+                                       const int32_t* lens, const int32_t* n_q, void* out,
+                                       float* lse, int B, int q_max, int Hq, int Hkv, int d,
+                                       int64_t S_max, float scale, void* ws, size_t ws_bytes,
+                                       int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_FULL, q, k, v, lens, n_q, q_max, out, lse, B, Hq, Hkv, d,
+                          S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream);
+}
+
+WMTP_EXPORT int wmtp_draft_extend_windowed(const void* q, const void* k, const void* v,
+                                           const int32_t* lens, const int32_t* n_q, void* out,
+                                           float* lse, int B, int q_max, int Hq, int Hkv, int d,
+                                           int64_t S_max, int W, int sink, float scale, void* ws,
+                                           size_t ws_bytes, int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, n_q, q_max, out, lse, B, Hq, Hkv,
+                          d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream);
+}
+
+WMTP_EXPORT int wmtp_ring_extend(const void* q, const void* k_ring, const void* v_ring,
+                                 const int32_t* lens, const int32_t* n_q, void* out, float* lse,
+                                 int B, int q_max, int Hq, int Hkv, int d, int W, int sink,
+                                 int R_w, float scale, void* ws, size_t ws_bytes, int32_t* err,
+                                 void* stream) {
+  if (check_window(W, sink) == WMTP_OK && static_cast<int64_t>(sink) + R_w > INT_MAX)
+    return WMTP_EINVAL;
+  return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, n_q, q_max, out, lse, B, Hq,
+                          Hkv, d, static_cast<int64_t>(sink) + R_w, W, sink, R_w, scale, ws,
+                          ws_bytes, err, stream);
 }
 
 WMTP_EXPORT int wmtp_ring_append(void* k_ring, void* v_ring, const void* k_new,

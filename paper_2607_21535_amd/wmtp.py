@@ -29,6 +29,9 @@ __all__ = [
     "draft_attn_full",
     "draft_attn_windowed",
     "ring_attn",
+    "draft_extend_full",
+    "draft_extend_windowed",
+    "ring_extend",
     "ring_append",
     "cache_append",
     "select_indices",
@@ -45,6 +48,9 @@ EXPORTED_SYMBOLS = (
     "wmtp_draft_attn_full",
     "wmtp_draft_attn_windowed",
     "wmtp_ring_attn",
+    "wmtp_draft_extend_full",
+    "wmtp_draft_extend_windowed",
+    "wmtp_ring_extend",
     "wmtp_ring_append",
     "wmtp_cache_append",
     "wmtp_select_indices",
@@ -66,6 +72,9 @@ _SIGNATURES = {
     "wmtp_draft_attn_full": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _F, _P, _SZ, _P, _P]),
     "wmtp_draft_attn_windowed": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _F, _P, _SZ, _P, _P]),
     "wmtp_ring_attn": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P, _SZ, _P, _P]),
+    "wmtp_draft_extend_full": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I64, _F, _P, _SZ, _P, _P]),
+    "wmtp_draft_extend_windowed": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I64, _I, _I, _F, _P, _SZ, _P, _P]),
+    "wmtp_ring_extend": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _SZ, _P, _P]),
     "wmtp_ring_append": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
     "wmtp_cache_append": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I64, _I, _P, _P]),
     "wmtp_select_indices": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
@@ -209,6 +218,83 @@ def ring_attn(q, k_ring, v_ring, lens, W, sink, R_w, out=None, lse=None, scale=N
         _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, W, sink,
         R_w, scale, _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _ptr(err), _stream(dev))
     _check(st, "wmtp_ring_attn")
+    return out
+
+
+def _extend_io(q, k, v, lens, n_q, out, lse):
+    _need(q, "q", torch.bfloat16, 4)
+    dev = q.device
+    _need(k, "k", torch.bfloat16, 4, dev)
+    _need(v, "v", torch.bfloat16, 4, dev)
+    _need(lens, "lens", torch.int32, 1, dev)
+    B, q_max, Hq, d = q.shape
+    if k.shape != v.shape or k.shape[0] != B or k.shape[3] != d or lens.shape[0] != B:
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} lens {tuple(lens.shape)}")
+    if n_q is not None:
+        _need(n_q, "n_q", torch.int32, 1, dev)
+        if n_q.shape[0] != B:
+            raise ValueError("n_q must be [B]")
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need(out, "out", torch.bfloat16, 4, dev)
+        if out.shape != q.shape:
+            raise ValueError("out must have q's shape")
+    if lse is not None:
+        _need(lse, "lse", torch.float32, 3, dev)
+        if tuple(lse.shape) != (B, q_max, Hq):
+            raise ValueError("lse must be [B, q_max, Hq]")
+    return dev, B, q_max, Hq, d, out
+
+
+def _wsize(ws):
+    return 0 if ws is None else ws.numel() * ws.element_size()
+
+
+def draft_extend_full(q, k, v, lens, n_q=None, out=None, lse=None, scale=None, ws=None, err=None):
+    """Causal multi-row draft attention over the full context.
+
+    q [B, q_max, Hq, d]; lens counts the cached rows including the new ones;
+    row t of sequence b sees lens[b] - n_q[b] + t + 1 rows.
+    """
+    dev, B, q_max, Hq, d, out = _extend_io(q, k, v, lens, n_q, out, lse)
+    S_max, Hkv = k.shape[1], k.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_FULL, B * q_max, Hq, Hkv, d, S_max), dev)
+    st = load_library().wmtp_draft_extend_full(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq, Hkv, d,
+        S_max, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_extend_full")
+    return out
+
+
+def draft_extend_windowed(q, k, v, lens, W, sink, n_q=None, out=None, lse=None, scale=None, ws=None,
+                          err=None):
+    """Causal multi-row draft attention, each row under its own sink + window."""
+    dev, B, q_max, Hq, d, out = _extend_io(q, k, v, lens, n_q, out, lse)
+    S_max, Hkv = k.shape[1], k.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_WINDOWED, B * q_max, Hq, Hkv, d, S_max, W, sink), dev)
+    st = load_library().wmtp_draft_extend_windowed(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq, Hkv, d,
+        S_max, W, sink, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_extend_windowed")
+    return out
+
+
+def ring_extend(q, k_ring, v_ring, lens, W, sink, R_w, n_q=None, out=None, lse=None, scale=None,
+                ws=None, err=None):
+    """Causal multi-row windowed draft attention over the ring (R_w >= W + q_max - 1)."""
+    dev, B, q_max, Hq, d, out = _extend_io(q, k_ring, v_ring, lens, n_q, out, lse)
+    if k_ring.shape[1] != sink + R_w:
+        raise ValueError(f"ring must hold sink + R_w = {sink + R_w} rows, has {k_ring.shape[1]}")
+    Hkv = k_ring.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_RING, B * q_max, Hq, Hkv, d, sink + R_w, W, sink), dev)
+    st = load_library().wmtp_ring_extend(
+        _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq,
+        Hkv, d, W, sink, R_w, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_ring_extend")
     return out
 
 

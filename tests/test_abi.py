@@ -206,3 +206,35 @@ def test_binding_rejects_host_tensors():
     lens = torch.zeros(1, dtype=torch.int32)
     with pytest.raises(ValueError, match="HIP device"):
         W.draft_attn_full(q, k, k, lens)
+
+
+def _ext(lib, which, **kw):
+    base = dict(q=P, k=P, v=P, lens=P, n_q=P, out=P, lse=None, B=1, q_max=4, Hq=16, Hkv=2, d=128)
+    if which == "full":
+        base.update(S_max=100)
+    elif which == "windowed":
+        base.update(S_max=100, W=8, sink=4)
+    else:
+        base.update(W=8, sink=4, R_w=11)
+    base.update(scale=0.1, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    base.update(kw)
+    fn = {"full": lib.wmtp_draft_extend_full, "windowed": lib.wmtp_draft_extend_windowed,
+          "ring": lib.wmtp_ring_extend}[which]
+    return fn(*base.values())
+
+
+@fake_pointers
+@pytest.mark.parametrize("which", ["full", "windowed", "ring"])
+def test_extend_argument_checks(lib, which):
+    assert _ext(lib, which, q_max=0) == W.EINVAL
+    assert _ext(lib, which, q_max=5000) == W.EINVAL
+    assert _ext(lib, which, n_q=P + 2) == W.EINVAL
+    assert _ext(lib, which, d=96) == W.EUNSUPPORTED
+    assert _ext(lib, which, ws_bytes=1) == W.EWORKSPACE
+    assert _ext(lib, which, q=None) == W.EINVAL
+
+
+@fake_pointers
+def test_ring_extend_needs_room_for_the_earliest_row(lib):
+    assert _ext(lib, "ring", R_w=10) == W.EINVAL  # W + q_max - 1 = 11
+    assert _ext(lib, "ring", q_max=1, R_w=8, ws_bytes=1) == W.EWORKSPACE  # R_w = W is enough for one row

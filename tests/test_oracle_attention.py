@@ -286,3 +286,54 @@ def test_batch_wrapper_and_sink_bias_case():
     o, lse = A.attend_batch(q, kb, vb, case["lens"], wl.scale, "windowed", W=wl.W, sink=wl.sink)
     o1, _ = A.attend_sequence(q[0], kb[0], vb[0], 600, wl.scale, None)
     assert np.array_equal(o[0], o1)  # S = 600 <= W + sink: degenerate
+
+
+# ---------------------------------------------------------------- extend
+def _sdpa_extend(q, K, V, S, n, scale, W=None, sink=None):
+    """torch SDPA (float64) over all new rows at once with an explicit
+    [n, S] boolean mask built from positions: row t is the token at position
+    S - n + t; it may see p <= S - n + t, and under the window only the sink
+    and the last W of those."""
+    qf = torch.from_numpy(A.bf16_to_f64(q[:n]))             # [n, Hq, d]
+    Kf = torch.from_numpy(A.bf16_to_f64(K[:S]))
+    Vf = torch.from_numpy(A.bf16_to_f64(V[:S]))
+    n_, Hq, d = qf.shape
+    Hkv = Kf.shape[1]
+    me = torch.arange(S - n, S).view(n, 1)                  # each row's own position
+    p = torch.arange(S).view(1, S)
+    m = p <= me
+    if W is not None:
+        L = me + 1
+        m = m & ((L <= sink + W) | (p < sink) | (p >= L - W))
+    out = torch.nn.functional.scaled_dot_product_attention(
+        qf.permute(1, 0, 2).unsqueeze(0), Kf.permute(1, 0, 2).unsqueeze(0).contiguous(),
+        Vf.permute(1, 0, 2).unsqueeze(0).contiguous(), attn_mask=m.view(1, 1, n, S), scale=scale,
+        enable_gqa=(Hq != Hkv))
+    return out[0].permute(1, 0, 2).numpy()
+
+
+@pytest.mark.parametrize("S,n,q_max", [(1, 1, 1), (5, 3, 4), (40, 8, 8), (300, 5, 8), (2100, 4, 4)])
+@pytest.mark.parametrize("W,sink", [(None, None), (16, 2), (1, 0), (64, 4)])
+def test_extend_matches_causal_sdpa(S, n, q_max, W, sink):
+    q, K, V = _rand_case(S + n, S, Hq=4, Hkv=2, d=8)
+    qr = I.bf16_bits(torch.from_numpy(np.random.default_rng(S).standard_normal((q_max, 4, 8))).to(torch.bfloat16))
+    variant = "full" if W is None else "windowed"
+    o, lse = A.attend_extend(qr, K, V, S, n, 0.3, variant, W, sink)
+    ref = _sdpa_extend(qr, K, V, S, n, 0.3, W, sink)
+    np.testing.assert_allclose(o[:n], ref, atol=1e-12)
+    assert np.all(o[n:] == 0) and np.all(np.isneginf(lse[n:]))
+
+
+def test_extend_rows_are_decode_steps():
+    # Row t of an extend equals a decode step at length S - n + t + 1, and a
+    # one-row extend is exactly the decode step.
+    S, n = 500, 6
+    q, K, V = _rand_case(1, S, Hq=4, Hkv=2, d=8)
+    qr = np.stack([I.bf16_bits(torch.randn(4, 8).to(torch.bfloat16)) for _ in range(n)])
+    o, lse = A.attend_extend(qr, K, V, S, n, 0.3, "windowed", 32, 3)
+    for t in range(n):
+        L = S - n + t + 1
+        od, ld = A.attend_sequence(qr[t], K, V, L, 0.3, A.window_mask(L, 32, 3))
+        assert np.array_equal(o[t], od) and np.array_equal(lse[t], ld)
+    assert A.extend_lengths(S, 1, 1) == [S]
+    assert A.extend_lengths(10, 3, 5) == [8, 9, 10, 0, 0]
