@@ -63,12 +63,15 @@ typedef enum {
 #define WMTP_DERR_LEN_RANGE 0x1  /* lens[b] < 0, > S_max for a dense cache, or < n_q[b]: clamped */
 #define WMTP_DERR_NNEW_RANGE 0x2 /* n_new[b] outside [0, n_max] (n_q[b] outside [0, q_max]): clamped */
 #define WMTP_DERR_CAPACITY 0x4   /* dense-cache append past S_max: extra rows dropped */
+#define WMTP_DERR_SLOT_RANGE 0x8 /* req_to_token entry outside the pool: row 0 read instead */
 
 /* Attention variants, for wmtp_workspace_bytes(). */
 typedef enum {
   WMTP_VARIANT_FULL = 0,
   WMTP_VARIANT_WINDOWED = 1,
-  WMTP_VARIANT_RING = 2
+  WMTP_VARIANT_RING = 2,
+  WMTP_VARIANT_PAGED_FULL = 3,
+  WMTP_VARIANT_PAGED_WINDOWED = 4
 } wmtp_variant;
 
 /*
@@ -165,6 +168,44 @@ int wmtp_ring_extend(const void* q, const void* k_ring, const void* v_ring, cons
                      const int32_t* n_q, void* out, float* lse, int B, int q_max, int Hq, int Hkv,
                      int d, int W, int sink, int R_w, float scale, void* ws, size_t ws_bytes,
                      int32_t* err, void* stream);
+
+/*
+ * Paged draft KV (a shared token pool with page size 1, as in the paper's
+ * serving setup, Section 4 "Mechanism" and Appendix A).  k_pool, v_pool
+ * [pool_rows, Hkv, d] bf16 hold every request's rows; req_to_token
+ * [B, table_stride] int32 gives the pool row of position p of request b
+ * (0 <= lens[b] <= table_stride).  The attention reads pool rows through the
+ * table only at the kept positions -- all of [0, lens[b]) natively, the sink
+ * and the last W windowed -- and gives the same result, bit for bit, as the
+ * dense call over a cache holding the same rows.  Table entries outside
+ * [0, pool_rows) read row 0 and raise WMTP_DERR_SLOT_RANGE.
+ * Workspace: wmtp_workspace_bytes(WMTP_VARIANT_PAGED_FULL / _WINDOWED, B, Hq,
+ * Hkv, d, table_stride, W, sink).
+ */
+int wmtp_paged_attn_full(const void* q, const void* k_pool, const void* v_pool,
+                         const int32_t* req_to_token, const int32_t* lens, void* out, float* lse,
+                         int B, int Hq, int Hkv, int d, int64_t pool_rows, int64_t table_stride,
+                         float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream);
+int wmtp_paged_attn_windowed(const void* q, const void* k_pool, const void* v_pool,
+                             const int32_t* req_to_token, const int32_t* lens, void* out,
+                             float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
+                             int64_t table_stride, int W, int sink, float scale, void* ws,
+                             size_t ws_bytes, int32_t* err, void* stream);
+
+/*
+ * The draft's KV-index builder (the step Windowed-MTP modifies, Appendix A
+ * pseudocode: kv_index = req_to_token[r, keep]).  Writes kv_indptr [B + 1]
+ * (prefix sums of the kept counts) and kv_indices (packed pool rows of the
+ * kept keys, request by request, ascending position) for variant
+ * WMTP_VARIANT_PAGED_FULL (keep all lens[b] positions: O(S)) or
+ * WMTP_VARIANT_PAGED_WINDOWED (sink + last W: O(sink + W)).  `capacity` is
+ * the length of kv_indices and must be at least
+ * wmtp_kv_indices_capacity(variant, B, table_stride, W, sink); B <= 65535.
+ */
+int64_t wmtp_kv_indices_capacity(int variant, int B, int64_t table_stride, int W, int sink);
+int wmtp_build_kv_indices(const int32_t* req_to_token, const int32_t* lens, int B,
+                          int64_t table_stride, int variant, int W, int sink, int32_t* kv_indptr,
+                          int32_t* kv_indices, int64_t capacity, int32_t* err, void* stream);
 
 /*
  * Append draft KV rows to the ring store (the draft forward writes the K/V

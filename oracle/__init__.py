@@ -14,6 +14,9 @@ Modules
   ring       -- the compact ring-buffer draft KV store: the slot map and an
                 operational replay of appends (Section 4 "Memory", Section 6
                 "Memory", the ring comment of the Appendix A pseudocode).
+  paged      -- the paged token pool (page size 1): the draft's index list
+                req_to_token[r, keep] and attention over the listed rows
+                (Section 4 "Mechanism", Appendix A pseudocode).
 
 Every function states the passage it follows.  Readings of points where the
 paper is silent are listed in the module docstrings.  No function here is
@@ -23,4 +26,4 @@ against closed forms, brute force, invariants, a library routine
 (tests/golden/).
 """
 
-from . import attention, ring  # noqa: F401
+from . import attention, paged, ring  # noqa: F401

@@ -51,6 +51,7 @@ namespace wmtp {
 namespace {
 
 constexpr int kMergeThreads = 1024;
+constexpr int kPagedChunkMax = 9216;  // largest work item of a paged call (its slots live in LDS)
 
 struct SplitArgs {
   const uint16_t* q;
@@ -63,9 +64,11 @@ struct SplitArgs {
   float* po;
   int32_t* err;
   const int32_t* n_q;  // new query rows per sequence (NULL: all qps rows)
+  const int32_t* table;  // paged: req_to_token [B, table_stride]
+  int64_t table_stride;
   int B, Hq, Hkv, G;
   int qps;             // query rows per sequence; NV = B * qps query rows in all
-  int64_t rows;
+  int64_t rows;        // dense: rows per sequence; ring: slots; paged: pool rows
   int64_t len_cap;
   int W, sink, R_w;
   int target;     // work items per KV head to aim for
@@ -255,9 +258,38 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int j1 = min(j0 + chunk, n_sel);
   const RowMap<M> map(S, a.W, a.sink, a.R_w);
   const int64_t rs = static_cast<int64_t>(a.Hkv) * D;  // elements between rows
-  const int64_t seq_off = (static_cast<int64_t>(b) * a.rows * a.Hkv + g) * D;
+  // Dense and ring caches hold `rows` rows per sequence; a paged pool is one
+  // shared array of rows indexed by the request's token table.
+  const int64_t seq_rows = is_paged(M) ? 0 : static_cast<int64_t>(b) * a.rows;
+  const int64_t seq_off = (seq_rows * a.Hkv + g) * D;
   const uint16_t* kbase = a.k + seq_off;
   const uint16_t* vbase = a.v + seq_off;
+
+  // Paged: the pool rows of this item's keys, looked up once into LDS.
+  [[maybe_unused]] int* slots = nullptr;
+  if constexpr (is_paged(M)) {
+    __shared__ int s_slot[kPagedChunkMax];
+    slots = s_slot;
+    const int32_t* trow = a.table + static_cast<int64_t>(b) * a.table_stride;
+    bool bad = false;
+    for (int j = j0 + static_cast<int>(threadIdx.x); j < j1; j += kThreads) {
+      int slot = trow[map.row(j)];
+      if (slot < 0 || static_cast<int64_t>(slot) >= a.rows) {
+        bad = true;
+        slot = 0;
+      }
+      s_slot[j - j0] = slot;
+    }
+    if (bad) raise_error(a.err, WMTP_DERR_SLOT_RANGE);
+    __syncthreads();
+  }
+  auto row_of = [&](int j) -> int {
+    if constexpr (is_paged(M)) {
+      return slots[j - j0];
+    } else {
+      return map.row(j);
+    }
+  };
 
   // Q^T operand: lane (grp, col) holds q[b, g*G + col, kk*32 + grp*8 .. +8].
   bf16x8 qf[KCH];
@@ -288,7 +320,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     const int jt = j0 + min(t, n_tiles - 1) * kTileKeys;
     {
       const int j = jt + col;
-      const int r = map.row(j < j1 ? j : j0);
+      const int r = row_of(j < j1 ? j : j0);
       const uint16_t* p = kbase + static_cast<int64_t>(r) * rs + grp * 8;
 #pragma unroll
       for (int kk = 0; kk < KCH; ++kk) T.kx[kk] = stream_load<u32x4>(p + kk * 32);
@@ -296,7 +328,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = jt + 4 * grp + i;
-      const int r = map.row(j < j1 ? j : j0);
+      const int r = row_of(j < j1 ? j : j0);
       const uint16_t* p = vbase + static_cast<int64_t>(r) * rs + SEG * col;
 #pragma unroll
       for (int sg = 0; sg < NSEG; ++sg) {
@@ -566,6 +598,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   if (L.max_items > 0) {
     SplitArgs a;
     a.q = L.q; a.k = L.k; a.v = L.v; a.lens = L.lens; a.n_q = L.n_q; a.qps = L.qps;
+    a.table = L.table; a.table_stride = L.table_stride;
     a.pm = L.pm; a.pl = L.pl; a.pz = L.pz; a.po = L.po; a.err = L.err;
     a.B = L.B; a.Hq = L.Hq; a.Hkv = L.Hkv; a.G = G;
     a.rows = L.rows; a.len_cap = L.len_cap;
@@ -598,7 +631,9 @@ hipError_t launch_d(const AttnLaunch& L, hipStream_t st) {
   switch (L.variant) {
     case WMTP_VARIANT_FULL: return launch_typed<D, KeyMap::Full>(L, st);
     case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::Window>(L, st);
-    default: return launch_typed<D, KeyMap::Ring>(L, st);
+    case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::Ring>(L, st);
+    case WMTP_VARIANT_PAGED_FULL: return launch_typed<D, KeyMap::PagedFull>(L, st);
+    default: return launch_typed<D, KeyMap::PagedWindow>(L, st);
   }
 }
 
@@ -648,28 +683,31 @@ int resident_split_groups(int d) {
   return v;
 }
 
-SplitPlan plan_split(int B, int Hq, int Hkv, int d, int64_t n_keys_max) {
-  // Aim for as many workgroups as the device keeps resident (one balanced
-  // round: 512 on MI355X at d = 256) with items of at most `chunk_max`
-  // keys, so that a long single
-  // sequence runs in one balanced round and many or variable-length
+SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_max) {
+  // Aim for as many workgroups as the device keeps resident (512 on MI355X
+  // at d = 256), with items of at most `chunk_max` keys, so that a long
+  // single sequence runs in one balanced round and many or variable-length
   // sequences are cut finely enough to pack without a long tail.  Fewer
   // items also mean fewer partials for the merge.  The kernels pick the item
   // size from the actual lengths; the workspace covers every choice they can
-  // make: with per-head target T and chunk in [quantum, chunk_max], the item
-  // count is at most min(B*ceil(n/quantum), max(T + B, B*ceil(n/chunk_max))).
+  // make: with per-head target T and chunk in [quantum, cap], the item count
+  // is at most min(B*ceil(n/quantum), max(T + B, B*ceil(n/cap))).
   static const int target_env = env_int("WMTP_TARGET_ITEMS", 0);
   static const int chunk_max = std::max(
       kChunkQuantum, env_int("WMTP_CHUNK_MAX", WMTP_CHUNK_MAX_DEFAULT) / kChunkQuantum * kChunkQuantum);
   SplitPlan p{};
+  // A paged item's pool rows are staged in LDS: its size is capped.
+  const int cap = (variant == WMTP_VARIANT_PAGED_FULL || variant == WMTP_VARIANT_PAGED_WINDOWED)
+                      ? std::min(chunk_max, kPagedChunkMax)
+                      : chunk_max;
   const int64_t wgs = target_env > 0 ? target_env : resident_split_groups(d);
   const int64_t T = std::max<int64_t>(1, wgs / std::max(Hkv, 1));
   p.target = static_cast<int>(std::min<int64_t>(T, INT32_MAX / 2));
-  p.chunk_cap = chunk_max;
+  p.chunk_cap = cap;
   int64_t items = 0;
   if (n_keys_max > 0) {
     const int64_t fine = static_cast<int64_t>(B) * ((n_keys_max + kChunkQuantum - 1) / kChunkQuantum);
-    const int64_t coarse = static_cast<int64_t>(B) * ((n_keys_max + chunk_max - 1) / chunk_max);
+    const int64_t coarse = static_cast<int64_t>(B) * ((n_keys_max + cap - 1) / cap);
     items = std::min(fine, std::max(T + B, coarse));
   }
   p.max_items = static_cast<int>(std::min<int64_t>(items, INT32_MAX));

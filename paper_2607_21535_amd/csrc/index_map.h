@@ -8,41 +8,41 @@
 //             0 .. sink-1 followed by S-W .. S-1, otherwise j itself
 // The compact ring keeps position p in slot p (p < sink) or
 // sink + (p - sink) mod R_w; the ring holds the whole window when R_w >= W.
-// Everything here is O(1) integer arithmetic per key: no index table exists.
+// Everything here is O(1) integer arithmetic per key: no index table is
+// built.  A paged pool adds one lookup of the request's token table
+// (req_to_token[b][position]) per kept key -- for the windowed draft only at
+// the sink + W kept positions (the Appendix A pseudocode's
+// kv_index = req_to_token[r, keep]).
 #pragma once
 
 #include "common.h"
 
 namespace wmtp {
 
-enum class KeyMap : int { Full = 0, Window = 1, Ring = 2 };
+// Key maps: where virtual key j of a query row is stored.
+//   Full, Window       dense per-sequence cache, row = logical position
+//   Ring               compact ring, row = ring slot of the position
+//   PagedFull/Window   shared token pool, row = req_to_token[b][position]
+//                      (the kernel resolves the table; RowMap gives positions)
+enum class KeyMap : int { Full = 0, Window = 1, Ring = 2, PagedFull = 3, PagedWindow = 4 };
+
+constexpr bool is_paged(KeyMap m) { return m == KeyMap::PagedFull || m == KeyMap::PagedWindow; }
+constexpr bool is_windowed(KeyMap m) {
+  return m == KeyMap::Window || m == KeyMap::Ring || m == KeyMap::PagedWindow;
+}
 
 template <KeyMap M>
 __device__ __forceinline__ int selected_count(int S, int W, int sink) {
-  if constexpr (M == KeyMap::Full) {
+  if constexpr (!is_windowed(M)) {
     return S;
   } else {
     return S > sink + W ? sink + W : S;
   }
 }
 
-// Logical position of virtual key j (0 <= j < selected_count).
-template <KeyMap M>
-__device__ __forceinline__ int key_position(int j, int S, int W, int sink) {
-  if constexpr (M == KeyMap::Full) {
-    return j;
-  } else {
-    return (S > sink + W && j >= sink) ? S - W + (j - sink) : j;
-  }
-}
-
-// Ring slot of logical position p.
-__device__ __forceinline__ int ring_slot(int p, int sink, int R_w) {
-  return p < sink ? p : sink + (p - sink) % R_w;
-}
-
-// Storage row of virtual key j, with the per-sequence part hoisted: one
-// compare for the window, one compare-and-subtract for the ring wrap.
+// Storage row (dense, ring) or logical position (paged) of virtual key j,
+// with the per-sequence part hoisted: one compare for the window, one
+// compare-and-subtract for the ring wrap.
 template <KeyMap M>
 struct RowMap {
   int sink;
@@ -51,14 +51,14 @@ struct RowMap {
   int r0;     // shift mod R_w (ring only)
 
   __device__ __forceinline__ RowMap(int S, int W, int sink_, int R_w_) : sink(sink_), R_w(R_w_) {
-    shift = (M != KeyMap::Full && S > sink_ + W) ? S - W - sink_ : 0;
+    shift = (is_windowed(M) && S > sink_ + W) ? S - W - sink_ : 0;
     r0 = (M == KeyMap::Ring) ? shift % R_w_ : 0;
   }
 
   __device__ __forceinline__ int row(int j) const {
-    if constexpr (M == KeyMap::Full) {
+    if constexpr (!is_windowed(M)) {
       return j;
-    } else if constexpr (M == KeyMap::Window) {
+    } else if constexpr (M != KeyMap::Ring) {
       return j < sink ? j : j + shift;
     } else {
       // j - sink < W <= R_w and r0 < R_w, so one subtraction wraps.

@@ -15,11 +15,13 @@ struct AttnLaunch {
   const int32_t* lens;
   const int32_t* n_q;  // new query rows per sequence, or NULL (all qps rows)
   int qps;             // query rows per sequence (1 for a draft decode step)
+  const int32_t* table;   // paged variants: req_to_token [B, table_stride]
+  int64_t table_stride;
   uint16_t* out;
   float* lse;
   int32_t* err;
   int B, Hq, Hkv, d;
-  int64_t rows;     // storage rows per sequence: S_max, or sink + R_w for the ring
+  int64_t rows;     // rows per sequence: S_max (dense), sink + R_w (ring); pool rows (paged)
   int64_t len_cap;  // largest valid lens[b]
   int W, sink, R_w;
   float scale;
@@ -45,7 +47,13 @@ struct SplitPlan {
 
 // Split plan for a validated shape; B counts query rows (sequences x rows per
 // sequence); n_keys_max = most keys one query row attends.
-SplitPlan plan_split(int B, int Hq, int Hkv, int d, int64_t n_keys_max);
+SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_max);
+
+// Index builder: kv_indptr [B+1] and kv_indices (packed) of the kept keys,
+// each entry req_to_token[b][position] (variant: full or windowed key set).
+hipError_t launch_kv_indices(const int32_t* table, int64_t table_stride, const int32_t* lens,
+                             int B, bool windowed, int W, int sink, int64_t n_keys_max,
+                             int32_t* indptr, int32_t* indices, int32_t* err, hipStream_t stream);
 
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t stream);
 

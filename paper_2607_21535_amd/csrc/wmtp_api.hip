@@ -5,6 +5,7 @@
 #include "../../include/wmtp.h"
 #include "launch.h"
 
+#include <algorithm>
 #include <climits>
 #include <cmath>
 #include <cstdint>
@@ -37,7 +38,18 @@ int check_window(int W, int sink) {
 // variants plan for sink + W whatever the cache capacity, so both split the
 // same key set identically (bit-identical results).
 int64_t keys_max(int variant, int64_t S_max, int W, int sink) {
-  return variant == WMTP_VARIANT_FULL ? S_max : static_cast<int64_t>(W) + sink;
+  return (variant == WMTP_VARIANT_FULL || variant == WMTP_VARIANT_PAGED_FULL)
+             ? S_max
+             : static_cast<int64_t>(W) + sink;
+}
+
+bool windowed_variant(int variant) {
+  return variant == WMTP_VARIANT_WINDOWED || variant == WMTP_VARIANT_RING ||
+         variant == WMTP_VARIANT_PAGED_WINDOWED;
+}
+
+bool paged_variant(int variant) {
+  return variant == WMTP_VARIANT_PAGED_FULL || variant == WMTP_VARIANT_PAGED_WINDOWED;
 }
 
 bool plan_fits(const SplitPlan& p, int Hkv) {
@@ -47,18 +59,22 @@ bool plan_fits(const SplitPlan& p, int Hkv) {
 // Largest number of query rows per sequence an extend call accepts.
 constexpr int kMaxQueryRows = 4096;
 
+// S_max: dense rows per sequence / ring slots / request-table capacity.
+// pool_rows: rows of the shared pool (paged variants only).
 int attention_common(int variant, const void* q, const void* k, const void* v,
                      const int32_t* lens, const int32_t* n_q, int q_max, void* out, float* lse,
                      int B, int Hq, int Hkv, int d, int64_t S_max, int W, int sink, int R_w,
-                     float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream) {
+                     float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream,
+                     const int32_t* table = nullptr, int64_t pool_rows = 0) {
   int st = check_heads(B, Hq, Hkv, d);
   if (st != WMTP_OK) return st;
   if (q_max < 1 || q_max > kMaxQueryRows) return WMTP_EINVAL;
   if (static_cast<int64_t>(B) * q_max > INT_MAX / 64) return WMTP_EINVAL;
-  if (variant != WMTP_VARIANT_FULL) {
+  if (windowed_variant(variant)) {
     st = check_window(W, sink);
     if (st != WMTP_OK) return st;
   }
+  if (paged_variant(variant) && (pool_rows < 1 || pool_rows > INT_MAX)) return WMTP_EINVAL;
   // The ring must hold the window of the earliest new row as well.
   if (variant == WMTP_VARIANT_RING && static_cast<int64_t>(R_w) < static_cast<int64_t>(W) + q_max - 1)
     return WMTP_EINVAL;
@@ -67,13 +83,15 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   if (B == 0) return WMTP_OK;
   if (q == nullptr || k == nullptr || v == nullptr || lens == nullptr || out == nullptr)
     return WMTP_EINVAL;
+  if (paged_variant(variant) && (table == nullptr || !aligned(table, 4))) return WMTP_EINVAL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
       !aligned(lens, 4) || (lse != nullptr && !aligned(lse, 4)) ||
       (err != nullptr && !aligned(err, 4)) || (n_q != nullptr && !aligned(n_q, 4)))
     return WMTP_EINVAL;
 
   const int rows_q = B * q_max;
-  const SplitPlan plan = wmtp::plan_split(rows_q, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
+  const SplitPlan plan =
+      wmtp::plan_split(variant, rows_q, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
   if (!plan_fits(plan, Hkv)) return WMTP_EUNSUPPORTED;
   if (ws_bytes < plan.bytes) return WMTP_EWORKSPACE;
   if (plan.bytes > 0 && (ws == nullptr || !aligned(ws, 256))) return WMTP_EINVAL;
@@ -93,9 +111,14 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   L.Hq = Hq;
   L.Hkv = Hkv;
   L.d = d;
+  L.table = table;
+  L.table_stride = S_max;
   if (variant == WMTP_VARIANT_RING) {
     L.rows = static_cast<int64_t>(sink) + R_w;
     L.len_cap = INT_MAX;
+  } else if (paged_variant(variant)) {
+    L.rows = pool_rows;
+    L.len_cap = S_max < INT_MAX ? S_max : INT_MAX;
   } else {
     L.rows = S_max;
     L.len_cap = S_max < INT_MAX ? S_max : INT_MAX;
@@ -155,13 +178,12 @@ int append_common(bool ring, void* k, void* v, const void* k_new, const void* v_
 
 WMTP_EXPORT size_t wmtp_workspace_bytes(int variant, int B, int Hq, int Hkv, int d, int64_t S_max,
                                         int W, int sink) {
-  if (variant != WMTP_VARIANT_FULL && variant != WMTP_VARIANT_WINDOWED &&
-      variant != WMTP_VARIANT_RING)
-    return 0;
+  if (variant < WMTP_VARIANT_FULL || variant > WMTP_VARIANT_PAGED_WINDOWED) return 0;
   if (check_heads(B, Hq, Hkv, d) != WMTP_OK || B == 0) return 0;
-  if (variant != WMTP_VARIANT_FULL && check_window(W, sink) != WMTP_OK) return 0;
-  if (variant == WMTP_VARIANT_FULL && S_max < 0) return 0;
-  const SplitPlan plan = wmtp::plan_split(B, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
+  if (windowed_variant(variant) && check_window(W, sink) != WMTP_OK) return 0;
+  if (!windowed_variant(variant) && S_max < 0) return 0;
+  const SplitPlan plan =
+      wmtp::plan_split(variant, B, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
   if (!plan_fits(plan, Hkv)) return 0;
   return plan.bytes;
 }
@@ -222,6 +244,65 @@ WMTP_EXPORT int wmtp_ring_extend(const void* q, const void* k_ring, const void* 
   return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, n_q, q_max, out, lse, B, Hq,
                           Hkv, d, static_cast<int64_t>(sink) + R_w, W, sink, R_w, scale, ws,
                           ws_bytes, err, stream);
+}
+
+WMTP_EXPORT int wmtp_paged_attn_full(const void* q, const void* k_pool, const void* v_pool,
+                                      const int32_t* req_to_token, const int32_t* lens, void* out,
+                                      float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
+                                      int64_t table_stride, float scale, void* ws, size_t ws_bytes,
+                                      int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_PAGED_FULL, q, k_pool, v_pool, lens, nullptr, 1, out, lse, B,
+                          Hq, Hkv, d, table_stride, 1, 0, 1, scale, ws, ws_bytes, err, stream,
+                          req_to_token, pool_rows);
+}
+
+WMTP_EXPORT int wmtp_paged_attn_windowed(const void* q, const void* k_pool, const void* v_pool,
+                                          const int32_t* req_to_token, const int32_t* lens,
+                                          void* out, float* lse, int B, int Hq, int Hkv, int d,
+                                          int64_t pool_rows, int64_t table_stride, int W, int sink,
+                                          float scale, void* ws, size_t ws_bytes, int32_t* err,
+                                          void* stream) {
+  return attention_common(WMTP_VARIANT_PAGED_WINDOWED, q, k_pool, v_pool, lens, nullptr, 1, out,
+                          lse, B, Hq, Hkv, d, table_stride, W, sink, W, scale, ws, ws_bytes, err,
+                          stream, req_to_token, pool_rows);
+}
+
+WMTP_EXPORT int64_t wmtp_kv_indices_capacity(int variant, int B, int64_t table_stride, int W,
+                                             int sink) {
+  if (B < 0 || table_stride < 0) return 0;
+  if (variant != WMTP_VARIANT_PAGED_FULL && variant != WMTP_VARIANT_PAGED_WINDOWED) return 0;
+  if (variant == WMTP_VARIANT_PAGED_WINDOWED && check_window(W, sink) != WMTP_OK) return 0;
+  const int64_t per = variant == WMTP_VARIANT_PAGED_FULL
+                          ? table_stride
+                          : std::min<int64_t>(table_stride, static_cast<int64_t>(W) + sink);
+  return static_cast<int64_t>(B) * per;
+}
+
+WMTP_EXPORT int wmtp_build_kv_indices(const int32_t* req_to_token, const int32_t* lens, int B,
+                                      int64_t table_stride, int variant, int W, int sink,
+                                      int32_t* kv_indptr, int32_t* kv_indices, int64_t capacity,
+                                      int32_t* err, void* stream) {
+  if (B < 0 || B > 65535 || table_stride < 0 || table_stride > INT_MAX) return WMTP_EINVAL;
+  if (variant != WMTP_VARIANT_PAGED_FULL && variant != WMTP_VARIANT_PAGED_WINDOWED)
+    return WMTP_EINVAL;
+  const bool windowed = variant == WMTP_VARIANT_PAGED_WINDOWED;
+  if (windowed && check_window(W, sink) != WMTP_OK) return WMTP_EINVAL;
+  if (capacity < wmtp_kv_indices_capacity(variant, B, table_stride, W, sink)) return WMTP_EWORKSPACE;
+  if (capacity > INT_MAX) return WMTP_EUNSUPPORTED;  // int32 offsets in kv_indptr
+  if (B == 0) return WMTP_OK;
+  if (req_to_token == nullptr || lens == nullptr || kv_indptr == nullptr ||
+      (capacity > 0 && kv_indices == nullptr))
+    return WMTP_EINVAL;
+  if (!aligned(req_to_token, 4) || !aligned(lens, 4) || !aligned(kv_indptr, 4) ||
+      !aligned(kv_indices, 4) || (err != nullptr && !aligned(err, 4)))
+    return WMTP_EINVAL;
+  const int64_t n_keys_max = windowed ? std::min<int64_t>(table_stride, static_cast<int64_t>(W) + sink)
+                                      : table_stride;
+  if (wmtp::launch_kv_indices(req_to_token, table_stride, lens, B, windowed, W, sink, n_keys_max,
+                              kv_indptr, kv_indices, err,
+                              static_cast<hipStream_t>(stream)) != hipSuccess)
+    return WMTP_ELAUNCH;
+  return WMTP_OK;
 }
 
 WMTP_EXPORT int wmtp_ring_append(void* k_ring, void* v_ring, const void* k_new,

@@ -20,9 +20,12 @@ __all__ = [
     "VARIANT_FULL",
     "VARIANT_WINDOWED",
     "VARIANT_RING",
+    "VARIANT_PAGED_FULL",
+    "VARIANT_PAGED_WINDOWED",
     "DERR_LEN_RANGE",
     "DERR_NNEW_RANGE",
     "DERR_CAPACITY",
+    "DERR_SLOT_RANGE",
     "lib_path",
     "load_library",
     "workspace_bytes",
@@ -32,6 +35,9 @@ __all__ = [
     "draft_extend_full",
     "draft_extend_windowed",
     "ring_extend",
+    "paged_attn_full",
+    "paged_attn_windowed",
+    "build_kv_indices",
     "ring_append",
     "cache_append",
     "select_indices",
@@ -40,7 +46,8 @@ __all__ = [
 ]
 
 VARIANT_FULL, VARIANT_WINDOWED, VARIANT_RING = 0, 1, 2
-DERR_LEN_RANGE, DERR_NNEW_RANGE, DERR_CAPACITY = 0x1, 0x2, 0x4
+VARIANT_PAGED_FULL, VARIANT_PAGED_WINDOWED = 3, 4
+DERR_LEN_RANGE, DERR_NNEW_RANGE, DERR_CAPACITY, DERR_SLOT_RANGE = 0x1, 0x2, 0x4, 0x8
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, ELAUNCH = 0, 1, 2, 3, 4
 
 EXPORTED_SYMBOLS = (
@@ -51,6 +58,10 @@ EXPORTED_SYMBOLS = (
     "wmtp_draft_extend_full",
     "wmtp_draft_extend_windowed",
     "wmtp_ring_extend",
+    "wmtp_paged_attn_full",
+    "wmtp_paged_attn_windowed",
+    "wmtp_kv_indices_capacity",
+    "wmtp_build_kv_indices",
     "wmtp_ring_append",
     "wmtp_cache_append",
     "wmtp_select_indices",
@@ -75,6 +86,10 @@ _SIGNATURES = {
     "wmtp_draft_extend_full": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I64, _F, _P, _SZ, _P, _P]),
     "wmtp_draft_extend_windowed": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I64, _I, _I, _F, _P, _SZ, _P, _P]),
     "wmtp_ring_extend": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _SZ, _P, _P]),
+    "wmtp_paged_attn_full": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I64, _F, _P, _SZ, _P, _P]),
+    "wmtp_paged_attn_windowed": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I64, _I, _I, _F, _P, _SZ, _P, _P]),
+    "wmtp_kv_indices_capacity": (_I64, [_I, _I, _I64, _I, _I]),
+    "wmtp_build_kv_indices": (_I, [_P, _P, _I, _I64, _I, _I, _I, _P, _P, _I64, _P, _P]),
     "wmtp_ring_append": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
     "wmtp_cache_append": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I64, _I, _P, _P]),
     "wmtp_select_indices": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
@@ -296,6 +311,75 @@ def ring_extend(q, k_ring, v_ring, lens, W, sink, R_w, n_q=None, out=None, lse=N
         Hkv, d, W, sink, R_w, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
     _check(st, "wmtp_ring_extend")
     return out
+
+
+def _paged_io(q, k_pool, v_pool, table, lens, out, lse):
+    _need(q, "q", torch.bfloat16, 3)
+    dev = q.device
+    _need(k_pool, "k_pool", torch.bfloat16, 3, dev)
+    _need(v_pool, "v_pool", torch.bfloat16, 3, dev)
+    _need(table, "req_to_token", torch.int32, 2, dev)
+    _need(lens, "lens", torch.int32, 1, dev)
+    B, Hq, d = q.shape
+    if (k_pool.shape != v_pool.shape or k_pool.shape[2] != d or table.shape[0] != B
+            or lens.shape[0] != B):
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} pool {tuple(k_pool.shape)} "
+                         f"table {tuple(table.shape)} lens {tuple(lens.shape)}")
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need(out, "out", torch.bfloat16, 3, dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, 2, dev)
+    return dev, B, Hq, d, out
+
+
+def paged_attn_full(q, k_pool, v_pool, req_to_token, lens, out=None, lse=None, scale=None, ws=None,
+                    err=None):
+    """Full-context draft attention over a token pool [P, Hkv, d] read through req_to_token [B, C]."""
+    dev, B, Hq, d, out = _paged_io(q, k_pool, v_pool, req_to_token, lens, out, lse)
+    P, Hkv = k_pool.shape[0], k_pool.shape[1]
+    C = req_to_token.shape[1]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_PAGED_FULL, B, Hq, Hkv, d, C), dev)
+    st = load_library().wmtp_paged_attn_full(
+        _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(req_to_token), _ptr(lens), _ptr(out), _ptr(lse), B, Hq,
+        Hkv, d, P, C, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_paged_attn_full")
+    return out
+
+
+def paged_attn_windowed(q, k_pool, v_pool, req_to_token, lens, W, sink, out=None, lse=None, scale=None,
+                        ws=None, err=None):
+    """Sink + window draft attention over a token pool read through req_to_token."""
+    dev, B, Hq, d, out = _paged_io(q, k_pool, v_pool, req_to_token, lens, out, lse)
+    P, Hkv = k_pool.shape[0], k_pool.shape[1]
+    C = req_to_token.shape[1]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_PAGED_WINDOWED, B, Hq, Hkv, d, C, W, sink), dev)
+    st = load_library().wmtp_paged_attn_windowed(
+        _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(req_to_token), _ptr(lens), _ptr(out), _ptr(lse), B, Hq,
+        Hkv, d, P, C, W, sink, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_paged_attn_windowed")
+    return out
+
+
+def build_kv_indices(req_to_token, lens, variant, W=1, sink=0, indptr=None, indices=None, err=None):
+    """Packed index list (kv_indptr [B+1], kv_indices) of the kept keys' pool rows."""
+    _need(req_to_token, "req_to_token", torch.int32, 2)
+    dev = req_to_token.device
+    _need(lens, "lens", torch.int32, 1, dev)
+    B, C = req_to_token.shape
+    cap = int(load_library().wmtp_kv_indices_capacity(variant, B, C, W, sink))
+    if indptr is None:
+        indptr = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    if indices is None:
+        indices = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    st = load_library().wmtp_build_kv_indices(
+        _ptr(req_to_token), _ptr(lens), B, C, variant, W, sink, _ptr(indptr), _ptr(indices),
+        indices.numel(), _ptr(err), _stream(dev))
+    _check(st, "wmtp_build_kv_indices")
+    return indptr, indices
 
 
 def _append_io(k, v, k_new, v_new, n_new, lens):
