@@ -15,7 +15,9 @@ Timed variants (each its own timed region of --steps steps):
 the windowed and ring loops are captured once in a HIP graph and replayed.
 Also reported: windowed/full time per draft step at 128K, 256K, 512K and 1M
 (same cache, shorter lengths: the window's cost must not grow with S), and
-the float64 CPU oracle timed on a bounded sample on this host.
+the float64 CPU oracle timed on a bounded sample on this host, and context
+figures: draft-extend over gamma+1 new rows, the paged pool's KV-index build
+(native vs windowed) and paged attention over a shuffled pool.
 
 Prints one JSON line.  --gpus N with N > 1 is not supported (one GPU).
 """
@@ -215,6 +217,88 @@ def sweep_flatness(loop, lengths, reps=20):
     return rows
 
 
+def event_us(fn, reps=20, warm=5):
+    """Median HIP-event time of fn() in microseconds (long calls)."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in pairs:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) for a, b in pairs])) * 1e3
+
+
+def graph_us(fn, calls=50, reps=10):
+    """GPU time of one fn() in microseconds for calls too short to time one by
+    one: `calls` back-to-back calls captured in a HIP graph, the replay timed
+    with events, the median over `reps` replays divided by `calls`."""
+    fn()
+    torch.cuda.synchronize()
+    g = graph_of(lambda: [fn() for _ in range(calls)])
+    g.replay()
+    torch.cuda.synchronize()
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in pairs:
+        a.record()
+        g.replay()
+        b.record()
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) for a, b in pairs])) * 1e3 / calls
+
+
+def extras(loop):
+    """Context measurements at the 1M shape: draft-extend over gamma+1 new
+    rows, and the paged pool (page size 1): the draft's KV-index build
+    (native O(S) vs windowed O(sink+W)) and attention through req_to_token
+    over a pool whose rows are scattered at random."""
+    wl, dev = loop.wl, loop.dev
+    S = wl.S
+    loop.lens.copy_(loop.lens0)
+    rows = wl.gamma + 1
+    qx = I.normal_bf16((1, rows, wl.Hq, wl.d), I.stream_seed(wl.seed, I.STREAM_Q, 99), dev)
+    nq = torch.full((1,), rows, dtype=torch.int32, device=dev)
+    ext = {
+        "rows": rows,
+        "windowed_us": round(graph_us(lambda: W.draft_extend_windowed(qx, loop.k, loop.v, loop.lens, wl.W, wl.sink,
+                                                                      n_q=nq, scale=wl.scale)), 2),
+        "full_us": round(event_us(lambda: W.draft_extend_full(qx, loop.k, loop.v, loop.lens, n_q=nq,
+                                                              scale=wl.scale), reps=5, warm=2), 1),
+    }
+    log(f"extend ({rows} rows): windowed {ext['windowed_us']} us, full {ext['full_us']} us")
+    C = loop.S_max
+    g = torch.Generator(device="cpu").manual_seed(wl.seed)
+    table = torch.randperm(C, generator=g).to(torch.int32).view(1, C).to(dev)
+    kp = torch.empty((C, wl.Hkv, wl.d), dtype=torch.bfloat16, device=dev)
+    vp = torch.empty_like(kp)
+    kp[table[0].long()] = loop.k[0]
+    vp[table[0].long()] = loop.v[0]
+    indptr = torch.empty(2, dtype=torch.int32, device=dev)
+    idx = torch.empty(C, dtype=torch.int32, device=dev)
+    q = loop.q[0]
+    kv_bytes = S * wl.Hkv * wl.d * 4
+    paged = {
+        "kv_index_build_full_us": round(graph_us(lambda: W.build_kv_indices(
+            table, loop.lens, W.VARIANT_PAGED_FULL, indptr=indptr, indices=idx)), 2),
+        "kv_index_build_windowed_us": round(graph_us(lambda: W.build_kv_indices(
+            table, loop.lens, W.VARIANT_PAGED_WINDOWED, wl.W, wl.sink, indptr=indptr, indices=idx)), 2),
+        "full_us": round(event_us(lambda: W.paged_attn_full(q, kp, vp, table, loop.lens, scale=wl.scale),
+                                  reps=10, warm=3), 1),
+        "windowed_us": round(graph_us(lambda: W.paged_attn_windowed(q, kp, vp, table, loop.lens, wl.W, wl.sink,
+                                                                    scale=wl.scale)), 2),
+        "pool": "1M rows at a random permutation of pool slots",
+    }
+    paged["full_hbm_gbps"] = round(kv_bytes / paged["full_us"] / 1e3, 1)
+    log(f"paged: index build full {paged['kv_index_build_full_us']} us, windowed "
+        f"{paged['kv_index_build_windowed_us']} us; attention full {paged['full_us']} us, "
+        f"windowed {paged['windowed_us']} us")
+    del kp, vp
+    torch.cuda.empty_cache()
+    return {"extend": ext, "paged": paged}
+
+
 def cpu_baseline(loop, budget_s=20.0):
     """The float64 oracle on this host: full-context draft steps at 1M on a
     bounded sample (as many whole steps as fit the budget, at least one)."""
@@ -286,6 +370,7 @@ def main(argv=None):
     ap.add_argument("--workload", default="draft_loop_s1m", choices=sorted(I.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-extras", action="store_true", help="skip the extend / paged context figures")
     ap.add_argument("--only-full", action="store_true", help="time only the full-context loop (profiling)")
     ap.add_argument("--calib-copy", action="store_true", help="also run a 1 GiB device copy (counter calibration)")
     args = ap.parse_args(argv)
@@ -337,6 +422,7 @@ def main(argv=None):
         log(f"windowed: {win_us:.2f} us/draft step, ring: {ring_us:.2f} us/draft step (graph replay)")
         if not args.no_sweep:
             sweep = sweep_flatness(loop, [131072, 262144, 524288, 1048576])
+    extra = None if (args.only_full or args.no_extras) else extras(loop)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -379,6 +465,7 @@ def main(argv=None):
             "algorithmic_bytes_per_launch": alg_bytes,
         },
         "cpu_baseline": cpu,
+        "extras": extra,
         "paper_context": "B200: native draft-decode attention 1608 us per 6 forwards (268 us each), "
                          "windowed+ring 348 us (58 us each); per-decode-step gain +28..44% at 1M",
     })
