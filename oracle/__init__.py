@@ -14,6 +14,9 @@ Modules
   ring       -- the compact ring-buffer draft KV store: the slot map and an
                 operational replay of appends (Section 4 "Memory", Section 6
                 "Memory", the ring comment of the Appendix A pseudocode).
+  fp8        -- the fp8 (OCP E4M3, per-tensor scale) draft KV cache: code
+                values, quantization on append, attention over the
+                dequantized rows (Section 7, KV-cache quantization).
   paged      -- the paged token pool (page size 1): the draft's index list
                 req_to_token[r, keep] and attention over the listed rows
                 (Section 4 "Mechanism", Appendix A pseudocode).
@@ -26,4 +29,4 @@ against closed forms, brute force, invariants, a library routine
 (tests/golden/).
 """
 
-from . import attention, paged, ring  # noqa: F401
+from . import attention, fp8, paged, ring  # noqa: F401
