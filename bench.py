@@ -249,6 +249,46 @@ def graph_us(fn, calls=50, reps=10):
     return float(np.median([a.elapsed_time(b) for a, b in pairs])) * 1e3 / calls
 
 
+def queued_call_us(fn, before, reps=20):
+    """HIP-event time of one fn() that is queued behind `before()` (a kernel
+    long enough for the host to enqueue the events and fn's launches while it
+    runs, so the interval holds GPU time only).  Median over reps, in us."""
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    fn()
+    torch.cuda.synchronize()
+    for a, b in pairs:
+        before()
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) for a, b in pairs])) * 1e3
+
+
+def cache_figures(loop):
+    """Windowed and ring attention calls at 1M, hot (inputs left in L2/MALL by
+    the previous call) and cold (a 1 GiB buffer, four times the 256 MB
+    Infinity Cache, written between calls)."""
+    wl, dev = loop.wl, loop.dev
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    spin = lambda: torch.cuda._sleep(400_000)  # ~0.2 ms of clock spin, touches no memory
+    cold = lambda: flush.fill_(1)
+    loop.lens.copy_(loop.lens0)
+    loop.lens_r.copy_(loop.lens0)
+    win = lambda: W.draft_attn_windowed(loop.q[0], loop.k, loop.v, loop.lens, wl.W, wl.sink, out=loop.out[0],
+                                        ws=loop.ws_win, scale=wl.scale)
+    ring = lambda: W.ring_attn(loop.q[0], loop.kr, loop.vr, loop.lens_r, wl.W, wl.sink, loop.R_w,
+                               out=loop.out[0], ws=loop.ws_win, scale=wl.scale)
+    res = {}
+    for name, fn in (("windowed", win), ("ring", ring)):
+        res[f"{name}_attention_call_hot_us"] = round(queued_call_us(fn, spin), 2)
+        res[f"{name}_attention_call_cold_us"] = round(queued_call_us(fn, cold), 2)
+    log("attention call (hot / cold): " + ", ".join(f"{k}={v}" for k, v in res.items()))
+    del flush
+    torch.cuda.empty_cache()
+    return res
+
+
 def extras(loop):
     """Context measurements at the 1M shape: draft-extend over gamma+1 new
     rows, and the paged pool (page size 1): the draft's KV-index build
@@ -296,7 +336,37 @@ def extras(loop):
         f"windowed {paged['windowed_us']} us")
     del kp, vp
     torch.cuda.empty_cache()
-    return {"extend": ext, "paged": paged}
+    return {"extend": ext, "paged": paged, "fp8": fp8_figures(loop)}
+
+
+def fp8_figures(loop):
+    """The same 1M draft attention over an fp8 (E4M3) cache: the cache holds
+    torch's E4M3 rounding of the bf16 cache (scales 1), half the bytes."""
+    wl, dev = loop.wl, loop.dev
+    S = wl.S
+    loop.lens.copy_(loop.lens0)
+    k8 = I.fp8_codes(loop.k)
+    v8 = I.fp8_codes(loop.v)
+    kr8 = I.fp8_codes(loop.kr)
+    vr8 = I.fp8_codes(loop.vr)
+    loop.lens_r.copy_(loop.lens0)
+    q = loop.q[0]
+    out = loop.out[0]
+    full = event_us(lambda: W.draft_attn_full_fp8(q, k8, v8, loop.lens, out=out, ws=loop.ws_full,
+                                                  scale=wl.scale), reps=20, warm=3)
+    win = graph_us(lambda: W.draft_attn_windowed_fp8(q, k8, v8, loop.lens, wl.W, wl.sink, out=out,
+                                                     ws=loop.ws_win, scale=wl.scale))
+    ring = graph_us(lambda: W.ring_attn_fp8(q, kr8, vr8, loop.lens_r, wl.W, wl.sink, loop.R_w, out=out,
+                                            ws=loop.ws_win, scale=wl.scale))
+    alg = wl.B * S * wl.Hkv * wl.d * 2 + 2 * wl.B * wl.Hq * wl.d * 2  # K+V codes + q + out
+    res = {"full_attention_call_us": round(full, 1), "full_hbm_gbps": round(alg / full / 1e3, 1),
+           "full_frac_of_peak": round(alg / full / 1e3 / HBM_PEAK_GBPS, 4),
+           "windowed_attention_call_us": round(win, 2), "ring_attention_call_us": round(ring, 2),
+           "algorithmic_bytes_full": alg}
+    log(f"fp8: full {full:.1f} us ({res['full_hbm_gbps']} GB/s), windowed {win:.2f} us, ring {ring:.2f} us")
+    del k8, v8, kr8, vr8
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(loop, budget_s=20.0):
@@ -408,7 +478,7 @@ def main(argv=None):
 
     res = {"metric": METRIC}
     win_us = ring_us = None
-    sweep = None
+    sweep = caches = None
     if not args.only_full:
         loop.lens.copy_(loop.lens0)
         gw = graph_of(loop.step_windowed)
@@ -422,6 +492,7 @@ def main(argv=None):
         log(f"windowed: {win_us:.2f} us/draft step, ring: {ring_us:.2f} us/draft step (graph replay)")
         if not args.no_sweep:
             sweep = sweep_flatness(loop, [131072, 262144, 524288, 1048576])
+        caches = cache_figures(loop)
     extra = None if (args.only_full or args.no_extras) else extras(loop)
 
     cpu = None
@@ -452,6 +523,7 @@ def main(argv=None):
         "ring_us_per_step": None if ring_us is None else round(ring_us, 2),
         "windowed_speedup_vs_full": None if win_us is None else round(us_full_step / win_us, 1),
         "flatness_sweep": sweep,
+        "windowed_hot_cold": caches,
         "windowed_flatness_max_over_min": None if not sweep else round(
             max(r["windowed_us_per_step"] for r in sweep) / min(r["windowed_us_per_step"] for r in sweep), 3),
         "roofline": {

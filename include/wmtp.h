@@ -244,13 +244,69 @@ int wmtp_cache_append(void* k, void* v, const void* k_new, const void* v_new,
 int wmtp_select_indices(const int32_t* lens, int B, int W, int sink, int R_w, int32_t* pos_out,
                         int32_t* slot_out, int32_t* n_sel_out, int32_t* err, void* stream);
 
+/*
+ * fp8 draft KV cache (Section 7, KV-cache quantization: the windowing
+ * composes with fp8 KV; the dtype sets the bytes per entry, windowing the
+ * number of entries read).  Format: OCP E4M3 ("e4m3fn": bias 7, subnormals,
+ * no infinities, largest finite 448), one byte per element, with one float32
+ * scale per tensor: code c of the key cache stands for value(c) * k_scale,
+ * of the value cache for value(c) * v_scale.  Layouts are those of the bf16
+ * cache with 1-byte elements ([B, S_max, Hkv, d] dense, [B, sink + R_w, Hkv,
+ * d] ring), 16-byte aligned.  q, out and lse are as for the bf16 calls, and
+ * so is the workspace (wmtp_workspace_bytes of the same variant).
+ *
+ * Attention: the same definition over the dequantized cache.  Codes are
+ * widened to bf16 exactly (every E4M3 value is a bf16 value); k_scale is
+ * folded into the logit scale, v_scale into the output normalisation.
+ * k_scale and v_scale must be finite and positive (else WMTP_EINVAL).
+ */
+int wmtp_draft_attn_full_fp8(const void* q, const void* k, const void* v, const int32_t* lens,
+                             void* out, float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
+                             float scale, float k_scale, float v_scale, void* ws, size_t ws_bytes,
+                             int32_t* err, void* stream);
+int wmtp_draft_attn_windowed_fp8(const void* q, const void* k, const void* v, const int32_t* lens,
+                                 void* out, float* lse, int B, int Hq, int Hkv, int d,
+                                 int64_t S_max, int W, int sink, float scale, float k_scale,
+                                 float v_scale, void* ws, size_t ws_bytes, int32_t* err,
+                                 void* stream);
+int wmtp_ring_attn_fp8(const void* q, const void* k_ring, const void* v_ring, const int32_t* lens,
+                       void* out, float* lse, int B, int Hq, int Hkv, int d, int W, int sink,
+                       int R_w, float scale, float k_scale, float v_scale, void* ws,
+                       size_t ws_bytes, int32_t* err, void* stream);
+
+/*
+ * fp8 appends: as wmtp_ring_append / wmtp_cache_append, with the bf16 rows
+ * quantised on the way in.  Element x of a key row is stored as the E4M3
+ * code nearest to x / k_scale (division in float32, correctly rounded),
+ * saturated to +-448, ties to the even code; values likewise with v_scale.
+ * Non-finite inputs are outside the contract.
+ */
+int wmtp_ring_append_fp8(void* k_ring, void* v_ring, const void* k_new, const void* v_new,
+                         const int32_t* n_new, int32_t* lens, int B, int Hkv, int d, int sink,
+                         int R_w, int n_max, float k_scale, float v_scale, int32_t* err,
+                         void* stream);
+int wmtp_cache_append_fp8(void* k, void* v, const void* k_new, const void* v_new,
+                          const int32_t* n_new, int32_t* lens, int B, int Hkv, int d,
+                          int64_t S_max, int n_max, float k_scale, float v_scale, int32_t* err,
+                          void* stream);
+
+/*
+ * The fp8 format's element conversions, as the appends and the attention
+ * kernels perform them (for tests and for filling a cache in bulk):
+ * quantize writes codes[i] for bf16 x[i] with `scale` (the appends' rule);
+ * dequantize writes the bf16 value of codes[i] (exact; NaN codes give NaN).
+ * n must be a multiple of 8; x and out 16-byte, codes 8-byte aligned.
+ */
+int wmtp_fp8_quantize(const void* x, int64_t n, float scale, void* codes, void* stream);
+int wmtp_fp8_dequantize(const void* codes, int64_t n, void* out, void* stream);
+
 /* Human-readable name of a wmtp_status value (static string). */
 const char* wmtp_status_string(int status);
 
 /* ABI version of this header, (major << 16) | minor. */
 int wmtp_abi_version(void);
 
-#define WMTP_ABI_VERSION ((1 << 16) | 0)
+#define WMTP_ABI_VERSION ((1 << 16) | 1)
 
 #ifdef __cplusplus
 }

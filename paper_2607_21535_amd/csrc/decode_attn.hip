@@ -36,12 +36,14 @@
 
 #include "../../include/wmtp.h"
 #include "common.h"
+#include "fp8.h"
 #include "index_map.h"
 #include "launch.h"
 
 #include <algorithm>
 #include <atomic>
 #include <cstdlib>
+#include <type_traits>
 
 #ifndef WMTP_CHUNK_MAX_DEFAULT
 #define WMTP_CHUNK_MAX_DEFAULT 9216
@@ -55,8 +57,8 @@ constexpr int kPagedChunkMax = 9216;  // largest work item of a paged call (its 
 
 struct SplitArgs {
   const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
+  const void* k;  // bf16 or fp8 elements
+  const void* v;
   const int32_t* lens;
   float* pm;
   float* pl;
@@ -90,6 +92,7 @@ struct MergeArgs {
   int qps;
   int64_t len_cap;
   int W, sink, target, chunk_cap;
+  float out_scale;  // value scale of an fp8 cache (1 for bf16)
 };
 
 __device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap, int32_t* err,
@@ -214,8 +217,8 @@ __device__ bool locate_item(const SplitArgs& a, int item, int& v_out, int& c_out
 #endif
 
 // Streaming loads of the KV cache (read once per call).
-template <typename T>
-__device__ __forceinline__ T stream_load(const uint16_t* p) {
+template <typename T, typename E>
+__device__ __forceinline__ T stream_load(const E* p) {
 #if WMTP_NT_LOADS
   return __builtin_nontemporal_load(reinterpret_cast<const T*>(p));
 #else
@@ -223,16 +226,32 @@ __device__ __forceinline__ T stream_load(const uint16_t* p) {
 #endif
 }
 
+// Registers of one 16-key tile on one lane.  bf16: kx holds the key's d
+// chunk kk*32 + grp*8 (8 values) and vx the lane's VEC values of keys
+// 4*grp + i as words.  fp8: kx holds 16-byte pieces kk2*4 + grp of the key
+// (16 codes, two MFMA steps each) and vx the lane's VEC codes of each key.
+template <int D, bool F8>
+struct TileRegs {
+  u32x4 kx[D / 32];
+  uint32_t vx[4][D / 32];
+};
+template <int D>
+struct TileRegs<D, true> {
+  u32x4 kx[D / 64];
+  uint32_t vx[4][D / 64];
+};
+
 // Two waves per SIMD at d = 256 (the kernel fits 256 registers per lane):
 // two workgroups share a CU, so one waits on memory while the other computes.
-template <int D, KeyMap M>
+template <int D, KeyMap M, bool F8>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void split_kernel(SplitArgs a) {
+  using KT = std::conditional_t<F8, uint8_t, uint16_t>;  // one cached K/V element
   constexpr int VEC = D / 16;  // d values of one key per lane in the PV operand
-  constexpr int VW = VEC / 2;  // ... as 32-bit words
   // A lane's VEC values come in pieces of SEG contiguous d values (16 bytes at
   // most); piece s of lane col starts at d = s*16*SEG + SEG*col, so the 16
   // lanes of one key read 16*SEG contiguous values per load instruction.
-  constexpr int SEG = VEC < 8 ? VEC : 8;
+  // fp8: one piece of VEC codes (at most 16 bytes).
+  constexpr int SEG = F8 ? VEC : (VEC < 8 ? VEC : 8);
   constexpr int NSEG = VEC / SEG;
   constexpr int KCH = D / 32;  // 16x16x32 steps over d for the logits
   constexpr int OPAD = kWave + 1;
@@ -262,8 +281,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // shared array of rows indexed by the request's token table.
   const int64_t seq_rows = is_paged(M) ? 0 : static_cast<int64_t>(b) * a.rows;
   const int64_t seq_off = (seq_rows * a.Hkv + g) * D;
-  const uint16_t* kbase = a.k + seq_off;
-  const uint16_t* vbase = a.v + seq_off;
+  const KT* kbase = static_cast<const KT*>(a.k) + seq_off;
+  const KT* vbase = static_cast<const KT*>(a.v) + seq_off;
 
   // Paged: the pool rows of this item's keys, looked up once into LDS.
   [[maybe_unused]] int* slots = nullptr;
@@ -291,24 +310,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
   };
 
-  // Q^T operand: lane (grp, col) holds q[b, g*G + col, kk*32 + grp*8 .. +8].
+  // Q^T operand: lane (grp, col) holds at step kk the 8 d values of head col
+  // that the key operand holds: d = kk*32 + grp*8 (bf16 keys) or
+  // (kk/2*4 + grp)*16 + (kk%2)*8 (fp8 keys: 16 codes per load).
   bf16x8 qf[KCH];
   {
     const bool live = col < a.G;
-    const uint16_t* qp =
-        a.q + (static_cast<int64_t>(v) * a.Hq + g * a.G + (live ? col : 0)) * D + grp * 8;
+    const uint16_t* qp = a.q + (static_cast<int64_t>(v) * a.Hq + g * a.G + (live ? col : 0)) * D;
 #pragma unroll
     for (int kk = 0; kk < KCH; ++kk) {
-      u32x4 w = *reinterpret_cast<const u32x4*>(qp + kk * 32);
+      const int d0 = F8 ? ((kk >> 1) * 4 + grp) * 16 + (kk & 1) * 8 : kk * 32 + grp * 8;
+      u32x4 w = *reinterpret_cast<const u32x4*>(qp + d0);
       if (!live) w = u32x4{0u, 0u, 0u, 0u};
       qf[kk] = __builtin_bit_cast(bf16x8, w);
     }
   }
 
-  struct Tile {
-    u32x4 kx[KCH];       // key (col) : d chunk kk*32 + grp*8
-    uint32_t vx[4][VW];  // key 4*grp + i : NSEG pieces of SEG values
-  };
+  using Tile = TileRegs<D, F8>;
 
   const int n_tiles = (j1 - j0 + kTileKeys - 1) / kTileKeys;
 
@@ -321,25 +339,45 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     {
       const int j = jt + col;
       const int r = row_of(j < j1 ? j : j0);
-      const uint16_t* p = kbase + static_cast<int64_t>(r) * rs + grp * 8;
+      if constexpr (F8) {
+        const KT* p = kbase + static_cast<int64_t>(r) * rs + grp * 16;
 #pragma unroll
-      for (int kk = 0; kk < KCH; ++kk) T.kx[kk] = stream_load<u32x4>(p + kk * 32);
+        for (int kk = 0; kk < D / 64; ++kk) T.kx[kk] = stream_load<u32x4>(p + kk * 64);
+      } else {
+        const KT* p = kbase + static_cast<int64_t>(r) * rs + grp * 8;
+#pragma unroll
+        for (int kk = 0; kk < KCH; ++kk) T.kx[kk] = stream_load<u32x4>(p + kk * 32);
+      }
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = jt + 4 * grp + i;
       const int r = row_of(j < j1 ? j : j0);
-      const uint16_t* p = vbase + static_cast<int64_t>(r) * rs + SEG * col;
+      const KT* p = vbase + static_cast<int64_t>(r) * rs + SEG * col;
+      if constexpr (F8) {
+        if constexpr (VEC == 16) {
+          const u32x4 x = stream_load<u32x4>(p);
 #pragma unroll
-      for (int sg = 0; sg < NSEG; ++sg) {
-        if constexpr (SEG == 8) {
-          const u32x4 x = stream_load<u32x4>(p + sg * 16 * SEG);
-#pragma unroll
-          for (int w = 0; w < 4; ++w) T.vx[i][sg * 4 + w] = x[w];
+          for (int w = 0; w < 4; ++w) T.vx[i][w] = x[w];
+        } else if constexpr (VEC == 8) {
+          const u32x2 x = stream_load<u32x2>(p);
+          T.vx[i][0] = x[0];
+          T.vx[i][1] = x[1];
         } else {
-          const u32x2 x = stream_load<u32x2>(p + sg * 16 * SEG);
-          T.vx[i][sg * 2] = x[0];
-          T.vx[i][sg * 2 + 1] = x[1];
+          T.vx[i][0] = stream_load<uint32_t>(p);
+        }
+      } else {
+#pragma unroll
+        for (int sg = 0; sg < NSEG; ++sg) {
+          if constexpr (SEG == 8) {
+            const u32x4 x = stream_load<u32x4>(p + sg * 16 * SEG);
+#pragma unroll
+            for (int w = 0; w < 4; ++w) T.vx[i][sg * 4 + w] = x[w];
+          } else {
+            const u32x2 x = stream_load<u32x2>(p + sg * 16 * SEG);
+            T.vx[i][sg * 2] = x[0];
+            T.vx[i][sg * 2 + 1] = x[1];
+          }
         }
       }
     }
@@ -356,10 +394,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   auto compute_tile = [&](const Tile& T, int t) {
     const int jt = j0 + t * kTileKeys;
     floatx4 s = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (F8) {
+      // 16 codes per piece: widened to bf16 (exact), two steps each.
 #pragma unroll
-    for (int kk = 0; kk < KCH; ++kk)
-      s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, T.kx[kk]), qf[kk], s,
-                                                  0, 0, 0);
+      for (int kk = 0; kk < D / 64; ++kk) {
+        const u32x4 w = T.kx[kk];
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fp8x8_to_bf16x8(w[0], w[1])),
+                                                    qf[2 * kk], s, 0, 0, 0);
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fp8x8_to_bf16x8(w[2], w[3])),
+                                                    qf[2 * kk + 1], s, 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < KCH; ++kk)
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, T.kx[kk]), qf[kk], s,
+                                                    0, 0, 0);
+    }
     // s[i] = logit of key jt + 4*grp + i for head col
     float sv[4];
     float mt = neg_inf();
@@ -392,15 +442,35 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       z_run += p0 + p1;
     }
     const bf16x4 pop = __builtin_bit_cast(bf16x4, u32x2{pb[0], pb[1]});
-    // V^T operand for output tile e: this lane's four keys at its value
-    // column e, packed from the loaded rows (low or high halves of a word).
+    if constexpr (F8) {
+      // V^T operand for output tiles 4w .. 4w+3: interleave the codes of keys
+      // (0, 1) and (2, 3) byte by byte, then widen pairs to bf16.
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-      const uint32_t a01 = __builtin_amdgcn_perm(T.vx[1][e >> 1], T.vx[0][e >> 1], sel);
-      const uint32_t a23 = __builtin_amdgcn_perm(T.vx[3][e >> 1], T.vx[2][e >> 1], sel);
-      acc[e] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, u32x2{a01, a23}),
-                                                        pop, acc[e], 0, 0, 0);
+      for (int w = 0; w < VEC / 4; ++w) {
+        const uint32_t p01 = __builtin_amdgcn_perm(T.vx[1][w], T.vx[0][w], 0x05010400u);
+        const uint32_t q01 = __builtin_amdgcn_perm(T.vx[1][w], T.vx[0][w], 0x07030602u);
+        const uint32_t p23 = __builtin_amdgcn_perm(T.vx[3][w], T.vx[2][w], 0x05010400u);
+        const uint32_t q23 = __builtin_amdgcn_perm(T.vx[3][w], T.vx[2][w], 0x07030602u);
+        const uint32_t lo01[4] = {fp8x2_to_bf16x2<false>(p01), fp8x2_to_bf16x2<true>(p01),
+                                  fp8x2_to_bf16x2<false>(q01), fp8x2_to_bf16x2<true>(q01)};
+        const uint32_t lo23[4] = {fp8x2_to_bf16x2<false>(p23), fp8x2_to_bf16x2<true>(p23),
+                                  fp8x2_to_bf16x2<false>(q23), fp8x2_to_bf16x2<true>(q23)};
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+          acc[4 * w + x] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+              __builtin_bit_cast(bf16x4, u32x2{lo01[x], lo23[x]}), pop, acc[4 * w + x], 0, 0, 0);
+      }
+    } else {
+      // V^T operand for output tile e: this lane's four keys at its value
+      // column e, packed from the loaded rows (low or high halves of a word).
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+        const uint32_t a01 = __builtin_amdgcn_perm(T.vx[1][e >> 1], T.vx[0][e >> 1], sel);
+        const uint32_t a23 = __builtin_amdgcn_perm(T.vx[3][e >> 1], T.vx[2][e >> 1], sel);
+        acc[e] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, u32x2{a01, a23}),
+                                                          pop, acc[e], 0, 0, 0);
+      }
     }
   };
 
@@ -583,7 +653,7 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
     const floatx4 ot = s_o[0][q4];
     float r[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) r[i] = n > 0 ? ot[i] / Lt : 0.f;
+    for (int i = 0; i < 4; ++i) r[i] = n > 0 ? ot[i] / Lt * a.out_scale : 0.f;
     const uint32_t lo = f32_to_bf16_rne(r[0]) | (uint32_t(f32_to_bf16_rne(r[1])) << 16);
     const uint32_t hi = f32_to_bf16_rne(r[2]) | (uint32_t(f32_to_bf16_rne(r[3])) << 16);
     *reinterpret_cast<u32x2*>(a.out + (static_cast<int64_t>(v) * a.Hq + h) * D + d0) = u32x2{lo, hi};
@@ -592,7 +662,7 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
   }
 }
 
-template <int D, KeyMap M>
+template <int D, KeyMap M, bool F8>
 hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   const int G = L.Hq / L.Hkv;
   if (L.max_items > 0) {
@@ -604,9 +674,9 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
     a.rows = L.rows; a.len_cap = L.len_cap;
     a.W = L.W; a.sink = L.sink; a.R_w = L.R_w;
     a.target = L.target; a.chunk_cap = L.chunk_cap;
-    a.scale_log2 = L.scale * kLog2e;
+    a.scale_log2 = L.scale * L.k_scale * kLog2e;
     const dim3 grid(static_cast<unsigned>(L.max_items) * static_cast<unsigned>(L.Hkv));
-    hipLaunchKernelGGL((split_kernel<D, M>), grid, dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((split_kernel<D, M, F8>), grid, dim3(kThreads), 0, st, a);
   }
   // Items per sequence the plan allows decide the merge shape.
   const int64_t NV = static_cast<int64_t>(L.B) * L.qps;
@@ -617,6 +687,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   m.B = L.B; m.Hq = L.Hq; m.Hkv = L.Hkv; m.G = G;
   m.len_cap = L.len_cap; m.W = L.W; m.sink = L.sink;
   m.target = L.target; m.chunk_cap = L.chunk_cap;
+  m.out_scale = L.v_scale;
   const unsigned bh = static_cast<unsigned>(NV) * static_cast<unsigned>(L.Hq);
   if (wide)
     hipLaunchKernelGGL((merge_kernel<D, M, kMergeThreads, 64>), dim3(bh, D / 64), dim3(kMergeThreads), 0,
@@ -628,12 +699,20 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
 
 template <int D>
 hipError_t launch_d(const AttnLaunch& L, hipStream_t st) {
+  if (L.kv_fp8) {
+    switch (L.variant) {
+      case WMTP_VARIANT_FULL: return launch_typed<D, KeyMap::Full, true>(L, st);
+      case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::Window, true>(L, st);
+      case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::Ring, true>(L, st);
+      default: return hipErrorInvalidValue;  // no fp8 paged kernels
+    }
+  }
   switch (L.variant) {
-    case WMTP_VARIANT_FULL: return launch_typed<D, KeyMap::Full>(L, st);
-    case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::Window>(L, st);
-    case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::Ring>(L, st);
-    case WMTP_VARIANT_PAGED_FULL: return launch_typed<D, KeyMap::PagedFull>(L, st);
-    default: return launch_typed<D, KeyMap::PagedWindow>(L, st);
+    case WMTP_VARIANT_FULL: return launch_typed<D, KeyMap::Full, false>(L, st);
+    case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::Window, false>(L, st);
+    case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::Ring, false>(L, st);
+    case WMTP_VARIANT_PAGED_FULL: return launch_typed<D, KeyMap::PagedFull, false>(L, st);
+    default: return launch_typed<D, KeyMap::PagedWindow, false>(L, st);
   }
 }
 
@@ -656,7 +735,7 @@ template <int D>
 int query_resident_groups(int dev) {
   int cus = 0, per_cu = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, split_kernel<D, KeyMap::Full>, kThreads,
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, split_kernel<D, KeyMap::Full, false>, kThreads,
                                                    0) != hipSuccess)
     return 0;
   return cus * per_cu;

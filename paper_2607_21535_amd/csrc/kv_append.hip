@@ -11,17 +11,19 @@
 
 #include "../../include/wmtp.h"
 #include "common.h"
+#include "fp8.h"
 #include "index_map.h"
 #include "launch.h"
 
+#include <algorithm>
 #include <climits>
 
 namespace wmtp {
 namespace {
 
 struct AppendArgs {
-  uint16_t* k;
-  uint16_t* v;
+  void* k;  // bf16 or E4M3 elements
+  void* v;
   const uint16_t* k_new;
   const uint16_t* v_new;
   const int32_t* n_new;
@@ -30,9 +32,10 @@ struct AppendArgs {
   int B, Hkv, d;
   int64_t rows;
   int sink, R_w, n_max;
+  float k_scale, v_scale;  // fp8: per-tensor scales the rows are divided by
 };
 
-template <bool RING>
+template <bool RING, bool F8>
 __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
   const int b = blockIdx.x;
   const int64_t cap = RING ? static_cast<int64_t>(INT_MAX) : a.rows;
@@ -79,8 +82,15 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
     const int slot = RING ? (p < a.sink ? p : a.sink + (p - a.sink) % a.R_w) : p;
     const int64_t src = src_seq + static_cast<int64_t>(i) * row_elems + off;
     const int64_t dst = dst_seq + static_cast<int64_t>(slot) * row_elems + off;
-    *reinterpret_cast<u32x4*>(a.k + dst) = *reinterpret_cast<const u32x4*>(a.k_new + src);
-    *reinterpret_cast<u32x4*>(a.v + dst) = *reinterpret_cast<const u32x4*>(a.v_new + src);
+    const u32x4 kx = *reinterpret_cast<const u32x4*>(a.k_new + src);
+    const u32x4 vx = *reinterpret_cast<const u32x4*>(a.v_new + src);
+    if constexpr (F8) {
+      *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(a.k) + dst) = bf16x8_to_fp8x8(kx, a.k_scale);
+      *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(a.v) + dst) = bf16x8_to_fp8x8(vx, a.v_scale);
+    } else {
+      *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.k) + dst) = kx;
+      *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.v) + dst) = vx;
+    }
   }
   __syncthreads();  // every thread has read lens[b] before it changes
   if (threadIdx.x == 0) a.lens[b] = S_new;
@@ -111,6 +121,25 @@ __global__ __launch_bounds__(256) void select_kernel(const int32_t* lens, int W,
   if (threadIdx.x == 0) n_sel_out[b] = n;
 }
 
+// The conversion exports run the appends' quantiser and the attention's
+// widening on flat arrays, 8 elements per thread and step.
+__global__ __launch_bounds__(256) void fp8_quantize_kernel(const uint16_t* x, int64_t units, float scale,
+                                                          uint8_t* codes) {
+  for (int64_t u = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; u < units;
+       u += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    *reinterpret_cast<u32x2*>(codes + u * 8) =
+        bf16x8_to_fp8x8(*reinterpret_cast<const u32x4*>(x + u * 8), scale);
+}
+
+__global__ __launch_bounds__(256) void fp8_dequantize_kernel(const uint8_t* codes, int64_t units,
+                                                            uint16_t* out) {
+  for (int64_t u = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; u < units;
+       u += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const u32x2 c = *reinterpret_cast<const u32x2*>(codes + u * 8);
+    *reinterpret_cast<u32x4*>(out + u * 8) = fp8x8_to_bf16x8(c[0], c[1]);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_append(const AppendLaunch& L, hipStream_t st) {
@@ -119,10 +148,36 @@ hipError_t launch_append(const AppendLaunch& L, hipStream_t st) {
   a.n_new = L.n_new; a.lens = L.lens; a.err = L.err;
   a.B = L.B; a.Hkv = L.Hkv; a.d = L.d; a.rows = L.rows;
   a.sink = L.sink; a.R_w = L.R_w; a.n_max = L.n_max;
-  if (L.ring)
-    hipLaunchKernelGGL(append_kernel<true>, dim3(L.B), dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL(append_kernel<false>, dim3(L.B), dim3(256), 0, st, a);
+  a.k_scale = L.k_scale; a.v_scale = L.v_scale;
+  const dim3 grid(L.B), block(256);
+  if (L.ring) {
+    if (L.fp8)
+      hipLaunchKernelGGL((append_kernel<true, true>), grid, block, 0, st, a);
+    else
+      hipLaunchKernelGGL((append_kernel<true, false>), grid, block, 0, st, a);
+  } else {
+    if (L.fp8)
+      hipLaunchKernelGGL((append_kernel<false, true>), grid, block, 0, st, a);
+    else
+      hipLaunchKernelGGL((append_kernel<false, false>), grid, block, 0, st, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fp8_quantize(const uint16_t* x, int64_t n, float scale, uint8_t* codes,
+                               hipStream_t st) {
+  const int64_t units = n / 8;
+  if (units == 0) return hipSuccess;
+  const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((units + 255) / 256, 65536));
+  hipLaunchKernelGGL(fp8_quantize_kernel, dim3(blocks), dim3(256), 0, st, x, units, scale, codes);
+  return hipGetLastError();
+}
+
+hipError_t launch_fp8_dequantize(const uint8_t* codes, int64_t n, uint16_t* out, hipStream_t st) {
+  const int64_t units = n / 8;
+  if (units == 0) return hipSuccess;
+  const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((units + 255) / 256, 65536));
+  hipLaunchKernelGGL(fp8_dequantize_kernel, dim3(blocks), dim3(256), 0, st, codes, units, out);
   return hipGetLastError();
 }
 

@@ -9,9 +9,10 @@ namespace wmtp {
 // One attention call, already validated on the host.
 struct AttnLaunch {
   int variant;  // wmtp_variant
+  bool kv_fp8;  // K/V are E4M3 codes (dense or ring variants) instead of bf16
   const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
+  const void* k;
+  const void* v;
   const int32_t* lens;
   const int32_t* n_q;  // new query rows per sequence, or NULL (all qps rows)
   int qps;             // query rows per sequence (1 for a draft decode step)
@@ -25,6 +26,7 @@ struct AttnLaunch {
   int64_t len_cap;  // largest valid lens[b]
   int W, sink, R_w;
   float scale;
+  float k_scale, v_scale;  // per-tensor scales of an fp8 cache (1 for bf16)
   // split plan (from plan_split)
   int target;     // work items per KV head to aim for
   int chunk_cap;  // largest work item, in keys
@@ -59,8 +61,9 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t stream);
 
 struct AppendLaunch {
   bool ring;
-  uint16_t* k;
-  uint16_t* v;
+  bool fp8;  // quantise the bf16 rows to E4M3 codes (k_scale, v_scale)
+  void* k;
+  void* v;
   const uint16_t* k_new;
   const uint16_t* v_new;
   const int32_t* n_new;
@@ -69,9 +72,16 @@ struct AppendLaunch {
   int B, Hkv, d;
   int64_t rows;     // dense: S_max; ring: sink + R_w
   int sink, R_w, n_max;
+  float k_scale, v_scale;
 };
 
 hipError_t launch_append(const AppendLaunch& a, hipStream_t stream);
+
+// Elementwise conversions of the fp8 cache format (the appends' quantiser and
+// the attention's widening), n a multiple of 8.
+hipError_t launch_fp8_quantize(const uint16_t* x, int64_t n, float scale, uint8_t* codes,
+                               hipStream_t stream);
+hipError_t launch_fp8_dequantize(const uint8_t* codes, int64_t n, uint16_t* out, hipStream_t stream);
 
 hipError_t launch_select(const int32_t* lens, int B, int W, int sink, int R_w, int32_t* pos_out,
                          int32_t* slot_out, int32_t* n_sel_out, int32_t* err, hipStream_t stream);

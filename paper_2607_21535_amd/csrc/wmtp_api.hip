@@ -52,6 +52,9 @@ bool paged_variant(int variant) {
   return variant == WMTP_VARIANT_PAGED_FULL || variant == WMTP_VARIANT_PAGED_WINDOWED;
 }
 
+// A per-tensor scale of an fp8 cache: finite and positive.
+bool valid_scale(float s) { return std::isfinite(s) && s > 0.0f; }
+
 bool plan_fits(const SplitPlan& p, int Hkv) {
   return static_cast<int64_t>(p.max_items) * Hkv < INT_MAX;
 }
@@ -65,9 +68,14 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
                      const int32_t* lens, const int32_t* n_q, int q_max, void* out, float* lse,
                      int B, int Hq, int Hkv, int d, int64_t S_max, int W, int sink, int R_w,
                      float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream,
-                     const int32_t* table = nullptr, int64_t pool_rows = 0) {
+                     const int32_t* table = nullptr, int64_t pool_rows = 0, bool fp8 = false,
+                     float k_scale = 1.0f, float v_scale = 1.0f) {
   int st = check_heads(B, Hq, Hkv, d);
   if (st != WMTP_OK) return st;
+  if (fp8) {
+    if (paged_variant(variant)) return WMTP_EUNSUPPORTED;
+    if (!valid_scale(k_scale) || !valid_scale(v_scale)) return WMTP_EINVAL;
+  }
   if (q_max < 1 || q_max > kMaxQueryRows) return WMTP_EINVAL;
   if (static_cast<int64_t>(B) * q_max > INT_MAX / 64) return WMTP_EINVAL;
   if (windowed_variant(variant)) {
@@ -79,7 +87,7 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   if (variant == WMTP_VARIANT_RING && static_cast<int64_t>(R_w) < static_cast<int64_t>(W) + q_max - 1)
     return WMTP_EINVAL;
   if (S_max < 0) return WMTP_EINVAL;
-  if (!std::isfinite(scale)) return WMTP_EINVAL;
+  if (!std::isfinite(scale) || !std::isfinite(scale * k_scale)) return WMTP_EINVAL;
   if (B == 0) return WMTP_OK;
   if (q == nullptr || k == nullptr || v == nullptr || lens == nullptr || out == nullptr)
     return WMTP_EINVAL;
@@ -98,9 +106,10 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
 
   AttnLaunch L{};
   L.variant = variant;
+  L.kv_fp8 = fp8;
   L.q = static_cast<const uint16_t*>(q);
-  L.k = static_cast<const uint16_t*>(k);
-  L.v = static_cast<const uint16_t*>(v);
+  L.k = k;
+  L.v = v;
   L.lens = lens;
   L.n_q = n_q;
   L.qps = q_max;
@@ -127,6 +136,8 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   L.sink = sink;
   L.R_w = R_w;
   L.scale = scale;
+  L.k_scale = k_scale;
+  L.v_scale = v_scale;
   L.target = plan.target;
   L.chunk_cap = plan.chunk_cap;
   L.max_items = plan.max_items;
@@ -142,8 +153,10 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
 
 int append_common(bool ring, void* k, void* v, const void* k_new, const void* v_new,
                   const int32_t* n_new, int32_t* lens, int B, int Hkv, int d, int64_t rows,
-                  int sink, int R_w, int n_max, int32_t* err, void* stream) {
+                  int sink, int R_w, int n_max, int32_t* err, void* stream, bool fp8 = false,
+                  float k_scale = 1.0f, float v_scale = 1.0f) {
   if (B < 0 || Hkv < 1 || d < 1 || n_max < 0) return WMTP_EINVAL;
+  if (fp8 && (!valid_scale(k_scale) || !valid_scale(v_scale))) return WMTP_EINVAL;
   if (d != 64 && d != 128 && d != 256) return WMTP_EUNSUPPORTED;
   if (ring && (sink < 0 || R_w < 1 || static_cast<int64_t>(sink) + R_w > INT_MAX))
     return WMTP_EINVAL;
@@ -156,8 +169,11 @@ int append_common(bool ring, void* k, void* v, const void* k_new, const void* v_
     return WMTP_EINVAL;
   wmtp::AppendLaunch L{};
   L.ring = ring;
-  L.k = static_cast<uint16_t*>(k);
-  L.v = static_cast<uint16_t*>(v);
+  L.fp8 = fp8;
+  L.k_scale = k_scale;
+  L.v_scale = v_scale;
+  L.k = k;
+  L.v = v;
   L.k_new = static_cast<const uint16_t*>(k_new);
   L.v_new = static_cast<const uint16_t*>(v_new);
   L.n_new = n_new;
@@ -318,6 +334,75 @@ WMTP_EXPORT int wmtp_cache_append(void* k, void* v, const void* k_new, const voi
                                   int64_t S_max, int n_max, int32_t* err, void* stream) {
   return append_common(false, k, v, k_new, v_new, n_new, lens, B, Hkv, d, S_max, 0, 1, n_max, err,
                        stream);
+}
+
+WMTP_EXPORT int wmtp_draft_attn_full_fp8(const void* q, const void* k, const void* v,
+                                         const int32_t* lens, void* out, float* lse, int B, int Hq,
+                                         int Hkv, int d, int64_t S_max, float scale, float k_scale,
+                                         float v_scale, void* ws, size_t ws_bytes, int32_t* err,
+                                         void* stream) {
+  return attention_common(WMTP_VARIANT_FULL, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv, d,
+                          S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream, nullptr, 0, true,
+                          k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_draft_attn_windowed_fp8(const void* q, const void* k, const void* v,
+                                             const int32_t* lens, void* out, float* lse, int B,
+                                             int Hq, int Hkv, int d, int64_t S_max, int W, int sink,
+                                             float scale, float k_scale, float v_scale, void* ws,
+                                             size_t ws_bytes, int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv,
+                          d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream, nullptr, 0, true,
+                          k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_ring_attn_fp8(const void* q, const void* k_ring, const void* v_ring,
+                                   const int32_t* lens, void* out, float* lse, int B, int Hq,
+                                   int Hkv, int d, int W, int sink, int R_w, float scale,
+                                   float k_scale, float v_scale, void* ws, size_t ws_bytes,
+                                   int32_t* err, void* stream) {
+  if (check_window(W, sink) == WMTP_OK && (R_w < W || static_cast<int64_t>(sink) + R_w > INT_MAX))
+    return WMTP_EINVAL;
+  return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, nullptr, 1, out, lse, B, Hq,
+                          Hkv, d, static_cast<int64_t>(sink) + R_w, W, sink, R_w, scale, ws,
+                          ws_bytes, err, stream, nullptr, 0, true, k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_ring_append_fp8(void* k_ring, void* v_ring, const void* k_new,
+                                     const void* v_new, const int32_t* n_new, int32_t* lens, int B,
+                                     int Hkv, int d, int sink, int R_w, int n_max, float k_scale,
+                                     float v_scale, int32_t* err, void* stream) {
+  return append_common(true, k_ring, v_ring, k_new, v_new, n_new, lens, B, Hkv, d, 0, sink, R_w,
+                       n_max, err, stream, true, k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_cache_append_fp8(void* k, void* v, const void* k_new, const void* v_new,
+                                      const int32_t* n_new, int32_t* lens, int B, int Hkv, int d,
+                                      int64_t S_max, int n_max, float k_scale, float v_scale,
+                                      int32_t* err, void* stream) {
+  return append_common(false, k, v, k_new, v_new, n_new, lens, B, Hkv, d, S_max, 0, 1, n_max, err,
+                       stream, true, k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_fp8_quantize(const void* x, int64_t n, float scale, void* codes, void* stream) {
+  if (n < 0 || n % 8 != 0 || !valid_scale(scale)) return WMTP_EINVAL;
+  if (n == 0) return WMTP_OK;
+  if (x == nullptr || codes == nullptr || !aligned(x, 16) || !aligned(codes, 8)) return WMTP_EINVAL;
+  if (wmtp::launch_fp8_quantize(static_cast<const uint16_t*>(x), n, scale,
+                                static_cast<uint8_t*>(codes),
+                                static_cast<hipStream_t>(stream)) != hipSuccess)
+    return WMTP_ELAUNCH;
+  return WMTP_OK;
+}
+
+WMTP_EXPORT int wmtp_fp8_dequantize(const void* codes, int64_t n, void* out, void* stream) {
+  if (n < 0 || n % 8 != 0) return WMTP_EINVAL;
+  if (n == 0) return WMTP_OK;
+  if (codes == nullptr || out == nullptr || !aligned(codes, 8) || !aligned(out, 16)) return WMTP_EINVAL;
+  if (wmtp::launch_fp8_dequantize(static_cast<const uint8_t*>(codes), n, static_cast<uint16_t*>(out),
+                                  static_cast<hipStream_t>(stream)) != hipSuccess)
+    return WMTP_ELAUNCH;
+  return WMTP_OK;
 }
 
 WMTP_EXPORT int wmtp_select_indices(const int32_t* lens, int B, int W, int sink, int R_w,

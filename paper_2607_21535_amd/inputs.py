@@ -15,7 +15,9 @@ depend on the KV contents, Section 3 of the Windowed-MTP paper):
     seed and a fixed stream id, so any one of them can be regenerated alone
     (per sequence for the batched cache);
   * integer draws (lengths, accept counts) always use a CPU generator, so they
-    are the same whichever device holds the tensors.
+    are the same whichever device holds the tensors;
+  * fp8 caches hold E4M3 codes (uint8) of float32 draws, rounded by torch's
+    float8_e4m3fn conversion (the draws stay far inside its range).
 """
 
 from __future__ import annotations
@@ -30,6 +32,8 @@ __all__ = [
     "WORKLOADS",
     "stream_seed",
     "normal_bf16",
+    "normal_fp8",
+    "fp8_codes",
     "uniform_lengths",
     "accept_counts",
     "bf16_bits",
@@ -106,6 +110,19 @@ def normal_bf16(shape, seed: int, device="cpu") -> torch.Tensor:
     g = _gen(seed, device)
     x = torch.randn(tuple(shape), generator=g, device=device, dtype=torch.float32)
     return x.to(torch.bfloat16)
+
+
+def fp8_codes(x: torch.Tensor) -> torch.Tensor:
+    """E4M3 codes (uint8) of a float tensor, by torch's float8_e4m3fn
+    conversion (round to nearest even)."""
+    return x.float().to(torch.float8_e4m3fn).view(torch.uint8)
+
+
+def normal_fp8(shape, seed: int, device="cpu", spread: float = 1.0) -> torch.Tensor:
+    """E4M3 codes (uint8) of standard-normal float32 draws times `spread`."""
+    g = _gen(seed, device)
+    x = torch.randn(tuple(shape), generator=g, device=device, dtype=torch.float32)
+    return fp8_codes(x * spread)
 
 
 def uniform_lengths(B: int, lo: int, hi: int, seed: int) -> np.ndarray:

@@ -41,6 +41,13 @@ __all__ = [
     "ring_append",
     "cache_append",
     "select_indices",
+    "draft_attn_full_fp8",
+    "draft_attn_windowed_fp8",
+    "ring_attn_fp8",
+    "cache_append_fp8",
+    "ring_append_fp8",
+    "fp8_quantize",
+    "fp8_dequantize",
     "status_string",
     "EXPORTED_SYMBOLS",
 ]
@@ -65,6 +72,13 @@ EXPORTED_SYMBOLS = (
     "wmtp_ring_append",
     "wmtp_cache_append",
     "wmtp_select_indices",
+    "wmtp_draft_attn_full_fp8",
+    "wmtp_draft_attn_windowed_fp8",
+    "wmtp_ring_attn_fp8",
+    "wmtp_ring_append_fp8",
+    "wmtp_cache_append_fp8",
+    "wmtp_fp8_quantize",
+    "wmtp_fp8_dequantize",
     "wmtp_status_string",
     "wmtp_abi_version",
 )
@@ -93,6 +107,14 @@ _SIGNATURES = {
     "wmtp_ring_append": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
     "wmtp_cache_append": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I64, _I, _P, _P]),
     "wmtp_select_indices": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _P]),
+    "wmtp_draft_attn_full_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _F, _F, _F, _P, _SZ, _P, _P]),
+    "wmtp_draft_attn_windowed_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _F, _F, _F, _P, _SZ,
+                                          _P, _P]),
+    "wmtp_ring_attn_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _F, _F, _P, _SZ, _P, _P]),
+    "wmtp_ring_append_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _F, _P, _P]),
+    "wmtp_cache_append_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I64, _I, _F, _F, _P, _P]),
+    "wmtp_fp8_quantize": (_I, [_P, _I64, _F, _P, _P]),
+    "wmtp_fp8_dequantize": (_I, [_P, _I64, _P, _P]),
     "wmtp_status_string": (ctypes.c_char_p, [_I]),
     "wmtp_abi_version": (_I, []),
 }
@@ -170,11 +192,23 @@ def _workspace(ws, nbytes, device):
     return ws
 
 
-def _attn_io(q, k, v, lens, out, lse):
+_FP8_DTYPES = (torch.uint8, torch.float8_e4m3fn)
+
+
+def _need_kv(t, name, fp8, ndim, device):
+    """A K/V cache: bf16, or (fp8) E4M3 codes as uint8 or float8_e4m3fn."""
+    if not fp8:
+        return _need(t, name, torch.bfloat16, ndim, device)
+    if not isinstance(t, torch.Tensor) or t.dtype not in _FP8_DTYPES:
+        raise TypeError(f"{name} must be a uint8 / float8_e4m3fn tensor of E4M3 codes")
+    _need(t, name, t.dtype, ndim, device)
+
+
+def _attn_io(q, k, v, lens, out, lse, fp8=False):
     _need(q, "q", torch.bfloat16, 3)
     dev = q.device
-    _need(k, "k", torch.bfloat16, 4, dev)
-    _need(v, "v", torch.bfloat16, 4, dev)
+    _need_kv(k, "k", fp8, 4, dev)
+    _need_kv(v, "v", fp8, 4, dev)
     _need(lens, "lens", torch.int32, 1, dev)
     B, Hq, d = q.shape
     if k.shape != v.shape or k.shape[0] != B or k.shape[3] != d or lens.shape[0] != B:
@@ -382,10 +416,12 @@ def build_kv_indices(req_to_token, lens, variant, W=1, sink=0, indptr=None, indi
     return indptr, indices
 
 
-def _append_io(k, v, k_new, v_new, n_new, lens):
-    _need(k, "k", torch.bfloat16, 4)
+def _append_io(k, v, k_new, v_new, n_new, lens, fp8=False):
+    if not isinstance(k, torch.Tensor):
+        raise TypeError("k must be a torch.Tensor")
     dev = k.device
-    _need(v, "v", torch.bfloat16, 4, dev)
+    _need_kv(k, "k", fp8, 4, dev)
+    _need_kv(v, "v", fp8, 4, dev)
     _need(k_new, "k_new", torch.bfloat16, 4, dev)
     _need(v_new, "v_new", torch.bfloat16, 4, dev)
     _need(n_new, "n_new", torch.int32, 1, dev)
@@ -430,3 +466,105 @@ def select_indices(lens, W, sink, R_w=None, err=None):
         _ptr(err), _stream(dev))
     _check(st, "wmtp_select_indices")
     return pos, slot, n_sel
+
+
+def _scales(k_scale, v_scale):
+    return float(k_scale), float(v_scale)
+
+
+def draft_attn_full_fp8(q, k, v, lens, k_scale=1.0, v_scale=1.0, out=None, lse=None, scale=None, ws=None,
+                        err=None):
+    """Full-context draft attention over an fp8 (E4M3) cache [B, S_max, Hkv, d]."""
+    dev, B, Hq, d, out = _attn_io(q, k, v, lens, out, lse, fp8=True)
+    S_max, Hkv = k.shape[1], k.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_FULL, B, Hq, Hkv, d, S_max), dev)
+    st = load_library().wmtp_draft_attn_full_fp8(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, S_max, scale,
+        *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_attn_full_fp8")
+    return out
+
+
+def draft_attn_windowed_fp8(q, k, v, lens, W, sink, k_scale=1.0, v_scale=1.0, out=None, lse=None, scale=None,
+                            ws=None, err=None):
+    """Sink + window draft attention over an fp8 (E4M3) dense cache."""
+    dev, B, Hq, d, out = _attn_io(q, k, v, lens, out, lse, fp8=True)
+    S_max, Hkv = k.shape[1], k.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_WINDOWED, B, Hq, Hkv, d, S_max, W, sink), dev)
+    st = load_library().wmtp_draft_attn_windowed_fp8(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, S_max, W, sink, scale,
+        *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_attn_windowed_fp8")
+    return out
+
+
+def ring_attn_fp8(q, k_ring, v_ring, lens, W, sink, R_w, k_scale=1.0, v_scale=1.0, out=None, lse=None,
+                  scale=None, ws=None, err=None):
+    """Windowed draft attention over an fp8 (E4M3) ring [B, sink + R_w, Hkv, d]."""
+    dev, B, Hq, d, out = _attn_io(q, k_ring, v_ring, lens, out, lse, fp8=True)
+    if k_ring.shape[1] != sink + R_w:
+        raise ValueError(f"ring must hold sink + R_w = {sink + R_w} rows, has {k_ring.shape[1]}")
+    Hkv = k_ring.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_RING, B, Hq, Hkv, d, sink + R_w, W, sink), dev)
+    st = load_library().wmtp_ring_attn_fp8(
+        _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, W, sink, R_w,
+        scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_ring_attn_fp8")
+    return out
+
+
+def cache_append_fp8(k, v, k_new, v_new, n_new, lens, k_scale=1.0, v_scale=1.0, err=None):
+    """Quantise and append n_new[b] bf16 rows per sequence to an fp8 dense cache; lens += n_new."""
+    dev, B, Hkv, d, n_max = _append_io(k, v, k_new, v_new, n_new, lens, fp8=True)
+    st = load_library().wmtp_cache_append_fp8(
+        _ptr(k), _ptr(v), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(lens), B, Hkv, d, k.shape[1], n_max,
+        *_scales(k_scale, v_scale), _ptr(err), _stream(dev))
+    _check(st, "wmtp_cache_append_fp8")
+
+
+def ring_append_fp8(k_ring, v_ring, k_new, v_new, n_new, lens, sink, R_w, k_scale=1.0, v_scale=1.0, err=None):
+    """Quantise and append n_new[b] bf16 rows per sequence to an fp8 ring; lens += n_new."""
+    dev, B, Hkv, d, n_max = _append_io(k_ring, v_ring, k_new, v_new, n_new, lens, fp8=True)
+    if k_ring.shape[1] != sink + R_w:
+        raise ValueError("ring must hold sink + R_w rows")
+    st = load_library().wmtp_ring_append_fp8(
+        _ptr(k_ring), _ptr(v_ring), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(lens), B, Hkv, d, sink, R_w,
+        n_max, *_scales(k_scale, v_scale), _ptr(err), _stream(dev))
+    _check(st, "wmtp_ring_append_fp8")
+
+
+def fp8_quantize(x, scale=1.0, out=None):
+    """E4M3 codes (uint8, x's shape) of bf16 x stored with per-tensor `scale` (the appends' rule)."""
+    _need(x, "x", torch.bfloat16)
+    if x.numel() % 8:
+        raise ValueError("x must hold a multiple of 8 elements")
+    if out is None:
+        out = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    else:
+        _need(out, "out", torch.uint8, None, x.device)
+        if out.numel() != x.numel():
+            raise ValueError("out must have x's size")
+    st = load_library().wmtp_fp8_quantize(_ptr(x), x.numel(), float(scale), _ptr(out), _stream(x.device))
+    _check(st, "wmtp_fp8_quantize")
+    return out
+
+
+def fp8_dequantize(codes, out=None):
+    """bf16 values (codes' shape) of E4M3 codes, as the attention kernels widen them."""
+    if not isinstance(codes, torch.Tensor) or codes.dtype not in _FP8_DTYPES:
+        raise TypeError("codes must be a uint8 / float8_e4m3fn tensor")
+    _need(codes, "codes", codes.dtype)
+    if codes.numel() % 8:
+        raise ValueError("codes must hold a multiple of 8 elements")
+    if out is None:
+        out = torch.empty(codes.shape, dtype=torch.bfloat16, device=codes.device)
+    else:
+        _need(out, "out", torch.bfloat16, None, codes.device)
+        if out.numel() != codes.numel():
+            raise ValueError("out must have codes' size")
+    st = load_library().wmtp_fp8_dequantize(_ptr(codes), codes.numel(), _ptr(out), _stream(codes.device))
+    _check(st, "wmtp_fp8_dequantize")
+    return out

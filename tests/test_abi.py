@@ -39,7 +39,7 @@ def lib():
 def _declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(wmtp_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(wmtp_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_declares_the_binding_symbols():
@@ -55,7 +55,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.wmtp_abi_version() == (1 << 16)
+    assert lib.wmtp_abi_version() == (1 << 16) | 1
     for code in range(5):
         assert W.status_string(code).startswith("WMTP_")
     assert "unknown" in W.status_string(99)
@@ -238,3 +238,80 @@ def test_extend_argument_checks(lib, which):
 def test_ring_extend_needs_room_for_the_earliest_row(lib):
     assert _ext(lib, "ring", R_w=10) == W.EINVAL  # W + q_max - 1 = 11
     assert _ext(lib, "ring", q_max=1, R_w=8, ws_bytes=1) == W.EWORKSPACE  # R_w = W is enough for one row
+
+
+def _full8(lib, **kw):
+    a = dict(q=P, k=P, v=P, lens=P, out=P, lse=None, B=1, Hq=16, Hkv=2, d=128, S_max=100,
+             scale=0.1, k_scale=0.5, v_scale=2.0, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_draft_attn_full_fp8(*a.values())
+
+
+def _win8(lib, **kw):
+    a = dict(q=P, k=P, v=P, lens=P, out=P, lse=None, B=1, Hq=16, Hkv=2, d=128, S_max=100, W=8,
+             sink=4, scale=0.1, k_scale=0.5, v_scale=2.0, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_draft_attn_windowed_fp8(*a.values())
+
+
+def _ring8(lib, **kw):
+    a = dict(q=P, k=P, v=P, lens=P, out=P, lse=None, B=1, Hq=16, Hkv=2, d=128, W=8, sink=4, R_w=8,
+             scale=0.1, k_scale=0.5, v_scale=2.0, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_ring_attn_fp8(*a.values())
+
+
+@fake_pointers
+@pytest.mark.parametrize("call", [_full8, _win8, _ring8])
+def test_fp8_attention_argument_checks(lib, call):
+    for bad in (0.0, -1.0, float("nan"), float("inf")):
+        assert call(lib, k_scale=bad) == W.EINVAL
+        assert call(lib, v_scale=bad) == W.EINVAL
+    assert call(lib, scale=1e30, k_scale=1e30) == W.EINVAL  # folded logit scale overflows
+    assert call(lib, d=96) == W.EUNSUPPORTED
+    assert call(lib, Hq=16, Hkv=3) == W.EINVAL
+    assert call(lib, k=P + 8) == W.EINVAL  # caches need 16-byte alignment
+    assert call(lib, q=None) == W.EINVAL
+    assert call(lib, ws_bytes=1) == W.EWORKSPACE
+    assert call(lib, B=0, q=None, k=None, v=None, lens=None, out=None) == W.OK
+
+
+def _rapp8(lib, **kw):
+    a = dict(k=P, v=P, kn=P, vn=P, n_new=P, lens=P, B=2, Hkv=2, d=256, sink=4, R_w=16, n_max=8,
+             k_scale=1.0, v_scale=1.0, err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_ring_append_fp8(*a.values())
+
+
+def _capp8(lib, **kw):
+    a = dict(k=P, v=P, kn=P, vn=P, n_new=P, lens=P, B=2, Hkv=2, d=256, S_max=100, n_max=8,
+             k_scale=1.0, v_scale=1.0, err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_cache_append_fp8(*a.values())
+
+
+@fake_pointers
+@pytest.mark.parametrize("call", [_rapp8, _capp8])
+def test_fp8_append_argument_checks(lib, call):
+    for bad in (0.0, -2.0, float("nan"), float("inf")):
+        assert call(lib, k_scale=bad) == W.EINVAL
+        assert call(lib, v_scale=bad) == W.EINVAL
+    assert call(lib, d=96) == W.EUNSUPPORTED
+    assert call(lib, kn=P + 4) == W.EINVAL
+    assert call(lib, B=0, k=None, v=None, kn=None, vn=None, n_new=None, lens=None) == W.OK
+
+
+@fake_pointers
+def test_fp8_conversion_argument_checks(lib):
+    q, dq = lib.wmtp_fp8_quantize, lib.wmtp_fp8_dequantize
+    assert q(P, 12, 1.0, P, None) == W.EINVAL  # n a multiple of 8
+    assert q(P, -8, 1.0, P, None) == W.EINVAL
+    assert q(P, 16, 0.0, P, None) == W.EINVAL
+    assert q(P + 8, 16, 1.0, P, None) == W.EINVAL  # bf16 input 16-byte aligned
+    assert q(P, 16, 1.0, P + 4, None) == W.EINVAL  # codes 8-byte aligned
+    assert q(None, 16, 1.0, P, None) == W.EINVAL
+    assert q(None, 0, 1.0, None, None) == W.OK
+    assert dq(P, 12, P, None) == W.EINVAL
+    assert dq(P + 4, 16, P, None) == W.EINVAL
+    assert dq(P, 16, P + 8, None) == W.EINVAL
+    assert dq(None, 0, None, None) == W.OK
