@@ -17,6 +17,9 @@ Modules
   fp8        -- the fp8 (OCP E4M3, per-tensor scale) draft KV cache: code
                 values, quantization on append, attention over the
                 dequantized rows (Section 7, KV-cache quantization).
+  spec       -- speculative draft rows in the ring: chain rollback and
+                tree-width rings (Section 7, tree speculation; Appendix A
+                ring comment).
   paged      -- the paged token pool (page size 1): the draft's index list
                 req_to_token[r, keep] and attention over the listed rows
                 (Section 4 "Mechanism", Appendix A pseudocode).
@@ -29,4 +32,4 @@ against closed forms, brute force, invariants, a library routine
 (tests/golden/).
 """
 
-from . import attention, fp8, paged, ring  # noqa: F401
+from . import attention, fp8, paged, ring, spec  # noqa: F401
