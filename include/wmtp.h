@@ -64,6 +64,7 @@ typedef enum {
 #define WMTP_DERR_NNEW_RANGE 0x2 /* n_new[b] outside [0, n_max] (n_q[b] outside [0, q_max]): clamped */
 #define WMTP_DERR_CAPACITY 0x4   /* dense-cache append past S_max: extra rows dropped */
 #define WMTP_DERR_SLOT_RANGE 0x8 /* req_to_token entry outside the pool: row 0 read instead */
+#define WMTP_DERR_DEPTH 0x10     /* tree append at the largest speculative depth: nothing written */
 
 /* Attention variants, for wmtp_workspace_bytes(). */
 typedef enum {
@@ -71,7 +72,8 @@ typedef enum {
   WMTP_VARIANT_WINDOWED = 1,
   WMTP_VARIANT_RING = 2,
   WMTP_VARIANT_PAGED_FULL = 3,
-  WMTP_VARIANT_PAGED_WINDOWED = 4
+  WMTP_VARIANT_PAGED_WINDOWED = 4,
+  WMTP_VARIANT_TREE = 5
 } wmtp_variant;
 
 /*
@@ -245,6 +247,60 @@ int wmtp_select_indices(const int32_t* lens, int B, int W, int sink, int R_w, in
                         int32_t* slot_out, int32_t* n_sel_out, int32_t* err, void* stream);
 
 /*
+ * Speculative draft rows.
+ *
+ * Chain rollback: a chain that appends its speculative draft rows with
+ * wmtp_ring_append (lens advancing with each) discards the rows the target
+ * rejected by lowering lens: lens[b] -= n_drop[b] on the device (n_drop
+ * outside [0, lens[b]] is clamped and flagged WMTP_DERR_NNEW_RANGE).  The
+ * rows stay in their slots and are overwritten by later appends.  Every row
+ * a later windowed read needs is still held when R_w >= W + (rows appended
+ * past the committed length) -- the paper's chain ring of
+ * n_sink + W + d slots (Section 7, tree speculation; Appendix A ring
+ * comment).
+ */
+int wmtp_ring_rollback(int32_t* lens, const int32_t* n_drop, int B, int32_t* err, void* stream);
+
+/*
+ * Tree-width rings (Section 7, tree speculation: the candidates share the
+ * sink + window prefix and differ only over their last d positions, so a
+ * tree of width k reserves n_sink + W + d k slots per request).
+ *   State per request: lens[b] = committed length S (rows the target has
+ *   accepted), depth[b] = speculative depth i (0 .. depth_max), both on the
+ *   device.  Candidate c's sequence is rows [0, S) followed by its own rows
+ *   at positions S .. S + i - 1.
+ *   Layout: the ring [B, sink + R_w, Hkv, d] with R_w >= W + depth_max holds
+ *   the committed rows and candidate 0's rows at their ring slots (in place,
+ *   as a chain writes them); the private runs [B, (width - 1) * depth_max,
+ *   Hkv, d] hold candidate c >= 1's row of position S + t at run row
+ *   (c - 1) * depth_max + t.  Sink + W + depth_max * width rows in all.
+ *   k_branch / v_branch may be NULL when width == 1.
+ * wmtp_tree_append: k_new, v_new [B, width, Hkv, d] bf16, one draft row per
+ *   candidate, written for position S + depth[b]; then depth[b] += 1.  A
+ *   request already at depth_max is left unchanged and flagged
+ *   WMTP_DERR_DEPTH.
+ * wmtp_tree_attn: q, out [B, width, Hq, d] bf16, lse [B, width, Hq] or NULL.
+ *   Candidate c of request b attends the windowed key set (sink + W) of its
+ *   own sequence at length S + depth[b].  Workspace:
+ *   wmtp_workspace_bytes(WMTP_VARIANT_TREE, B * width, Hq, Hkv, d, 0, W, sink).
+ * wmtp_tree_reset: depth[b] = 0 for every request (after the verify).  The
+ *   accepted tokens' draft rows are then written at their committed
+ *   positions by wmtp_ring_append + wmtp_ring_extend (the draft-extend step,
+ *   at most depth_max + 1 rows, which the R_w >= W + depth_max headroom
+ *   allows).
+ */
+int wmtp_tree_append(void* k_ring, void* v_ring, void* k_branch, void* v_branch, const void* k_new,
+                     const void* v_new, const int32_t* lens, int32_t* depth, int B, int width,
+                     int Hkv, int d, int W, int sink, int R_w, int depth_max, int32_t* err,
+                     void* stream);
+int wmtp_tree_attn(const void* q, const void* k_ring, const void* v_ring, const void* k_branch,
+                   const void* v_branch, const int32_t* lens, const int32_t* depth, void* out,
+                   float* lse, int B, int width, int Hq, int Hkv, int d, int W, int sink, int R_w,
+                   int depth_max, float scale, void* ws, size_t ws_bytes, int32_t* err,
+                   void* stream);
+int wmtp_tree_reset(int32_t* depth, int B, void* stream);
+
+/*
  * fp8 draft KV cache (Section 7, KV-cache quantization: the windowing
  * composes with fp8 KV; the dtype sets the bytes per entry, windowing the
  * number of entries read).  Format: OCP E4M3 ("e4m3fn": bias 7, subnormals,
@@ -306,7 +362,7 @@ const char* wmtp_status_string(int status);
 /* ABI version of this header, (major << 16) | minor. */
 int wmtp_abi_version(void);
 
-#define WMTP_ABI_VERSION ((1 << 16) | 1)
+#define WMTP_ABI_VERSION ((1 << 16) | 2)
 
 #ifdef __cplusplus
 }

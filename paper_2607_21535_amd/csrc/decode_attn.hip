@@ -42,6 +42,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <climits>
 #include <cstdlib>
 #include <type_traits>
 
@@ -76,6 +77,12 @@ struct SplitArgs {
   int target;     // work items per KV head to aim for
   int chunk_cap;  // largest item, in keys
   float scale_log2;
+  // Tree: n_q holds each request's speculative depth (0 .. dd); candidate
+  // b >= 1 reads its private run from k2 / v2 [B, rows2, Hkv, D]
+  const void* k2;
+  const void* v2;
+  int64_t rows2;
+  int dd;
 };
 
 struct MergeArgs {
@@ -93,6 +100,7 @@ struct MergeArgs {
   int64_t len_cap;
   int W, sink, target, chunk_cap;
   float out_scale;  // value scale of an fp8 cache (1 for bf16)
+  int dd;           // Tree: largest speculative depth
 };
 
 __device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap, int32_t* err,
@@ -112,9 +120,36 @@ __device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap,
 // every row of an empty sequence, have no keys; a non-empty sequence with
 // fewer rows than n is flagged.  Returns that length; `b_out` receives the
 // sequence.
+// Tree (speculation candidates): query row v = b * qps + t is candidate t of
+// request b, whose committed length is lens[b] and speculative depth
+// n_q[b] (0 .. dd, clamped and flagged outside); every candidate sees
+// lens[b] + depth rows.  `s_commit` receives the committed length.
+__device__ __forceinline__ int tree_len(const int32_t* lens, const int32_t* depth, int dd, int b,
+                                        int32_t* err, bool report, int& s_commit) {
+  int S = lens[b];
+  if (S < 0 || S > INT_MAX - dd) {
+    if (report) raise_error(err, WMTP_DERR_LEN_RANGE);
+    S = S < 0 ? 0 : INT_MAX - dd;
+  }
+  int i = depth[b];
+  if (i < 0 || i > dd) {
+    if (report) raise_error(err, WMTP_DERR_NNEW_RANGE);
+    i = i < 0 ? 0 : dd;
+  }
+  s_commit = S;
+  return S + i;
+}
+
+template <KeyMap M>
 __device__ __forceinline__ int visible_len(const int32_t* lens, const int32_t* n_q, int qps,
                                            int64_t cap, int32_t* err, int v, bool report,
-                                           int& b_out) {
+                                           int& b_out, int dd) {
+  if constexpr (M == KeyMap::Tree) {
+    const int b = v / qps;
+    b_out = b;
+    int s_commit;
+    return tree_len(lens, n_q, dd, b, err, report && v == b * qps, s_commit);
+  }
   const int b = qps == 1 ? v : v / qps;
   const int t = v - b * qps;
   b_out = b;
@@ -146,14 +181,14 @@ __device__ __forceinline__ int visible_len(const int32_t* lens, const int32_t* n
 // lane returns the same value.
 template <KeyMap M>
 __device__ int wave_chunk(const int32_t* lens, const int32_t* n_q, int qps, int NV, int64_t len_cap,
-                          int W, int sink, int target, int chunk_cap, int32_t* err, bool report) {
+                          int W, int sink, int target, int chunk_cap, int32_t* err, bool report, int dd) {
   const int lane = threadIdx.x & (kWave - 1);
   long long total = 0;
   for (int base = 0; base < NV; base += kWave) {
     const int v = base + lane;
     int b;
     if (v < NV)
-      total += selected_count<M>(visible_len(lens, n_q, qps, len_cap, err, v, report, b), W, sink);
+      total += selected_count<M>(visible_len<M>(lens, n_q, qps, len_cap, err, v, report, b, dd), W, sink);
   }
 #pragma unroll
   for (int off = kWave / 2; off > 0; off >>= 1) total += __shfl_xor(total, off);
@@ -174,7 +209,7 @@ __device__ bool locate_item(const SplitArgs& a, int item, int& v_out, int& c_out
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
     const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, NV, a.len_cap, a.W, a.sink, a.target,
-                                    a.chunk_cap, a.err, true);
+                                    a.chunk_cap, a.err, true, a.dd);
     if (lane == 0) {
       s_v = -1;
       s_chunk = chunk;
@@ -185,7 +220,7 @@ __device__ bool locate_item(const SplitArgs& a, int item, int& v_out, int& c_out
       int S = 0, cnt = 0;
       if (v < NV) {
         int b;
-        S = visible_len(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, false, b);
+        S = visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, false, b, a.dd);
         cnt = ceil_div_i(selected_count<M>(S, a.W, a.sink), chunk);
       }
       int incl = cnt;
@@ -275,7 +310,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int n_sel = selected_count<M>(S, a.W, a.sink);
   const int j0 = c * chunk;
   const int j1 = min(j0 + chunk, n_sel);
-  const RowMap<M> map(S, a.W, a.sink, a.R_w);
+  RowMap<M> map(S, a.W, a.sink, a.R_w);
+  if constexpr (M == KeyMap::Tree) {
+    int s_commit;
+    (void)tree_len(a.lens, a.n_q, a.dd, b, a.err, false, s_commit);
+    const int cand = v - b * a.qps;
+    map.S_c = s_commit;
+    map.bbase = cand == 0 ? -1 : static_cast<int>(a.rows) + (cand - 1) * a.dd;
+  }
   const int64_t rs = static_cast<int64_t>(a.Hkv) * D;  // elements between rows
   // Dense and ring caches hold `rows` rows per sequence; a paged pool is one
   // shared array of rows indexed by the request's token table.
@@ -283,6 +325,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int64_t seq_off = (seq_rows * a.Hkv + g) * D;
   const KT* kbase = static_cast<const KT*>(a.k) + seq_off;
   const KT* vbase = static_cast<const KT*>(a.v) + seq_off;
+  // Tree: rows at or past the ring's `rows` are in the candidate's private run.
+  [[maybe_unused]] const int64_t off2 = (static_cast<int64_t>(b) * a.rows2 * a.Hkv + g) * D;
+  auto key_row = [&](int r) -> const KT* {
+    if constexpr (M == KeyMap::Tree) {
+      if (r >= a.rows) return static_cast<const KT*>(a.k2) + off2 + static_cast<int64_t>(r - a.rows) * rs;
+    }
+    return kbase + static_cast<int64_t>(r) * rs;
+  };
+  auto value_row = [&](int r) -> const KT* {
+    if constexpr (M == KeyMap::Tree) {
+      if (r >= a.rows) return static_cast<const KT*>(a.v2) + off2 + static_cast<int64_t>(r - a.rows) * rs;
+    }
+    return vbase + static_cast<int64_t>(r) * rs;
+  };
 
   // Paged: the pool rows of this item's keys, looked up once into LDS.
   [[maybe_unused]] int* slots = nullptr;
@@ -340,11 +396,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       const int j = jt + col;
       const int r = row_of(j < j1 ? j : j0);
       if constexpr (F8) {
-        const KT* p = kbase + static_cast<int64_t>(r) * rs + grp * 16;
+        const KT* p = key_row(r) + grp * 16;
 #pragma unroll
         for (int kk = 0; kk < D / 64; ++kk) T.kx[kk] = stream_load<u32x4>(p + kk * 64);
       } else {
-        const KT* p = kbase + static_cast<int64_t>(r) * rs + grp * 8;
+        const KT* p = key_row(r) + grp * 8;
 #pragma unroll
         for (int kk = 0; kk < KCH; ++kk) T.kx[kk] = stream_load<u32x4>(p + kk * 32);
       }
@@ -353,7 +409,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     for (int i = 0; i < 4; ++i) {
       const int j = jt + 4 * grp + i;
       const int r = row_of(j < j1 ? j : j0);
-      const KT* p = vbase + static_cast<int64_t>(r) * rs + SEG * col;
+      const KT* p = value_row(r) + SEG * col;
       if constexpr (F8) {
         if constexpr (VEC == 16) {
           const u32x4 x = stream_load<u32x4>(p);
@@ -583,13 +639,13 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
   __shared__ float s_Z[NS];
   if (tid < kWave) {
     const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, a.B * a.qps, a.len_cap, a.W, a.sink,
-                                    a.target, a.chunk_cap, a.err, false);
+                                    a.target, a.chunk_cap, a.err, false, a.dd);
     int before = 0, mine = 0;
     for (int base = 0; base <= v; base += kWave) {
       const int vv = base + lane;
       if (vv <= v) {
         int bb;
-        const int S = visible_len(a.lens, a.n_q, a.qps, a.len_cap, a.err, vv, false, bb);
+        const int S = visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, vv, false, bb, a.dd);
         const int cnt = ceil_div_i(selected_count<M>(S, a.W, a.sink), chunk);
         if (vv < v) before += cnt; else mine = cnt;
       }
@@ -675,6 +731,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
     a.W = L.W; a.sink = L.sink; a.R_w = L.R_w;
     a.target = L.target; a.chunk_cap = L.chunk_cap;
     a.scale_log2 = L.scale * L.k_scale * kLog2e;
+    a.k2 = L.k2; a.v2 = L.v2; a.rows2 = L.rows2; a.dd = L.dd;
     const dim3 grid(static_cast<unsigned>(L.max_items) * static_cast<unsigned>(L.Hkv));
     hipLaunchKernelGGL((split_kernel<D, M, F8>), grid, dim3(kThreads), 0, st, a);
   }
@@ -688,6 +745,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   m.len_cap = L.len_cap; m.W = L.W; m.sink = L.sink;
   m.target = L.target; m.chunk_cap = L.chunk_cap;
   m.out_scale = L.v_scale;
+  m.dd = L.dd;
   const unsigned bh = static_cast<unsigned>(NV) * static_cast<unsigned>(L.Hq);
   if (wide)
     hipLaunchKernelGGL((merge_kernel<D, M, kMergeThreads, 64>), dim3(bh, D / 64), dim3(kMergeThreads), 0,
@@ -712,7 +770,8 @@ hipError_t launch_d(const AttnLaunch& L, hipStream_t st) {
     case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::Window, false>(L, st);
     case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::Ring, false>(L, st);
     case WMTP_VARIANT_PAGED_FULL: return launch_typed<D, KeyMap::PagedFull, false>(L, st);
-    default: return launch_typed<D, KeyMap::PagedWindow, false>(L, st);
+    case WMTP_VARIANT_PAGED_WINDOWED: return launch_typed<D, KeyMap::PagedWindow, false>(L, st);
+    default: return launch_typed<D, KeyMap::Tree, false>(L, st);
   }
 }
 

@@ -24,12 +24,18 @@ namespace wmtp {
 //   Ring               compact ring, row = ring slot of the position
 //   PagedFull/Window   shared token pool, row = req_to_token[b][position]
 //                      (the kernel resolves the table; RowMap gives positions)
-enum class KeyMap : int { Full = 0, Window = 1, Ring = 2, PagedFull = 3, PagedWindow = 4 };
+//   Tree               speculation candidates over a ring (Section 7, tree
+//                      speculation): candidate 0 and committed positions
+//                      live at their ring slots; positions of candidate
+//                      b >= 1 past the committed length live in its private
+//                      run, rows numbered after the ring's
+enum class KeyMap : int { Full = 0, Window = 1, Ring = 2, PagedFull = 3, PagedWindow = 4, Tree = 5 };
 
 constexpr bool is_paged(KeyMap m) { return m == KeyMap::PagedFull || m == KeyMap::PagedWindow; }
 constexpr bool is_windowed(KeyMap m) {
-  return m == KeyMap::Window || m == KeyMap::Ring || m == KeyMap::PagedWindow;
+  return m == KeyMap::Window || m == KeyMap::Ring || m == KeyMap::PagedWindow || m == KeyMap::Tree;
 }
+constexpr bool is_ring(KeyMap m) { return m == KeyMap::Ring || m == KeyMap::Tree; }
 
 template <KeyMap M>
 __device__ __forceinline__ int selected_count(int S, int W, int sink) {
@@ -48,19 +54,25 @@ struct RowMap {
   int sink;
   int R_w;
   int shift;  // position(j) = j + shift for j >= sink
-  int r0;     // shift mod R_w (ring only)
+  int r0;     // shift mod R_w (ring maps only)
+  int S_c = 0;     // Tree: committed length
+  int bbase = -1;  // Tree: first row of the candidate's private run (-1: candidate 0)
 
   __device__ __forceinline__ RowMap(int S, int W, int sink_, int R_w_) : sink(sink_), R_w(R_w_) {
     shift = (is_windowed(M) && S > sink_ + W) ? S - W - sink_ : 0;
-    r0 = (M == KeyMap::Ring) ? shift % R_w_ : 0;
+    r0 = is_ring(M) ? shift % R_w_ : 0;
   }
 
   __device__ __forceinline__ int row(int j) const {
     if constexpr (!is_windowed(M)) {
       return j;
-    } else if constexpr (M != KeyMap::Ring) {
+    } else if constexpr (!is_ring(M)) {
       return j < sink ? j : j + shift;
     } else {
+      if constexpr (M == KeyMap::Tree) {
+        const int pos = j < sink ? j : j + shift;
+        if (bbase >= 0 && pos >= S_c) return bbase + (pos - S_c);
+      }
       // j - sink < W <= R_w and r0 < R_w, so one subtraction wraps.
       if (j < sink) return j;
       int t = (j - sink) + r0;

@@ -121,6 +121,70 @@ __global__ __launch_bounds__(256) void select_kernel(const int32_t* lens, int W,
   if (threadIdx.x == 0) n_sel_out[b] = n;
 }
 
+// Speculation candidates (Windowed-MTP Section 7, tree speculation): one
+// workgroup per request writes each candidate's draft row for position
+// lens[b] + depth[b] -- candidate 0 at that position's ring slot (in place,
+// as a chain writes), candidate c >= 1 at slot depth[b] of its private run
+// -- then advances depth[b].  A request already at the largest depth is
+// flagged and left unchanged.
+__global__ __launch_bounds__(256) void tree_append_kernel(TreeAppendLaunch a) {
+  const int b = blockIdx.x;
+  const bool report = threadIdx.x == 0;
+  int S = a.lens[b];
+  if (S < 0 || S > INT_MAX - a.dd) {
+    if (report) raise_error(a.err, WMTP_DERR_LEN_RANGE);
+    S = S < 0 ? 0 : INT_MAX - a.dd;
+  }
+  const int i = a.depth[b];
+  if (i < 0 || i >= a.dd) {  // uniform over the workgroup
+    if (report) raise_error(a.err, WMTP_DERR_DEPTH);
+    return;
+  }
+  const int p = S + i;
+  const int ring_slot = p < a.sink ? p : a.sink + (p - a.sink) % a.R_w;
+  const int units = a.Hkv * a.d / 8;  // 16-byte units per row
+  const int64_t row_elems = static_cast<int64_t>(a.Hkv) * a.d;
+  const int64_t ring_rows = static_cast<int64_t>(a.sink) + a.R_w;
+  const int64_t run_rows = static_cast<int64_t>(a.width - 1) * a.dd;
+  for (int u = threadIdx.x; u < a.width * units; u += blockDim.x) {
+    const int c = u / units;
+    const int off = (u % units) * 8;
+    const int64_t src = (static_cast<int64_t>(b) * a.width + c) * row_elems + off;
+    const u32x4 kx = *reinterpret_cast<const u32x4*>(a.k_new + src);
+    const u32x4 vx = *reinterpret_cast<const u32x4*>(a.v_new + src);
+    if (c == 0) {
+      const int64_t dst = (static_cast<int64_t>(b) * ring_rows + ring_slot) * row_elems + off;
+      *reinterpret_cast<u32x4*>(a.k + dst) = kx;
+      *reinterpret_cast<u32x4*>(a.v + dst) = vx;
+    } else {
+      const int64_t dst = (static_cast<int64_t>(b) * run_rows + static_cast<int64_t>(c - 1) * a.dd + i) * row_elems + off;
+      *reinterpret_cast<u32x4*>(a.k2 + dst) = kx;
+      *reinterpret_cast<u32x4*>(a.v2 + dst) = vx;
+    }
+  }
+  __syncthreads();  // every thread has read depth[b] before it changes
+  if (threadIdx.x == 0) a.depth[b] = i + 1;
+}
+
+// counts[b] -= n_drop[b], or counts[b] = 0 without n_drop.
+__global__ __launch_bounds__(256) void rollback_kernel(int32_t* counts, const int32_t* n_drop, int B,
+                                                      int32_t* err) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  if (n_drop == nullptr) {
+    counts[b] = 0;
+    return;
+  }
+  const int c = counts[b];
+  const int n = n_drop[b];
+  if (n < 0 || c < 0 || n > c) {
+    raise_error(err, WMTP_DERR_NNEW_RANGE);
+    counts[b] = c < 0 ? 0 : (n < 0 ? c : 0);
+    return;
+  }
+  counts[b] = c - n;
+}
+
 // The conversion exports run the appends' quantiser and the attention's
 // widening on flat arrays, 8 elements per thread and step.
 __global__ __launch_bounds__(256) void fp8_quantize_kernel(const uint16_t* x, int64_t units, float scale,
@@ -161,6 +225,16 @@ hipError_t launch_append(const AppendLaunch& L, hipStream_t st) {
     else
       hipLaunchKernelGGL((append_kernel<false, false>), grid, block, 0, st, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_tree_append(const TreeAppendLaunch& L, hipStream_t st) {
+  hipLaunchKernelGGL(tree_append_kernel, dim3(L.B), dim3(256), 0, st, L);
+  return hipGetLastError();
+}
+
+hipError_t launch_rollback(int32_t* counts, const int32_t* n_drop, int B, int32_t* err, hipStream_t st) {
+  hipLaunchKernelGGL(rollback_kernel, dim3((B + 255) / 256), dim3(256), 0, st, counts, n_drop, B, err);
   return hipGetLastError();
 }
 

@@ -27,6 +27,12 @@ struct AttnLaunch {
   int W, sink, R_w;
   float scale;
   float k_scale, v_scale;  // per-tensor scales of an fp8 cache (1 for bf16)
+  // Tree variant: n_q is the speculative depth per request; candidates
+  // b >= 1 read their private runs from k2 / v2 [B, rows2, Hkv, d]
+  const void* k2;
+  const void* v2;
+  int64_t rows2;
+  int dd;  // largest speculative depth (private-run length)
   // split plan (from plan_split)
   int target;     // work items per KV head to aim for
   int chunk_cap;  // largest work item, in keys
@@ -76,6 +82,26 @@ struct AppendLaunch {
 };
 
 hipError_t launch_append(const AppendLaunch& a, hipStream_t stream);
+
+// Speculation bookkeeping.  Tree append: one draft row per candidate at
+// position lens[b] + depth[b] (candidate 0 at its ring slot, candidate
+// c >= 1 in its private run), then depth[b] += 1.
+struct TreeAppendLaunch {
+  uint16_t* k;  // ring [B, sink + R_w, Hkv, d]
+  uint16_t* v;
+  uint16_t* k2;  // private runs [B, (width - 1) * dd, Hkv, d]
+  uint16_t* v2;
+  const uint16_t* k_new;  // [B, width, Hkv, d]
+  const uint16_t* v_new;
+  const int32_t* lens;
+  int32_t* depth;
+  int32_t* err;
+  int B, width, Hkv, d, sink, R_w, dd;
+};
+hipError_t launch_tree_append(const TreeAppendLaunch& a, hipStream_t stream);
+
+// counts[b] -= n_drop[b] (n_drop NULL: counts[b] = 0), clamped at 0 and flagged.
+hipError_t launch_rollback(int32_t* counts, const int32_t* n_drop, int B, int32_t* err, hipStream_t stream);
 
 // Elementwise conversions of the fp8 cache format (the appends' quantiser and
 // the attention's widening), n a multiple of 8.

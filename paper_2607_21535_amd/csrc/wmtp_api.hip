@@ -45,7 +45,7 @@ int64_t keys_max(int variant, int64_t S_max, int W, int sink) {
 
 bool windowed_variant(int variant) {
   return variant == WMTP_VARIANT_WINDOWED || variant == WMTP_VARIANT_RING ||
-         variant == WMTP_VARIANT_PAGED_WINDOWED;
+         variant == WMTP_VARIANT_PAGED_WINDOWED || variant == WMTP_VARIANT_TREE;
 }
 
 bool paged_variant(int variant) {
@@ -69,9 +69,20 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
                      int B, int Hq, int Hkv, int d, int64_t S_max, int W, int sink, int R_w,
                      float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream,
                      const int32_t* table = nullptr, int64_t pool_rows = 0, bool fp8 = false,
-                     float k_scale = 1.0f, float v_scale = 1.0f) {
+                     float k_scale = 1.0f, float v_scale = 1.0f, const void* k2 = nullptr,
+                     const void* v2 = nullptr, int dd = 0) {
   int st = check_heads(B, Hq, Hkv, d);
   if (st != WMTP_OK) return st;
+  const bool tree = variant == WMTP_VARIANT_TREE;
+  // Tree: q_max candidates per request; the ring's window region holds the
+  // window plus the draft-extend headroom (R_w >= W + dd), candidates 1 ..
+  // q_max - 1 own private runs of dd rows.
+  const int64_t rows2 = tree ? static_cast<int64_t>(q_max - 1) * dd : 0;
+  if (tree) {
+    if (fp8 || dd < 1 || q_max < 1) return WMTP_EINVAL;
+    if (static_cast<int64_t>(R_w) < static_cast<int64_t>(W) + dd) return WMTP_EINVAL;
+    if (static_cast<int64_t>(sink) + R_w + rows2 > INT_MAX) return WMTP_EINVAL;
+  }
   if (fp8) {
     if (paged_variant(variant)) return WMTP_EUNSUPPORTED;
     if (!valid_scale(k_scale) || !valid_scale(v_scale)) return WMTP_EINVAL;
@@ -92,6 +103,9 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   if (q == nullptr || k == nullptr || v == nullptr || lens == nullptr || out == nullptr)
     return WMTP_EINVAL;
   if (paged_variant(variant) && (table == nullptr || !aligned(table, 4))) return WMTP_EINVAL;
+  if (tree && (n_q == nullptr || (rows2 > 0 && (k2 == nullptr || v2 == nullptr || !aligned(k2, 16) ||
+                                                 !aligned(v2, 16)))))
+    return WMTP_EINVAL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
       !aligned(lens, 4) || (lse != nullptr && !aligned(lse, 4)) ||
       (err != nullptr && !aligned(err, 4)) || (n_q != nullptr && !aligned(n_q, 4)))
@@ -122,7 +136,11 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   L.d = d;
   L.table = table;
   L.table_stride = S_max;
-  if (variant == WMTP_VARIANT_RING) {
+  L.k2 = k2;
+  L.v2 = v2;
+  L.rows2 = rows2;
+  L.dd = dd;
+  if (variant == WMTP_VARIANT_RING || tree) {
     L.rows = static_cast<int64_t>(sink) + R_w;
     L.len_cap = INT_MAX;
   } else if (paged_variant(variant)) {
@@ -194,7 +212,7 @@ int append_common(bool ring, void* k, void* v, const void* k_new, const void* v_
 
 WMTP_EXPORT size_t wmtp_workspace_bytes(int variant, int B, int Hq, int Hkv, int d, int64_t S_max,
                                         int W, int sink) {
-  if (variant < WMTP_VARIANT_FULL || variant > WMTP_VARIANT_PAGED_WINDOWED) return 0;
+  if (variant < WMTP_VARIANT_FULL || variant > WMTP_VARIANT_TREE) return 0;
   if (check_heads(B, Hq, Hkv, d) != WMTP_OK || B == 0) return 0;
   if (windowed_variant(variant) && check_window(W, sink) != WMTP_OK) return 0;
   if (!windowed_variant(variant) && S_max < 0) return 0;
@@ -382,6 +400,79 @@ WMTP_EXPORT int wmtp_cache_append_fp8(void* k, void* v, const void* k_new, const
                                       int32_t* err, void* stream) {
   return append_common(false, k, v, k_new, v_new, n_new, lens, B, Hkv, d, S_max, 0, 1, n_max, err,
                        stream, true, k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_tree_attn(const void* q, const void* k_ring, const void* v_ring,
+                               const void* k_branch, const void* v_branch, const int32_t* lens,
+                               const int32_t* depth, void* out, float* lse, int B, int width, int Hq,
+                               int Hkv, int d, int W, int sink, int R_w, int depth_max, float scale,
+                               void* ws, size_t ws_bytes, int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_TREE, q, k_ring, v_ring, lens, depth, width, out, lse, B, Hq,
+                          Hkv, d, static_cast<int64_t>(sink) + R_w, W, sink, R_w, scale, ws,
+                          ws_bytes, err, stream, nullptr, 0, false, 1.0f, 1.0f, k_branch, v_branch,
+                          depth_max);
+}
+
+WMTP_EXPORT int wmtp_tree_append(void* k_ring, void* v_ring, void* k_branch, void* v_branch,
+                                 const void* k_new, const void* v_new, const int32_t* lens,
+                                 int32_t* depth, int B, int width, int Hkv, int d, int W, int sink,
+                                 int R_w, int depth_max, int32_t* err, void* stream) {
+  if (B < 0 || width < 1 || Hkv < 1 || d < 1 || depth_max < 1 || sink < 0 || check_window(W, sink))
+    return WMTP_EINVAL;
+  if (d != 64 && d != 128 && d != 256) return WMTP_EUNSUPPORTED;
+  if (static_cast<int64_t>(R_w) < static_cast<int64_t>(W) + depth_max ||
+      static_cast<int64_t>(sink) + R_w + static_cast<int64_t>(width - 1) * depth_max > INT_MAX)
+    return WMTP_EINVAL;
+  if (B == 0) return WMTP_OK;
+  if (k_ring == nullptr || v_ring == nullptr || k_new == nullptr || v_new == nullptr ||
+      lens == nullptr || depth == nullptr)
+    return WMTP_EINVAL;
+  if (width > 1 && (k_branch == nullptr || v_branch == nullptr || !aligned(k_branch, 16) ||
+                    !aligned(v_branch, 16)))
+    return WMTP_EINVAL;
+  if (!aligned(k_ring, 16) || !aligned(v_ring, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) ||
+      !aligned(lens, 4) || !aligned(depth, 4) || (err != nullptr && !aligned(err, 4)))
+    return WMTP_EINVAL;
+  wmtp::TreeAppendLaunch L{};
+  L.k = static_cast<uint16_t*>(k_ring);
+  L.v = static_cast<uint16_t*>(v_ring);
+  L.k2 = static_cast<uint16_t*>(k_branch);
+  L.v2 = static_cast<uint16_t*>(v_branch);
+  L.k_new = static_cast<const uint16_t*>(k_new);
+  L.v_new = static_cast<const uint16_t*>(v_new);
+  L.lens = lens;
+  L.depth = depth;
+  L.err = err;
+  L.B = B;
+  L.width = width;
+  L.Hkv = Hkv;
+  L.d = d;
+  L.sink = sink;
+  L.R_w = R_w;
+  L.dd = depth_max;
+  if (wmtp::launch_tree_append(L, static_cast<hipStream_t>(stream)) != hipSuccess) return WMTP_ELAUNCH;
+  return WMTP_OK;
+}
+
+WMTP_EXPORT int wmtp_tree_reset(int32_t* depth, int B, void* stream) {
+  if (B < 0) return WMTP_EINVAL;
+  if (B == 0) return WMTP_OK;
+  if (depth == nullptr || !aligned(depth, 4)) return WMTP_EINVAL;
+  if (wmtp::launch_rollback(depth, nullptr, B, nullptr, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return WMTP_ELAUNCH;
+  return WMTP_OK;
+}
+
+WMTP_EXPORT int wmtp_ring_rollback(int32_t* lens, const int32_t* n_drop, int B, int32_t* err,
+                                   void* stream) {
+  if (B < 0) return WMTP_EINVAL;
+  if (B == 0) return WMTP_OK;
+  if (lens == nullptr || n_drop == nullptr || !aligned(lens, 4) || !aligned(n_drop, 4) ||
+      (err != nullptr && !aligned(err, 4)))
+    return WMTP_EINVAL;
+  if (wmtp::launch_rollback(lens, n_drop, B, err, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return WMTP_ELAUNCH;
+  return WMTP_OK;
 }
 
 WMTP_EXPORT int wmtp_fp8_quantize(const void* x, int64_t n, float scale, void* codes, void* stream) {

@@ -22,10 +22,12 @@ __all__ = [
     "VARIANT_RING",
     "VARIANT_PAGED_FULL",
     "VARIANT_PAGED_WINDOWED",
+    "VARIANT_TREE",
     "DERR_LEN_RANGE",
     "DERR_NNEW_RANGE",
     "DERR_CAPACITY",
     "DERR_SLOT_RANGE",
+    "DERR_DEPTH",
     "lib_path",
     "load_library",
     "workspace_bytes",
@@ -48,13 +50,17 @@ __all__ = [
     "ring_append_fp8",
     "fp8_quantize",
     "fp8_dequantize",
+    "ring_rollback",
+    "tree_append",
+    "tree_attn",
+    "tree_reset",
     "status_string",
     "EXPORTED_SYMBOLS",
 ]
 
 VARIANT_FULL, VARIANT_WINDOWED, VARIANT_RING = 0, 1, 2
-VARIANT_PAGED_FULL, VARIANT_PAGED_WINDOWED = 3, 4
-DERR_LEN_RANGE, DERR_NNEW_RANGE, DERR_CAPACITY, DERR_SLOT_RANGE = 0x1, 0x2, 0x4, 0x8
+VARIANT_PAGED_FULL, VARIANT_PAGED_WINDOWED, VARIANT_TREE = 3, 4, 5
+DERR_LEN_RANGE, DERR_NNEW_RANGE, DERR_CAPACITY, DERR_SLOT_RANGE, DERR_DEPTH = 0x1, 0x2, 0x4, 0x8, 0x10
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, ELAUNCH = 0, 1, 2, 3, 4
 
 EXPORTED_SYMBOLS = (
@@ -79,6 +85,10 @@ EXPORTED_SYMBOLS = (
     "wmtp_cache_append_fp8",
     "wmtp_fp8_quantize",
     "wmtp_fp8_dequantize",
+    "wmtp_ring_rollback",
+    "wmtp_tree_append",
+    "wmtp_tree_attn",
+    "wmtp_tree_reset",
     "wmtp_status_string",
     "wmtp_abi_version",
 )
@@ -115,6 +125,11 @@ _SIGNATURES = {
     "wmtp_cache_append_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I64, _I, _F, _F, _P, _P]),
     "wmtp_fp8_quantize": (_I, [_P, _I64, _F, _P, _P]),
     "wmtp_fp8_dequantize": (_I, [_P, _I64, _P, _P]),
+    "wmtp_ring_rollback": (_I, [_P, _P, _I, _P, _P]),
+    "wmtp_tree_append": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
+    "wmtp_tree_attn": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _SZ,
+                            _P, _P]),
+    "wmtp_tree_reset": (_I, [_P, _I, _P]),
     "wmtp_status_string": (ctypes.c_char_p, [_I]),
     "wmtp_abi_version": (_I, []),
 }
@@ -568,3 +583,80 @@ def fp8_dequantize(codes, out=None):
     st = load_library().wmtp_fp8_dequantize(_ptr(codes), codes.numel(), _ptr(out), _stream(codes.device))
     _check(st, "wmtp_fp8_dequantize")
     return out
+
+
+def ring_rollback(lens, n_drop, err=None):
+    """Discard rejected speculative rows of a chain: lens -= n_drop on the device."""
+    _need(lens, "lens", torch.int32, 1)
+    _need(n_drop, "n_drop", torch.int32, 1, lens.device)
+    if n_drop.shape != lens.shape:
+        raise ValueError("n_drop must have lens' shape")
+    st = load_library().wmtp_ring_rollback(_ptr(lens), _ptr(n_drop), lens.shape[0], _ptr(err), _stream(lens.device))
+    _check(st, "wmtp_ring_rollback")
+
+
+def _tree_store(k_ring, v_ring, k_branch, v_branch, width, depth_max, sink, R_w):
+    _need(k_ring, "k_ring", torch.bfloat16, 4)
+    dev = k_ring.device
+    _need(v_ring, "v_ring", torch.bfloat16, 4, dev)
+    B, rows, Hkv, d = k_ring.shape
+    if v_ring.shape != k_ring.shape or rows != sink + R_w:
+        raise ValueError(f"ring must be [B, sink + R_w = {sink + R_w}, Hkv, d]")
+    if width > 1:
+        _need(k_branch, "k_branch", torch.bfloat16, 4, dev)
+        _need(v_branch, "v_branch", torch.bfloat16, 4, dev)
+        if tuple(k_branch.shape) != (B, (width - 1) * depth_max, Hkv, d) or v_branch.shape != k_branch.shape:
+            raise ValueError(f"private runs must be [B, (width - 1) * depth_max, Hkv, d], got {tuple(k_branch.shape)}")
+    return dev, B, Hkv, d
+
+
+def tree_append(k_ring, v_ring, k_branch, v_branch, k_new, v_new, lens, depth, W, sink, R_w, depth_max, err=None):
+    """One draft row per candidate (k_new [B, width, Hkv, d]) at position lens + depth; depth += 1."""
+    _need(k_new, "k_new", torch.bfloat16, 4)
+    width = k_new.shape[1]
+    dev, B, Hkv, d = _tree_store(k_ring, v_ring, k_branch, v_branch, width, depth_max, sink, R_w)
+    _need(v_new, "v_new", torch.bfloat16, 4, dev)
+    _need(lens, "lens", torch.int32, 1, dev)
+    _need(depth, "depth", torch.int32, 1, dev)
+    if tuple(k_new.shape) != (B, width, Hkv, d) or v_new.shape != k_new.shape:
+        raise ValueError("k_new / v_new must be [B, width, Hkv, d]")
+    st = load_library().wmtp_tree_append(
+        _ptr(k_ring), _ptr(v_ring), _ptr(k_branch), _ptr(v_branch), _ptr(k_new), _ptr(v_new), _ptr(lens), _ptr(depth),
+        B, width, Hkv, d, W, sink, R_w, depth_max, _ptr(err), _stream(dev))
+    _check(st, "wmtp_tree_append")
+
+
+def tree_attn(q, k_ring, v_ring, k_branch, v_branch, lens, depth, W, sink, R_w, depth_max, out=None, lse=None,
+              scale=None, ws=None, err=None):
+    """Windowed draft attention of every speculation candidate: q, out [B, width, Hq, d]."""
+    _need(q, "q", torch.bfloat16, 4)
+    B, width, Hq, d = q.shape
+    dev, B2, Hkv, d2 = _tree_store(k_ring, v_ring, k_branch, v_branch, width, depth_max, sink, R_w)
+    if B2 != B or d2 != d:
+        raise ValueError("q and the ring disagree on B or d")
+    _need(lens, "lens", torch.int32, 1, dev)
+    _need(depth, "depth", torch.int32, 1, dev)
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need(out, "out", torch.bfloat16, 4, dev)
+        if out.shape != q.shape:
+            raise ValueError("out must have q's shape")
+    if lse is not None:
+        _need(lse, "lse", torch.float32, 3, dev)
+        if tuple(lse.shape) != (B, width, Hq):
+            raise ValueError("lse must be [B, width, Hq]")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_TREE, B * width, Hq, Hkv, d, 0, W, sink), dev)
+    st = load_library().wmtp_tree_attn(
+        _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(k_branch), _ptr(v_branch), _ptr(lens), _ptr(depth), _ptr(out),
+        _ptr(lse), B, width, Hq, Hkv, d, W, sink, R_w, depth_max, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_tree_attn")
+    return out
+
+
+def tree_reset(depth):
+    """Speculative depth back to 0 for every request (after the verify)."""
+    _need(depth, "depth", torch.int32, 1)
+    st = load_library().wmtp_tree_reset(_ptr(depth), depth.shape[0], _stream(depth.device))
+    _check(st, "wmtp_tree_reset")

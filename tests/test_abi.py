@@ -55,7 +55,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.wmtp_abi_version() == (1 << 16) | 1
+    assert lib.wmtp_abi_version() == (1 << 16) | 2
     for code in range(5):
         assert W.status_string(code).startswith("WMTP_")
     assert "unknown" in W.status_string(99)
@@ -315,3 +315,53 @@ def test_fp8_conversion_argument_checks(lib):
     assert dq(P + 4, 16, P, None) == W.EINVAL
     assert dq(P, 16, P + 8, None) == W.EINVAL
     assert dq(None, 0, None, None) == W.OK
+
+
+def _tattn(lib, **kw):
+    a = dict(q=P, kr=P, vr=P, kb=P, vb=P, lens=P, depth=P, out=P, lse=None, B=2, width=3, Hq=16, Hkv=2,
+             d=128, W=8, sink=4, R_w=12, dd=4, scale=0.1, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_tree_attn(*a.values())
+
+
+def _tapp(lib, **kw):
+    a = dict(kr=P, vr=P, kb=P, vb=P, kn=P, vn=P, lens=P, depth=P, B=2, width=3, Hkv=2, d=128, W=8, sink=4,
+             R_w=12, dd=4, err=None, stream=None)
+    a.update(kw)
+    return lib.wmtp_tree_append(*a.values())
+
+
+@fake_pointers
+@pytest.mark.parametrize("call", [_tattn, _tapp])
+def test_tree_argument_checks(lib, call):
+    assert call(lib, R_w=11) == W.EINVAL  # the ring needs W + depth_max window slots
+    assert call(lib, dd=0) == W.EINVAL
+    assert call(lib, width=0) == W.EINVAL
+    assert call(lib, W=0) == W.EINVAL
+    assert call(lib, depth=None) == W.EINVAL
+    assert call(lib, kb=None) == W.EINVAL  # candidates 1.. need private runs
+    assert call(lib, kb=P + 8) == W.EINVAL
+    assert call(lib, d=96) == W.EUNSUPPORTED
+    assert call(lib, B=0, kr=None, vr=None, kb=None, vb=None, lens=None, depth=None) == W.OK
+
+
+@fake_pointers
+def test_tree_attn_specific_checks(lib):
+    assert _tattn(lib, ws_bytes=1) == W.EWORKSPACE
+    assert _tattn(lib, q=None) == W.EINVAL
+    assert _tattn(lib, Hq=64, Hkv=2) == W.EUNSUPPORTED
+    assert W.workspace_bytes(W.VARIANT_TREE, 6, 16, 2, 128, 0, 8, 4) == \
+        W.workspace_bytes(W.VARIANT_RING, 6, 16, 2, 128, 12, 8, 4)
+
+
+@fake_pointers
+def test_rollback_argument_checks(lib):
+    rb, rs = lib.wmtp_ring_rollback, lib.wmtp_tree_reset
+    assert rb(None, P, 2, None, None) == W.EINVAL
+    assert rb(P, None, 2, None, None) == W.EINVAL
+    assert rb(P + 2, P, 2, None, None) == W.EINVAL
+    assert rb(P, P, -1, None, None) == W.EINVAL
+    assert rb(None, None, 0, None, None) == W.OK
+    assert rs(None, 2, None) == W.EINVAL
+    assert rs(P + 1, 2, None) == W.EINVAL
+    assert rs(None, 0, None) == W.OK
