@@ -442,6 +442,7 @@ def main(argv=None):
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="skip the extend / paged context figures")
     ap.add_argument("--only-full", action="store_true", help="time only the full-context loop (profiling)")
+    ap.add_argument("--only-fp8", action="store_true", help="time only the fp8-cache calls (profiling)")
     ap.add_argument("--calib-copy", action="store_true", help="also run a 1 GiB device copy (counter calibration)")
     args = ap.parse_args(argv)
 
@@ -465,6 +466,9 @@ def main(argv=None):
         calib_copy(dev)
 
     g = wl.gamma
+    if args.only_fp8:
+        print(json.dumps({"fp8": fp8_figures(loop)}), flush=True)
+        return 0
     log("timing full (eager, events per attention call)")
     wall_full, call_ms = attention_call_times(loop, args.steps, args.warmup)
     us_full_step = wall_full * 1e6 / g
