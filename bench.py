@@ -116,6 +116,38 @@ class DraftLoop:
         self.kr[:, si] = self.k[:, li]
         self.vr[:, si] = self.v[:, li]
         self.lens_r = self.lens0.clone()
+        # length pairs for the fused steps (read one, write the other)
+        self.lp = [self.lens0.clone(), self.lens0.clone()]
+        self.lp_r = [self.lens0.clone(), self.lens0.clone()]
+
+    def _pairs(self, pair):
+        g = self.wl.gamma
+        return [(pair[j % 2], pair[(j + 1) % 2]) for j in range(g)]
+
+    def _settle(self, pair):
+        if self.wl.gamma % 2:  # the last step wrote pair[1]
+            pair[0].copy_(pair[1])
+
+    def step_windowed_fused(self):
+        wl = self.wl
+        for j, (lin, lout) in enumerate(self._pairs(self.lp)):
+            W.draft_step_windowed(self.q[j], self.k, self.v, self.kn[j], self.vn[j], self.ones, lin, lout, wl.W,
+                                  wl.sink, out=self.out[j], ws=self.ws_win, scale=wl.scale)
+        self._settle(self.lp)
+
+    def step_ring_fused(self):
+        wl = self.wl
+        for j, (lin, lout) in enumerate(self._pairs(self.lp_r)):
+            W.ring_step(self.q[j], self.kr, self.vr, self.kn[j], self.vn[j], self.ones, lin, lout, wl.W, wl.sink,
+                        self.R_w, out=self.out[j], ws=self.ws_win, scale=wl.scale)
+        self._settle(self.lp_r)
+
+    def step_full_fused(self):
+        wl = self.wl
+        for j, (lin, lout) in enumerate(self._pairs(self.lp)):
+            W.draft_step_full(self.q[j], self.k, self.v, self.kn[j], self.vn[j], self.ones, lin, lout,
+                              out=self.out[j], ws=self.ws_full, scale=wl.scale)
+        self._settle(self.lp)
 
     def step_full(self):
         wl = self.wl
@@ -482,7 +514,7 @@ def main(argv=None):
 
     res = {"metric": METRIC}
     win_us = ring_us = None
-    sweep = caches = None
+    sweep = caches = fused = None
     if not args.only_full:
         loop.lens.copy_(loop.lens0)
         gw = graph_of(loop.step_windowed)
@@ -494,6 +526,18 @@ def main(argv=None):
         ring_step = timed(gr.replay, args.steps, args.warmup)
         ring_us = ring_step * 1e6 / g
         log(f"windowed: {win_us:.2f} us/draft step, ring: {ring_us:.2f} us/draft step (graph replay)")
+        for pr in loop.lp + loop.lp_r:
+            pr.copy_(loop.lens0)
+        gwf = graph_of(loop.step_windowed_fused)
+        grf = graph_of(loop.step_ring_fused)
+        for pr in loop.lp + loop.lp_r:
+            pr.copy_(loop.lens0)
+        fused = {"windowed_us_per_step": round(timed(gwf.replay, args.steps, args.warmup) * 1e6 / g, 2),
+                 "ring_us_per_step": round(timed(grf.replay, args.steps, args.warmup) * 1e6 / g, 2)}
+        for pr in loop.lp:
+            pr.copy_(loop.lens0)
+        fused["full_us_per_step"] = round(timed(loop.step_full_fused, max(3, args.steps // 2), 1) * 1e6 / g, 2)
+        log("fused append + attention steps: " + ", ".join(f"{k}={v}" for k, v in fused.items()))
         if not args.no_sweep:
             sweep = sweep_flatness(loop, [131072, 262144, 524288, 1048576])
         caches = cache_figures(loop)
@@ -525,6 +569,7 @@ def main(argv=None):
         "full_hbm_gbps": round(achieved, 1),
         "windowed_us_per_step": None if win_us is None else round(win_us, 2),
         "ring_us_per_step": None if ring_us is None else round(ring_us, 2),
+        "fused_step": fused,
         "windowed_speedup_vs_full": None if win_us is None else round(us_full_step / win_us, 1),
         "flatness_sweep": sweep,
         "windowed_hot_cold": caches,

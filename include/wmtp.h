@@ -247,6 +247,40 @@ int wmtp_select_indices(const int32_t* lens, int B, int W, int sink, int R_w, in
                         int32_t* slot_out, int32_t* n_sel_out, int32_t* err, void* stream);
 
 /*
+ * Fused draft step: the append and the attention of one draft step in one
+ * call (the draft forward writes its token's K/V row, then attends; Section
+ * 3, per-step latency model).  For each sequence b, the n_new[b] rows
+ * k_new[b, i], v_new[b, i] (i < n_new[b] <= n_max) take positions
+ * lens_in[b] + i; the one query row q[b] attends at length
+ * lens_in[b] + n_new[b] (full, windowed, or windowed over the ring), reading
+ * the new rows from k_new / v_new; the rows are written into the cache
+ * (ring: the resident ones) and lens_out[b] = lens_in[b] + n_new[b].
+ * Results, cache contents and lengths equal those of wmtp_cache_append /
+ * wmtp_ring_append followed by the attention call, bit for bit; one launch
+ * fewer.  lens_in is only read and lens_out only written; they must be
+ * different arrays (a draft loop alternates two).  A dense cache that would
+ * grow past S_max keeps the rows that fit, lens_out is clamped and
+ * WMTP_DERR_CAPACITY raised.  k_new, v_new [B, n_max, Hkv, d] bf16 (may be
+ * NULL when n_max == 0); workspace as for the attention call of the same
+ * variant.  The ring needs R_w >= W.
+ */
+int wmtp_draft_step_full(const void* q, void* k, void* v, const void* k_new, const void* v_new,
+                         const int32_t* n_new, const int32_t* lens_in, int32_t* lens_out,
+                         void* out, float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
+                         int n_max, float scale, void* ws, size_t ws_bytes, int32_t* err,
+                         void* stream);
+int wmtp_draft_step_windowed(const void* q, void* k, void* v, const void* k_new,
+                             const void* v_new, const int32_t* n_new, const int32_t* lens_in,
+                             int32_t* lens_out, void* out, float* lse, int B, int Hq, int Hkv,
+                             int d, int64_t S_max, int n_max, int W, int sink, float scale,
+                             void* ws, size_t ws_bytes, int32_t* err, void* stream);
+int wmtp_ring_step(const void* q, void* k_ring, void* v_ring, const void* k_new,
+                   const void* v_new, const int32_t* n_new, const int32_t* lens_in,
+                   int32_t* lens_out, void* out, float* lse, int B, int Hq, int Hkv, int d, int W,
+                   int sink, int R_w, int n_max, float scale, void* ws, size_t ws_bytes,
+                   int32_t* err, void* stream);
+
+/*
  * Speculative draft rows.
  *
  * Chain rollback: a chain that appends its speculative draft rows with
@@ -362,7 +396,7 @@ const char* wmtp_status_string(int status);
 /* ABI version of this header, (major << 16) | minor. */
 int wmtp_abi_version(void);
 
-#define WMTP_ABI_VERSION ((1 << 16) | 2)
+#define WMTP_ABI_VERSION ((1 << 16) | 3)
 
 #ifdef __cplusplus
 }

@@ -100,7 +100,8 @@ struct MergeArgs {
   int64_t len_cap;
   int W, sink, target, chunk_cap;
   float out_scale;  // value scale of an fp8 cache (1 for bf16)
-  int dd;           // Tree: largest speculative depth
+  int dd;           // Tree: largest speculative depth; fused step: n_max
+  int32_t* lens_out;  // fused step: each row's new length
 };
 
 __device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap, int32_t* err,
@@ -120,21 +121,31 @@ __device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap,
 // every row of an empty sequence, have no keys; a non-empty sequence with
 // fewer rows than n is flagged.  Returns that length; `b_out` receives the
 // sequence.
-// Tree (speculation candidates): query row v = b * qps + t is candidate t of
-// request b, whose committed length is lens[b] and speculative depth
-// n_q[b] (0 .. dd, clamped and flagged outside); every candidate sees
-// lens[b] + depth rows.  `s_commit` receives the committed length.
-__device__ __forceinline__ int tree_len(const int32_t* lens, const int32_t* depth, int dd, int b,
-                                        int32_t* err, bool report, int& s_commit) {
+// Tail maps.  Tree (speculation candidates): query row v = b * qps + t is
+// candidate t of request b, whose committed length is lens[b] and
+// speculative depth n_q[b] (0 .. dd); every candidate sees lens[b] + depth
+// rows.  Fused draft step: the row sees its old length lens[b] plus the
+// n_q[b] (0 .. dd) rows appended by this call; a dense cache cannot grow
+// past `cap` (flagged, the rows past it dropped).  Out-of-range values are
+// clamped and flagged.  `s_commit` receives the old / committed length.
+template <KeyMap M>
+__device__ __forceinline__ int tail_len(const int32_t* lens, const int32_t* extra, int dd, int64_t cap,
+                                        int b, int32_t* err, bool report, int& s_commit) {
+  constexpr bool kDense = is_step(M) && !is_ring(M);
+  const int64_t lim = kDense ? (cap < INT_MAX - dd ? cap : INT_MAX - dd) : INT_MAX - dd;
   int S = lens[b];
-  if (S < 0 || S > INT_MAX - dd) {
+  if (S < 0 || S > lim) {
     if (report) raise_error(err, WMTP_DERR_LEN_RANGE);
-    S = S < 0 ? 0 : INT_MAX - dd;
+    S = S < 0 ? 0 : static_cast<int>(lim);
   }
-  int i = depth[b];
+  int i = extra[b];
   if (i < 0 || i > dd) {
     if (report) raise_error(err, WMTP_DERR_NNEW_RANGE);
     i = i < 0 ? 0 : dd;
+  }
+  if (kDense && static_cast<int64_t>(S) + i > cap) {
+    if (report) raise_error(err, WMTP_DERR_CAPACITY);
+    i = static_cast<int>(cap - S);
   }
   s_commit = S;
   return S + i;
@@ -144,11 +155,11 @@ template <KeyMap M>
 __device__ __forceinline__ int visible_len(const int32_t* lens, const int32_t* n_q, int qps,
                                            int64_t cap, int32_t* err, int v, bool report,
                                            int& b_out, int dd) {
-  if constexpr (M == KeyMap::Tree) {
+  if constexpr (has_tail(M)) {
     const int b = v / qps;
     b_out = b;
     int s_commit;
-    return tree_len(lens, n_q, dd, b, err, report && v == b * qps, s_commit);
+    return tail_len<M>(lens, n_q, dd, cap, b, err, report && v == b * qps, s_commit);
   }
   const int b = qps == 1 ? v : v / qps;
   const int t = v - b * qps;
@@ -311,12 +322,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int j0 = c * chunk;
   const int j1 = min(j0 + chunk, n_sel);
   RowMap<M> map(S, a.W, a.sink, a.R_w);
-  if constexpr (M == KeyMap::Tree) {
+  if constexpr (has_tail(M)) {
     int s_commit;
-    (void)tree_len(a.lens, a.n_q, a.dd, b, a.err, false, s_commit);
-    const int cand = v - b * a.qps;
+    (void)tail_len<M>(a.lens, a.n_q, a.dd, a.len_cap, b, a.err, false, s_commit);
     map.S_c = s_commit;
-    map.bbase = cand == 0 ? -1 : static_cast<int>(a.rows) + (cand - 1) * a.dd;
+    if constexpr (M == KeyMap::Tree) {
+      const int cand = v - b * a.qps;
+      map.bbase = cand == 0 ? -1 : static_cast<int>(a.rows) + (cand - 1) * a.dd;
+    } else {
+      map.bbase = static_cast<int>(a.rows);
+    }
   }
   const int64_t rs = static_cast<int64_t>(a.Hkv) * D;  // elements between rows
   // Dense and ring caches hold `rows` rows per sequence; a paged pool is one
@@ -328,17 +343,45 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // Tree: rows at or past the ring's `rows` are in the candidate's private run.
   [[maybe_unused]] const int64_t off2 = (static_cast<int64_t>(b) * a.rows2 * a.Hkv + g) * D;
   auto key_row = [&](int r) -> const KT* {
-    if constexpr (M == KeyMap::Tree) {
+    if constexpr (has_tail(M)) {
       if (r >= a.rows) return static_cast<const KT*>(a.k2) + off2 + static_cast<int64_t>(r - a.rows) * rs;
     }
     return kbase + static_cast<int64_t>(r) * rs;
   };
   auto value_row = [&](int r) -> const KT* {
-    if constexpr (M == KeyMap::Tree) {
+    if constexpr (has_tail(M)) {
       if (r >= a.rows) return static_cast<const KT*>(a.v2) + off2 + static_cast<int64_t>(r - a.rows) * rs;
     }
     return vbase + static_cast<int64_t>(r) * rs;
   };
+
+  // Fused draft step: the first work item of a row also writes its KV head's
+  // slice of the appended rows into the cache (ring: the resident ones).  No
+  // workgroup of this launch reads those slots: the appended positions are
+  // read from the new-row buffer, and on a ring (R_w >= W) a slot they
+  // overwrite held a position outside every window of this call.
+  if constexpr (is_step(M)) {
+    if (c == 0) {
+      constexpr int kUnits = D / 8;  // 16-byte units per head row
+      const int n_app = S - map.S_c;
+      uint16_t* kw = const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(kbase));
+      uint16_t* vw = const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(vbase));
+      for (int u = static_cast<int>(threadIdx.x); u < n_app * kUnits; u += kThreads) {
+        const int i = u / kUnits;
+        const int off = (u % kUnits) * 8;
+        const int p = map.S_c + i;
+        int slot = p;
+        if constexpr (is_ring(M)) {
+          if (p >= a.sink && p < S - a.R_w) continue;  // overwritten later in the same append
+          slot = p < a.sink ? p : a.sink + (p - a.sink) % a.R_w;
+        }
+        const int64_t src = off2 + static_cast<int64_t>(i) * rs + off;
+        const int64_t dst = static_cast<int64_t>(slot) * rs + off;
+        *reinterpret_cast<u32x4*>(kw + dst) = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k2) + src);
+        *reinterpret_cast<u32x4*>(vw + dst) = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v2) + src);
+      }
+    }
+  }
 
   // Paged: the pool rows of this item's keys, looked up once into LDS.
   [[maybe_unused]] int* slots = nullptr;
@@ -664,6 +707,13 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
   const int base = s_base;
   const int n = s_cnt;
   auto prow = [&](int c) { return (static_cast<int64_t>(base + c) * a.Hkv + g) * a.G + hl; };
+  if constexpr (is_step(M)) {
+    // The fused step's new length; this launch reads only the old lengths.
+    if (h == 0 && blockIdx.y == 0 && tid == 0) {
+      int bb;
+      a.lens_out[v] = visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, false, bb, a.dd);
+    }
+  }
 
   // Largest partial maximum.
   float mx = neg_inf();
@@ -746,6 +796,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   m.target = L.target; m.chunk_cap = L.chunk_cap;
   m.out_scale = L.v_scale;
   m.dd = L.dd;
+  m.lens_out = L.lens_out;
   const unsigned bh = static_cast<unsigned>(NV) * static_cast<unsigned>(L.Hq);
   if (wide)
     hipLaunchKernelGGL((merge_kernel<D, M, kMergeThreads, 64>), dim3(bh, D / 64), dim3(kMergeThreads), 0,
@@ -763,6 +814,14 @@ hipError_t launch_d(const AttnLaunch& L, hipStream_t st) {
       case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::Window, true>(L, st);
       case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::Ring, true>(L, st);
       default: return hipErrorInvalidValue;  // no fp8 paged kernels
+    }
+  }
+  if (L.step) {
+    switch (L.variant) {
+      case WMTP_VARIANT_FULL: return launch_typed<D, KeyMap::FullStep, false>(L, st);
+      case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::WindowStep, false>(L, st);
+      case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::RingStep, false>(L, st);
+      default: return hipErrorInvalidValue;
     }
   }
   switch (L.variant) {

@@ -29,13 +29,27 @@ namespace wmtp {
 //                      live at their ring slots; positions of candidate
 //                      b >= 1 past the committed length live in its private
 //                      run, rows numbered after the ring's
-enum class KeyMap : int { Full = 0, Window = 1, Ring = 2, PagedFull = 3, PagedWindow = 4, Tree = 5 };
+//   FullStep, WindowStep, RingStep
+//                      a draft step fused with its append: positions before
+//                      the old length live in the cache / ring, the step's
+//                      new rows (at and past it) are read from the caller's
+//                      new-row buffer, rows numbered after the cache's
+enum class KeyMap : int {
+  Full = 0, Window = 1, Ring = 2, PagedFull = 3, PagedWindow = 4, Tree = 5,
+  FullStep = 6, WindowStep = 7, RingStep = 8
+};
 
 constexpr bool is_paged(KeyMap m) { return m == KeyMap::PagedFull || m == KeyMap::PagedWindow; }
 constexpr bool is_windowed(KeyMap m) {
-  return m == KeyMap::Window || m == KeyMap::Ring || m == KeyMap::PagedWindow || m == KeyMap::Tree;
+  return m == KeyMap::Window || m == KeyMap::Ring || m == KeyMap::PagedWindow || m == KeyMap::Tree ||
+         m == KeyMap::WindowStep || m == KeyMap::RingStep;
 }
-constexpr bool is_ring(KeyMap m) { return m == KeyMap::Ring || m == KeyMap::Tree; }
+constexpr bool is_ring(KeyMap m) { return m == KeyMap::Ring || m == KeyMap::Tree || m == KeyMap::RingStep; }
+constexpr bool is_step(KeyMap m) {
+  return m == KeyMap::FullStep || m == KeyMap::WindowStep || m == KeyMap::RingStep;
+}
+// Maps whose keys past a per-row boundary S_c come from a second buffer.
+constexpr bool has_tail(KeyMap m) { return m == KeyMap::Tree || is_step(m); }
 
 template <KeyMap M>
 __device__ __forceinline__ int selected_count(int S, int W, int sink) {
@@ -55,8 +69,8 @@ struct RowMap {
   int R_w;
   int shift;  // position(j) = j + shift for j >= sink
   int r0;     // shift mod R_w (ring maps only)
-  int S_c = 0;     // Tree: committed length
-  int bbase = -1;  // Tree: first row of the candidate's private run (-1: candidate 0)
+  int S_c = 0;     // tail maps: positions >= S_c come from the second buffer ...
+  int bbase = -1;  // ... at rows bbase + (position - S_c); -1: no second buffer
 
   __device__ __forceinline__ RowMap(int S, int W, int sink_, int R_w_) : sink(sink_), R_w(R_w_) {
     shift = (is_windowed(M) && S > sink_ + W) ? S - W - sink_ : 0;
@@ -65,11 +79,18 @@ struct RowMap {
 
   __device__ __forceinline__ int row(int j) const {
     if constexpr (!is_windowed(M)) {
+      if constexpr (has_tail(M)) {
+        if (j >= S_c) return bbase + (j - S_c);
+      }
       return j;
     } else if constexpr (!is_ring(M)) {
-      return j < sink ? j : j + shift;
+      const int pos = j < sink ? j : j + shift;
+      if constexpr (has_tail(M)) {
+        if (pos >= S_c) return bbase + (pos - S_c);
+      }
+      return pos;
     } else {
-      if constexpr (M == KeyMap::Tree) {
+      if constexpr (has_tail(M)) {
         const int pos = j < sink ? j : j + shift;
         if (bbase >= 0 && pos >= S_c) return bbase + (pos - S_c);
       }

@@ -33,6 +33,11 @@ struct AttnLaunch {
   const void* v2;
   int64_t rows2;
   int dd;  // largest speculative depth (private-run length)
+  // Fused draft step (variants full / windowed / ring): n_q holds n_new, k2 /
+  // v2 the new rows [B, dd = n_max, Hkv, d]; the split kernel writes them into
+  // the cache and the merge writes lens_out = old length + rows appended.
+  bool step;
+  int32_t* lens_out;
   // split plan (from plan_split)
   int target;     // work items per KV head to aim for
   int chunk_cap;  // largest work item, in keys

@@ -70,14 +70,20 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
                      float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream,
                      const int32_t* table = nullptr, int64_t pool_rows = 0, bool fp8 = false,
                      float k_scale = 1.0f, float v_scale = 1.0f, const void* k2 = nullptr,
-                     const void* v2 = nullptr, int dd = 0) {
+                     const void* v2 = nullptr, int dd = 0, bool step = false,
+                     int32_t* lens_out = nullptr) {
   int st = check_heads(B, Hq, Hkv, d);
   if (st != WMTP_OK) return st;
   const bool tree = variant == WMTP_VARIANT_TREE;
   // Tree: q_max candidates per request; the ring's window region holds the
   // window plus the draft-extend headroom (R_w >= W + dd), candidates 1 ..
-  // q_max - 1 own private runs of dd rows.
-  const int64_t rows2 = tree ? static_cast<int64_t>(q_max - 1) * dd : 0;
+  // q_max - 1 own private runs of dd rows.  Fused step: k2 / v2 hold the
+  // dd = n_max new rows per sequence.
+  const int64_t rows2 = tree ? static_cast<int64_t>(q_max - 1) * dd : (step ? dd : 0);
+  if (step) {
+    if (fp8 || tree || paged_variant(variant) || q_max != 1 || dd < 0) return WMTP_EINVAL;
+    if (variant != WMTP_VARIANT_RING && S_max + dd > INT_MAX) return WMTP_EINVAL;
+  }
   if (tree) {
     if (fp8 || dd < 1 || q_max < 1) return WMTP_EINVAL;
     if (static_cast<int64_t>(R_w) < static_cast<int64_t>(W) + dd) return WMTP_EINVAL;
@@ -103,9 +109,10 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   if (q == nullptr || k == nullptr || v == nullptr || lens == nullptr || out == nullptr)
     return WMTP_EINVAL;
   if (paged_variant(variant) && (table == nullptr || !aligned(table, 4))) return WMTP_EINVAL;
-  if (tree && (n_q == nullptr || (rows2 > 0 && (k2 == nullptr || v2 == nullptr || !aligned(k2, 16) ||
-                                                 !aligned(v2, 16)))))
+  if ((tree || step) && (n_q == nullptr || (rows2 > 0 && (k2 == nullptr || v2 == nullptr ||
+                                                           !aligned(k2, 16) || !aligned(v2, 16)))))
     return WMTP_EINVAL;
+  if (step && (lens_out == nullptr || !aligned(lens_out, 4) || lens_out == lens)) return WMTP_EINVAL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
       !aligned(lens, 4) || (lse != nullptr && !aligned(lse, 4)) ||
       (err != nullptr && !aligned(err, 4)) || (n_q != nullptr && !aligned(n_q, 4)))
@@ -140,6 +147,8 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   L.v2 = v2;
   L.rows2 = rows2;
   L.dd = dd;
+  L.step = step;
+  L.lens_out = lens_out;
   if (variant == WMTP_VARIANT_RING || tree) {
     L.rows = static_cast<int64_t>(sink) + R_w;
     L.len_cap = INT_MAX;
@@ -400,6 +409,41 @@ WMTP_EXPORT int wmtp_cache_append_fp8(void* k, void* v, const void* k_new, const
                                       int32_t* err, void* stream) {
   return append_common(false, k, v, k_new, v_new, n_new, lens, B, Hkv, d, S_max, 0, 1, n_max, err,
                        stream, true, k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_draft_step_full(const void* q, void* k, void* v, const void* k_new,
+                                     const void* v_new, const int32_t* n_new,
+                                     const int32_t* lens_in, int32_t* lens_out, void* out,
+                                     float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
+                                     int n_max, float scale, void* ws, size_t ws_bytes,
+                                     int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_FULL, q, k, v, lens_in, n_new, 1, out, lse, B, Hq, Hkv, d,
+                          S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream, nullptr, 0, false, 1.0f,
+                          1.0f, k_new, v_new, n_max, true, lens_out);
+}
+
+WMTP_EXPORT int wmtp_draft_step_windowed(const void* q, void* k, void* v, const void* k_new,
+                                         const void* v_new, const int32_t* n_new,
+                                         const int32_t* lens_in, int32_t* lens_out, void* out,
+                                         float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
+                                         int n_max, int W, int sink, float scale, void* ws,
+                                         size_t ws_bytes, int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens_in, n_new, 1, out, lse, B, Hq, Hkv,
+                          d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream, nullptr, 0, false,
+                          1.0f, 1.0f, k_new, v_new, n_max, true, lens_out);
+}
+
+WMTP_EXPORT int wmtp_ring_step(const void* q, void* k_ring, void* v_ring, const void* k_new,
+                               const void* v_new, const int32_t* n_new, const int32_t* lens_in,
+                               int32_t* lens_out, void* out, float* lse, int B, int Hq, int Hkv,
+                               int d, int W, int sink, int R_w, int n_max, float scale, void* ws,
+                               size_t ws_bytes, int32_t* err, void* stream) {
+  if (check_window(W, sink) == WMTP_OK && (R_w < W || static_cast<int64_t>(sink) + R_w > INT_MAX))
+    return WMTP_EINVAL;
+  return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens_in, n_new, 1, out, lse, B, Hq,
+                          Hkv, d, static_cast<int64_t>(sink) + R_w, W, sink, R_w, scale, ws,
+                          ws_bytes, err, stream, nullptr, 0, false, 1.0f, 1.0f, k_new, v_new, n_max,
+                          true, lens_out);
 }
 
 WMTP_EXPORT int wmtp_tree_attn(const void* q, const void* k_ring, const void* v_ring,

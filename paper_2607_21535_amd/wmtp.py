@@ -50,6 +50,9 @@ __all__ = [
     "ring_append_fp8",
     "fp8_quantize",
     "fp8_dequantize",
+    "draft_step_full",
+    "draft_step_windowed",
+    "ring_step",
     "ring_rollback",
     "tree_append",
     "tree_attn",
@@ -85,6 +88,9 @@ EXPORTED_SYMBOLS = (
     "wmtp_cache_append_fp8",
     "wmtp_fp8_quantize",
     "wmtp_fp8_dequantize",
+    "wmtp_draft_step_full",
+    "wmtp_draft_step_windowed",
+    "wmtp_ring_step",
     "wmtp_ring_rollback",
     "wmtp_tree_append",
     "wmtp_tree_attn",
@@ -126,6 +132,12 @@ _SIGNATURES = {
     "wmtp_fp8_quantize": (_I, [_P, _I64, _F, _P, _P]),
     "wmtp_fp8_dequantize": (_I, [_P, _I64, _P, _P]),
     "wmtp_ring_rollback": (_I, [_P, _P, _I, _P, _P]),
+    "wmtp_draft_step_full": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _F, _P, _SZ,
+                                  _P, _P]),
+    "wmtp_draft_step_windowed": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _I, _F,
+                                      _P, _SZ, _P, _P]),
+    "wmtp_ring_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _SZ,
+                            _P, _P]),
     "wmtp_tree_append": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P]),
     "wmtp_tree_attn": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _SZ,
                             _P, _P]),
@@ -660,3 +672,62 @@ def tree_reset(depth):
     _need(depth, "depth", torch.int32, 1)
     st = load_library().wmtp_tree_reset(_ptr(depth), depth.shape[0], _stream(depth.device))
     _check(st, "wmtp_tree_reset")
+
+
+def _step_io(q, k, v, k_new, v_new, n_new, lens_in, lens_out, out, lse):
+    dev, B, Hq, d, out = _attn_io(q, k, v, lens_in, out, lse)
+    _need(k_new, "k_new", torch.bfloat16, 4, dev)
+    _need(v_new, "v_new", torch.bfloat16, 4, dev)
+    _need(n_new, "n_new", torch.int32, 1, dev)
+    _need(lens_out, "lens_out", torch.int32, 1, dev)
+    Hkv = k.shape[2]
+    if (k_new.shape != v_new.shape or k_new.shape[0] != B or tuple(k_new.shape[2:]) != (Hkv, d)
+            or n_new.shape[0] != B or lens_out.shape[0] != B):
+        raise ValueError("step shape mismatch")
+    if lens_out.data_ptr() == lens_in.data_ptr():
+        raise ValueError("lens_out must be a different array from lens_in")
+    return dev, B, Hq, Hkv, d, k_new.shape[1], out
+
+
+def draft_step_full(q, k, v, k_new, v_new, n_new, lens_in, lens_out, out=None, lse=None, scale=None, ws=None,
+                    err=None):
+    """Append n_new rows at lens_in, attend the full context; lens_out = lens_in + n_new."""
+    dev, B, Hq, Hkv, d, n_max, out = _step_io(q, k, v, k_new, v_new, n_new, lens_in, lens_out, out, lse)
+    S_max = k.shape[1]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_FULL, B, Hq, Hkv, d, S_max), dev)
+    st = load_library().wmtp_draft_step_full(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(lens_in), _ptr(lens_out), _ptr(out),
+        _ptr(lse), B, Hq, Hkv, d, S_max, n_max, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_step_full")
+    return out
+
+
+def draft_step_windowed(q, k, v, k_new, v_new, n_new, lens_in, lens_out, W, sink, out=None, lse=None, scale=None,
+                        ws=None, err=None):
+    """Append n_new rows at lens_in, attend sink + window; lens_out = lens_in + n_new."""
+    dev, B, Hq, Hkv, d, n_max, out = _step_io(q, k, v, k_new, v_new, n_new, lens_in, lens_out, out, lse)
+    S_max = k.shape[1]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_WINDOWED, B, Hq, Hkv, d, S_max, W, sink), dev)
+    st = load_library().wmtp_draft_step_windowed(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(lens_in), _ptr(lens_out), _ptr(out),
+        _ptr(lse), B, Hq, Hkv, d, S_max, n_max, W, sink, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_step_windowed")
+    return out
+
+
+def ring_step(q, k_ring, v_ring, k_new, v_new, n_new, lens_in, lens_out, W, sink, R_w, out=None, lse=None,
+              scale=None, ws=None, err=None):
+    """Append n_new rows to the ring at lens_in, attend sink + window; lens_out = lens_in + n_new."""
+    dev, B, Hq, Hkv, d, n_max, out = _step_io(q, k_ring, v_ring, k_new, v_new, n_new, lens_in, lens_out, out, lse)
+    if k_ring.shape[1] != sink + R_w:
+        raise ValueError(f"ring must hold sink + R_w = {sink + R_w} rows, has {k_ring.shape[1]}")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_RING, B, Hq, Hkv, d, sink + R_w, W, sink), dev)
+    st = load_library().wmtp_ring_step(
+        _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(lens_in), _ptr(lens_out),
+        _ptr(out), _ptr(lse), B, Hq, Hkv, d, W, sink, R_w, n_max, scale, _ptr(ws), _wsize(ws), _ptr(err),
+        _stream(dev))
+    _check(st, "wmtp_ring_step")
+    return out

@@ -55,7 +55,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.wmtp_abi_version() == (1 << 16) | 2
+    assert lib.wmtp_abi_version() == (1 << 16) | 3
     for code in range(5):
         assert W.status_string(code).startswith("WMTP_")
     assert "unknown" in W.status_string(99)
@@ -365,3 +365,39 @@ def test_rollback_argument_checks(lib):
     assert rs(None, 2, None) == W.EINVAL
     assert rs(P + 1, 2, None) == W.EINVAL
     assert rs(None, 0, None) == W.OK
+
+
+def _step(lib, fn, **kw):
+    if fn == "ring":
+        a = dict(q=P, k=P, v=P, kn=P, vn=P, nn=P, li=P, lo=P + 256, out=P, lse=None, B=2, Hq=16, Hkv=2, d=128,
+                 W=8, sink=4, R_w=8, n_max=2, scale=0.1, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+        a.update(kw)
+        return lib.wmtp_ring_step(*a.values())
+    a = dict(q=P, k=P, v=P, kn=P, vn=P, nn=P, li=P, lo=P + 256, out=P, lse=None, B=2, Hq=16, Hkv=2, d=128,
+             S_max=100, n_max=2)
+    if fn == "windowed":
+        a.update(W=8, sink=4)
+    a.update(scale=0.1, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    a.update(kw)
+    f = lib.wmtp_draft_step_full if fn == "full" else lib.wmtp_draft_step_windowed
+    return f(*a.values())
+
+
+@fake_pointers
+@pytest.mark.parametrize("fn", ["full", "windowed", "ring"])
+def test_step_argument_checks(lib, fn):
+    assert _step(lib, fn, lo=P) == W.EINVAL  # lens_out must not alias lens_in
+    assert _step(lib, fn, lo=None) == W.EINVAL
+    assert _step(lib, fn, lo=P + 2) == W.EINVAL
+    assert _step(lib, fn, nn=None) == W.EINVAL
+    assert _step(lib, fn, kn=None) == W.EINVAL
+    assert _step(lib, fn, vn=P + 8) == W.EINVAL
+    assert _step(lib, fn, n_max=-1) == W.EINVAL
+    assert _step(lib, fn, d=96) == W.EUNSUPPORTED
+    assert _step(lib, fn, ws_bytes=1) == W.EWORKSPACE
+    assert _step(lib, fn, B=0, q=None, k=None, v=None, kn=None, vn=None, nn=None, li=None, lo=None,
+                 out=None) == W.OK
+    if fn == "ring":
+        assert _step(lib, fn, R_w=7) == W.EINVAL
+    else:
+        assert _step(lib, fn, S_max=(1 << 31) - 2, n_max=4) == W.EINVAL  # positions must fit int32
