@@ -256,8 +256,12 @@ int wmtp_select_indices(const int32_t* lens, int B, int W, int sink, int R_w, in
  * the new rows from k_new / v_new; the rows are written into the cache
  * (ring: the resident ones) and lens_out[b] = lens_in[b] + n_new[b].
  * Results, cache contents and lengths equal those of wmtp_cache_append /
- * wmtp_ring_append followed by the attention call, bit for bit; one launch
- * fewer.  lens_in is only read and lens_out only written; they must be
+ * wmtp_ring_append followed by the attention call, bit for bit.  The
+ * windowed and ring steps are one launch fewer (the attention reads the new
+ * rows from k_new / v_new and writes them into the cache); the full step
+ * runs the append and then the full attention (redirecting the new rows
+ * would cost the O(S) kernel more than the launch it saves).  lens_in is
+ * only read and lens_out only written; they must be
  * different arrays (a draft loop alternates two).  A dense cache that would
  * grow past S_max keeps the rows that fit, lens_out is clamped and
  * WMTP_DERR_CAPACITY raised.  k_new, v_new [B, n_max, Hkv, d] bf16 (may be

@@ -124,7 +124,7 @@ __device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap,
 // Tail maps.  Tree (speculation candidates): query row v = b * qps + t is
 // candidate t of request b, whose committed length is lens[b] and
 // speculative depth n_q[b] (0 .. dd); every candidate sees lens[b] + depth
-// rows.  Fused draft step: the row sees its old length lens[b] plus the
+// rows.  Fused windowed draft step: the row sees its old length lens[b] plus the
 // n_q[b] (0 .. dd) rows appended by this call; a dense cache cannot grow
 // past `cap` (flagged, the rows past it dropped).  Out-of-range values are
 // clamped and flagged.  `s_commit` receives the old / committed length.
@@ -818,7 +818,6 @@ hipError_t launch_d(const AttnLaunch& L, hipStream_t st) {
   }
   if (L.step) {
     switch (L.variant) {
-      case WMTP_VARIANT_FULL: return launch_typed<D, KeyMap::FullStep, false>(L, st);
       case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::WindowStep, false>(L, st);
       case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::RingStep, false>(L, st);
       default: return hipErrorInvalidValue;

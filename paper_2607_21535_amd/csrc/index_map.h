@@ -29,14 +29,14 @@ namespace wmtp {
 //                      live at their ring slots; positions of candidate
 //                      b >= 1 past the committed length live in its private
 //                      run, rows numbered after the ring's
-//   FullStep, WindowStep, RingStep
-//                      a draft step fused with its append: positions before
-//                      the old length live in the cache / ring, the step's
-//                      new rows (at and past it) are read from the caller's
-//                      new-row buffer, rows numbered after the cache's
+//   WindowStep, RingStep
+//                      a windowed draft step fused with its append:
+//                      positions before the old length live in the cache /
+//                      ring, the step's new rows (at and past it) are read
+//                      from the caller's new-row buffer, rows numbered after
+//                      the cache's
 enum class KeyMap : int {
-  Full = 0, Window = 1, Ring = 2, PagedFull = 3, PagedWindow = 4, Tree = 5,
-  FullStep = 6, WindowStep = 7, RingStep = 8
+  Full = 0, Window = 1, Ring = 2, PagedFull = 3, PagedWindow = 4, Tree = 5, WindowStep = 7, RingStep = 8
 };
 
 constexpr bool is_paged(KeyMap m) { return m == KeyMap::PagedFull || m == KeyMap::PagedWindow; }
@@ -45,9 +45,7 @@ constexpr bool is_windowed(KeyMap m) {
          m == KeyMap::WindowStep || m == KeyMap::RingStep;
 }
 constexpr bool is_ring(KeyMap m) { return m == KeyMap::Ring || m == KeyMap::Tree || m == KeyMap::RingStep; }
-constexpr bool is_step(KeyMap m) {
-  return m == KeyMap::FullStep || m == KeyMap::WindowStep || m == KeyMap::RingStep;
-}
+constexpr bool is_step(KeyMap m) { return m == KeyMap::WindowStep || m == KeyMap::RingStep; }
 // Maps whose keys past a per-row boundary S_c come from a second buffer.
 constexpr bool has_tail(KeyMap m) { return m == KeyMap::Tree || is_step(m); }
 

@@ -33,6 +33,7 @@ struct AppendArgs {
   int64_t rows;
   int sink, R_w, n_max;
   float k_scale, v_scale;  // fp8: per-tensor scales the rows are divided by
+  int32_t* lens_out;       // NULL: advance lens in place
 };
 
 template <bool RING, bool F8>
@@ -91,6 +92,10 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
       *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.k) + dst) = kx;
       *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.v) + dst) = vx;
     }
+  }
+  if (a.lens_out != nullptr) {
+    if (threadIdx.x == 0) a.lens_out[b] = S_new;
+    return;
   }
   __syncthreads();  // every thread has read lens[b] before it changes
   if (threadIdx.x == 0) a.lens[b] = S_new;
@@ -213,6 +218,7 @@ hipError_t launch_append(const AppendLaunch& L, hipStream_t st) {
   a.B = L.B; a.Hkv = L.Hkv; a.d = L.d; a.rows = L.rows;
   a.sink = L.sink; a.R_w = L.R_w; a.n_max = L.n_max;
   a.k_scale = L.k_scale; a.v_scale = L.v_scale;
+  a.lens_out = L.lens_out;
   const dim3 grid(L.B), block(256);
   if (L.ring) {
     if (L.fp8)

@@ -33,7 +33,7 @@ struct AttnLaunch {
   const void* v2;
   int64_t rows2;
   int dd;  // largest speculative depth (private-run length)
-  // Fused draft step (variants full / windowed / ring): n_q holds n_new, k2 /
+  // Fused draft step (variants windowed / ring): n_q holds n_new, k2 /
   // v2 the new rows [B, dd = n_max, Hkv, d]; the split kernel writes them into
   // the cache and the merge writes lens_out = old length + rows appended.
   bool step;
@@ -84,6 +84,7 @@ struct AppendLaunch {
   int64_t rows;     // dense: S_max; ring: sink + R_w
   int sink, R_w, n_max;
   float k_scale, v_scale;
+  int32_t* lens_out;  // NULL: lens is advanced in place; else lens is only read
 };
 
 hipError_t launch_append(const AppendLaunch& a, hipStream_t stream);

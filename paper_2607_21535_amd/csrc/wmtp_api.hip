@@ -71,7 +71,7 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
                      const int32_t* table = nullptr, int64_t pool_rows = 0, bool fp8 = false,
                      float k_scale = 1.0f, float v_scale = 1.0f, const void* k2 = nullptr,
                      const void* v2 = nullptr, int dd = 0, bool step = false,
-                     int32_t* lens_out = nullptr) {
+                     int32_t* lens_out = nullptr, bool dry_run = false) {
   int st = check_heads(B, Hq, Hkv, d);
   if (st != WMTP_OK) return st;
   const bool tree = variant == WMTP_VARIANT_TREE;
@@ -81,7 +81,8 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   // dd = n_max new rows per sequence.
   const int64_t rows2 = tree ? static_cast<int64_t>(q_max - 1) * dd : (step ? dd : 0);
   if (step) {
-    if (fp8 || tree || paged_variant(variant) || q_max != 1 || dd < 0) return WMTP_EINVAL;
+    if (fp8 || tree || paged_variant(variant) || variant == WMTP_VARIANT_FULL || q_max != 1 || dd < 0)
+      return WMTP_EINVAL;
     if (variant != WMTP_VARIANT_RING && S_max + dd > INT_MAX) return WMTP_EINVAL;
   }
   if (tree) {
@@ -168,6 +169,7 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   L.target = plan.target;
   L.chunk_cap = plan.chunk_cap;
   L.max_items = plan.max_items;
+  if (dry_run) return WMTP_OK;
   char* base = static_cast<char*>(ws);
   L.pm = reinterpret_cast<float*>(base);
   L.pl = reinterpret_cast<float*>(base + plan.off_pl);
@@ -181,7 +183,8 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
 int append_common(bool ring, void* k, void* v, const void* k_new, const void* v_new,
                   const int32_t* n_new, int32_t* lens, int B, int Hkv, int d, int64_t rows,
                   int sink, int R_w, int n_max, int32_t* err, void* stream, bool fp8 = false,
-                  float k_scale = 1.0f, float v_scale = 1.0f) {
+                  float k_scale = 1.0f, float v_scale = 1.0f, int32_t* lens_out = nullptr,
+                  bool dry_run = false) {
   if (B < 0 || Hkv < 1 || d < 1 || n_max < 0) return WMTP_EINVAL;
   if (fp8 && (!valid_scale(k_scale) || !valid_scale(v_scale))) return WMTP_EINVAL;
   if (d != 64 && d != 128 && d != 256) return WMTP_EUNSUPPORTED;
@@ -192,8 +195,10 @@ int append_common(bool ring, void* k, void* v, const void* k_new, const void* v_
   if (k == nullptr || v == nullptr || lens == nullptr || n_new == nullptr) return WMTP_EINVAL;
   if (n_max > 0 && (k_new == nullptr || v_new == nullptr)) return WMTP_EINVAL;
   if (!aligned(k, 16) || !aligned(v, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) ||
-      !aligned(n_new, 4) || !aligned(lens, 4) || (err != nullptr && !aligned(err, 4)))
+      !aligned(n_new, 4) || !aligned(lens, 4) || (err != nullptr && !aligned(err, 4)) ||
+      (lens_out != nullptr && (!aligned(lens_out, 4) || lens_out == lens)))
     return WMTP_EINVAL;
+  if (dry_run) return WMTP_OK;
   wmtp::AppendLaunch L{};
   L.ring = ring;
   L.fp8 = fp8;
@@ -213,6 +218,7 @@ int append_common(bool ring, void* k, void* v, const void* k_new, const void* v_
   L.sink = ring ? sink : 0;
   L.R_w = ring ? R_w : 1;
   L.n_max = n_max;
+  L.lens_out = lens_out;
   if (wmtp::launch_append(L, static_cast<hipStream_t>(stream)) != hipSuccess) return WMTP_ELAUNCH;
   return WMTP_OK;
 }
@@ -417,9 +423,23 @@ WMTP_EXPORT int wmtp_draft_step_full(const void* q, void* k, void* v, const void
                                      float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
                                      int n_max, float scale, void* ws, size_t ws_bytes,
                                      int32_t* err, void* stream) {
-  return attention_common(WMTP_VARIANT_FULL, q, k, v, lens_in, n_new, 1, out, lse, B, Hq, Hkv, d,
-                          S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream, nullptr, 0, false, 1.0f,
-                          1.0f, k_new, v_new, n_max, true, lens_out);
+  // The full-context step is the append (lens_in -> lens_out) followed by the
+  // full attention at lens_out: reading the new rows through the fused path
+  // costs the O(S) kernel more than the separate append launch saves.
+  if (B > 0 && (lens_in == nullptr || lens_out == nullptr)) return WMTP_EINVAL;
+  int32_t* lin = const_cast<int32_t*>(lens_in);
+  int st = append_common(false, k, v, k_new, v_new, n_new, lin, B, Hkv, d, S_max, 0, 1, n_max, err,
+                         stream, false, 1.0f, 1.0f, lens_out, true);
+  if (st != WMTP_OK) return st;
+  st = attention_common(WMTP_VARIANT_FULL, q, k, v, lens_out, nullptr, 1, out, lse, B, Hq, Hkv, d,
+                        S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream, nullptr, 0, false, 1.0f,
+                        1.0f, nullptr, nullptr, 0, false, nullptr, true);
+  if (st != WMTP_OK) return st;
+  st = append_common(false, k, v, k_new, v_new, n_new, lin, B, Hkv, d, S_max, 0, 1, n_max, err, stream,
+                     false, 1.0f, 1.0f, lens_out);
+  if (st != WMTP_OK) return st;
+  return attention_common(WMTP_VARIANT_FULL, q, k, v, lens_out, nullptr, 1, out, lse, B, Hq, Hkv, d,
+                          S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream);
 }
 
 WMTP_EXPORT int wmtp_draft_step_windowed(const void* q, void* k, void* v, const void* k_new,
