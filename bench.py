@@ -15,9 +15,15 @@ Timed variants (each its own timed region of --steps steps):
 the windowed and ring loops are captured once in a HIP graph and replayed.
 Also reported: windowed/full time per draft step at 128K, 256K, 512K and 1M
 (same cache, shorter lengths: the window's cost must not grow with S), and
-the float64 CPU oracle timed on a bounded sample on this host, and context
-figures: draft-extend over gamma+1 new rows, the paged pool's KV-index build
-(native vs windowed) and paged attention over a shuffled pool.
+the float64 CPU oracle timed on a bounded sample on this host, the fused
+append + attention steps, and context figures: draft-extend over gamma+1 new
+rows, the paged pool's KV-index build (native vs windowed), paged attention
+over a shuffled pool, and the same attention over an fp8 cache.
+
+--workload selects another configuration: decode_s8k and draft_loop_s128k
+run the same loop at their shapes; batch32_varlen times one decode call over
+32 sequences of 64K..1M keys (full and windowed); ring_b8 times the 1000
+iterations of ring appends and ring attention.
 
 Prints one JSON line.  --gpus N with N > 1 is not supported (one GPU).
 """
@@ -441,6 +447,104 @@ def cpu_baseline(loop, budget_s=20.0):
     }
 
 
+def bench_batch(wl, dev, args):
+    """Variable-length batch: one decode call over B sequences, full and
+    windowed (one query row per sequence, lengths from the workload seed)."""
+    log(f"generating {wl.name}: B={wl.B} S in [{wl.S_lo}, {wl.S}]")
+    case = I.decode_case(wl, dev, steps=1)
+    k, v, q = case["k"], case["v"], case["q"][0]
+    lens = torch.as_tensor(case["lens"], device=dev)
+    S_max = case["S_max"]
+    B, Hq, Hkv, d = wl.B, wl.Hq, wl.Hkv, wl.d
+    ws_f = torch.empty(W.workspace_bytes(W.VARIANT_FULL, B, Hq, Hkv, d, S_max), dtype=torch.uint8, device=dev)
+    ws_w = torch.empty(W.workspace_bytes(W.VARIANT_WINDOWED, B, Hq, Hkv, d, S_max, wl.W, wl.sink),
+                       dtype=torch.uint8, device=dev)
+    out = torch.empty_like(q)
+    full = event_us(lambda: W.draft_attn_full(q, k, v, lens, out=out, ws=ws_f, scale=wl.scale),
+                    reps=args.steps, warm=args.warmup)
+    win = graph_us(lambda: W.draft_attn_windowed(q, k, v, lens, wl.W, wl.sink, out=out, ws=ws_w, scale=wl.scale))
+    tot = int(case["lens"].astype(np.int64).sum())
+    alg = tot * Hkv * d * 4 + 2 * B * Hq * d * 2
+    gbps = alg / full / 1e3
+    log(f"{wl.name}: full {full:.1f} us ({gbps:.0f} GB/s over {tot} keys), windowed {win:.2f} us")
+    return {"metric": METRIC, "value": round(full, 1), "unit": "us/call", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(full / 1e3, 4), "higher_is_better": False,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic: seeded N(0,1) bf16 KV",
+            "config": {"workload": wl.name, "B": B, "Hq": Hq, "Hkv": Hkv, "d": d, "S_lo": wl.S_lo, "S_hi": wl.S,
+                       "total_keys": tot, "W": wl.W, "sink": wl.sink, "step": "one decode call (B query rows)"},
+            "full_us": round(full, 1), "windowed_us": round(win, 2),
+            "roofline": {"bound": "hbm", "kernel": "full-context attention call (split + merge)",
+                         "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                         "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                         "algorithmic_bytes_per_launch": alg}}
+
+
+def bench_ring(wl, dev, args):
+    """The ring workload: every iteration appends U{1..max_accept} rows per
+    sequence to the ring and attends (unfused, and as one fused ring step);
+    all iterations captured in graphs of 100 and replayed back to back."""
+    B, Hq, Hkv, d, n_max = wl.B, wl.Hq, wl.Hkv, wl.d, wl.max_accept
+    its = wl.iterations
+    log(f"generating {wl.name}: {its} iterations")
+    acc = I.accept_counts(its, B, n_max, I.stream_seed(wl.seed, I.STREAM_ACCEPT))
+    n_new = torch.as_tensor(acc, device=dev)
+    kn = torch.stack([I.normal_bf16((B, n_max, Hkv, d), I.stream_seed(wl.seed, I.STREAM_KNEW, it), dev)
+                      for it in range(its)])
+    vn = torch.stack([I.normal_bf16((B, n_max, Hkv, d), I.stream_seed(wl.seed, I.STREAM_VNEW, it), dev)
+                      for it in range(its)])
+    q = torch.stack([I.normal_bf16((B, Hq, d), I.stream_seed(wl.seed, I.STREAM_Q, it), dev) for it in range(its)])
+    R_w = wl.R_w
+    kr = torch.zeros((B, wl.sink + R_w, Hkv, d), dtype=torch.bfloat16, device=dev)
+    vr = torch.zeros_like(kr)
+    lens = torch.zeros(B, dtype=torch.int32, device=dev)
+    lp = [torch.zeros_like(lens), torch.zeros_like(lens)]
+    out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(W.workspace_bytes(W.VARIANT_RING, B, Hq, Hkv, d, wl.sink + R_w, wl.W, wl.sink),
+                     dtype=torch.uint8, device=dev)
+
+    def unfused(lo, hi):
+        def f():
+            for it in range(lo, hi):
+                W.ring_append(kr, vr, kn[it], vn[it], n_new[it], lens, wl.sink, R_w)
+                W.ring_attn(q[it], kr, vr, lens, wl.W, wl.sink, R_w, out=out, ws=ws, scale=wl.scale)
+        return f
+
+    def fused(lo, hi):
+        def f():
+            for it in range(lo, hi):
+                W.ring_step(q[it], kr, vr, kn[it], vn[it], n_new[it], lp[it % 2], lp[(it + 1) % 2], wl.W, wl.sink,
+                            R_w, out=out, ws=ws, scale=wl.scale)
+        return f
+
+    res = {}
+    for name, mk in (("unfused", unfused), ("fused", fused)):
+        graphs = [graph_of(mk(lo, lo + 100)) for lo in range(0, its, 100)]
+        ts = []
+        for _ in range(3):
+            kr.zero_()
+            vr.zero_()
+            lens.zero_()
+            for t in lp:
+                t.zero_()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for gr in graphs:
+                gr.replay()
+            torch.cuda.synchronize()
+            ts.append(time.perf_counter() - t0)
+        res[name] = float(np.median(ts)) * 1e6 / its
+    log(f"{wl.name}: {res['unfused']:.2f} us per iteration (append + ring attention), fused ring step "
+        f"{res['fused']:.2f} us")
+    return {"metric": METRIC, "value": round(res["unfused"], 2), "unit": "us/iteration", "n_gpus": 1,
+            "steps": its, "warmup": 0, "ms_per_step": round(res["unfused"] / 1e3, 5), "higher_is_better": False,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic: seeded N(0,1) bf16 KV",
+            "config": {"workload": wl.name, "B": B, "Hq": Hq, "Hkv": Hkv, "d": d, "W": wl.W, "sink": wl.sink,
+                       "ring_slots": wl.sink + R_w, "iterations": its, "accepted_rows": f"U{{1..{n_max}}}",
+                       "step": "append accepted rows + ring attention, B sequences"},
+            "unfused_us_per_iteration": round(res["unfused"], 2), "fused_us_per_iteration": round(res["fused"], 2),
+            "roofline": None}
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -489,9 +593,9 @@ def main(argv=None):
     dev = torch.device("cuda:0")
     W.load_library()
     wl = I.WORKLOADS[args.workload]
-    if wl.S_lo or wl.R_w:
-        print("bench.py times the single-sequence draft-loop workloads", file=sys.stderr)
-        return 1
+    if wl.S_lo or wl.R_w:  # the batch and ring workloads: their own timed call
+        print(json.dumps(bench_batch(wl, dev, args) if wl.S_lo else bench_ring(wl, dev, args)), flush=True)
+        return 0
     extra = args.warmup * 3 + args.steps * 3 + 64
     loop = DraftLoop(wl, dev, extra_steps=extra)
     if args.calib_copy:
@@ -538,8 +642,9 @@ def main(argv=None):
             pr.copy_(loop.lens0)
         fused["full_us_per_step"] = round(timed(loop.step_full_fused, max(3, args.steps // 2), 1) * 1e6 / g, 2)
         log("fused append + attention steps: " + ", ".join(f"{k}={v}" for k, v in fused.items()))
-        if not args.no_sweep:
-            sweep = sweep_flatness(loop, [131072, 262144, 524288, 1048576])
+        lengths = [S for S in (131072, 262144, 524288, 1048576) if S <= wl.S]
+        if not args.no_sweep and len(lengths) > 1:
+            sweep = sweep_flatness(loop, lengths)
         caches = cache_figures(loop)
     extra = None if (args.only_full or args.no_extras) else extras(loop)
 
