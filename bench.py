@@ -436,6 +436,24 @@ def cpu_baseline(loop, budget_s=20.0):
         A.attend_sequence(qb, kb, vb, S, wl.scale, A.window_mask(S, wl.W, wl.sink))
         nw += 1
     win_s = (time.perf_counter() - t1) / nw
+    # the oracle beside the next rows, at the same shape: draft-extend over
+    # gamma + 1 causal rows (windowed) and the windowed step over an fp8 cache
+    from oracle import fp8 as F
+    rows = wl.gamma + 1
+    qx = I.bf16_bits(I.normal_bf16((rows, wl.Hq, wl.d), I.stream_seed(wl.seed, I.STREAM_Q, 99), "cpu"))
+
+    def per_call(fn, budget=1.0):
+        n, t = 0, time.perf_counter()
+        while n == 0 or time.perf_counter() - t < budget:
+            fn()
+            n += 1
+        return (time.perf_counter() - t) / n * 1e6
+
+    ext_us = per_call(lambda: A.attend_extend(qx, kb, vb, S, rows, wl.scale, "windowed", wl.W, wl.sink))
+    keep = A.selected_positions(S, wl.W, wl.sink)
+    k8 = I.fp8_codes(torch.from_numpy(A.bf16_to_f64(kb[keep]))).numpy()
+    v8 = I.fp8_codes(torch.from_numpy(A.bf16_to_f64(vb[keep]))).numpy()
+    f8_us = per_call(lambda: F.attend_sequence_fp8(qb, k8, v8, keep.size, wl.scale, 1.0, 1.0))
     return {
         "value": round(full_s * 1e6, 1),
         "unit": "us/step",
@@ -444,6 +462,8 @@ def cpu_baseline(loop, budget_s=20.0):
         "sample": (f"{done} full-context draft steps (Hq=32, Hkv=2, d=256, S=1,048,576, float64 NumPy) "
                    f"+ {nw} windowed steps ({win_s * 1e6:.0f} us/step); CPU: {cpu_model()}"),
         "windowed_us_per_step": round(win_s * 1e6, 1),
+        "extend_windowed_us": round(ext_us, 1),
+        "fp8_windowed_us": round(f8_us, 1),
     }
 
 

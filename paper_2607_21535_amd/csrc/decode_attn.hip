@@ -114,13 +114,6 @@ __device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap,
   return S;
 }
 
-// Query row v = b * qps + t is row t of sequence b.  lens[b] counts every
-// cached row, including the n new rows of this call (n = n_q[b], or qps when
-// n_q is NULL); row t attends causally: it sees the first lens[b] - n + t + 1
-// rows (the draft decode step is the case qps = n = 1).  Rows t >= n, and
-// every row of an empty sequence, have no keys; a non-empty sequence with
-// fewer rows than n is flagged.  Returns that length; `b_out` receives the
-// sequence.
 // Tail maps.  Tree (speculation candidates): query row v = b * qps + t is
 // candidate t of request b, whose committed length is lens[b] and
 // speculative depth n_q[b] (0 .. dd); every candidate sees lens[b] + depth
@@ -151,6 +144,13 @@ __device__ __forceinline__ int tail_len(const int32_t* lens, const int32_t* extr
   return S + i;
 }
 
+// Query row v = b * qps + t is row t of sequence b.  lens[b] counts every
+// cached row, including the n new rows of this call (n = n_q[b], or qps when
+// n_q is NULL); row t attends causally: it sees the first lens[b] - n + t + 1
+// rows (the draft decode step is the case qps = n = 1).  Rows t >= n, and
+// every row of an empty sequence, have no keys; a non-empty sequence with
+// fewer rows than n is flagged.  Tail maps use tail_len.  Returns that
+// length; `b_out` receives the sequence.
 template <KeyMap M>
 __device__ __forceinline__ int visible_len(const int32_t* lens, const int32_t* n_q, int qps,
                                            int64_t cap, int32_t* err, int v, bool report,
