@@ -427,6 +427,24 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 
   using Tile = TileRegs<D, F8>;
 
+  // bf16 keys (dense, ring, tree and step maps) reach the MFMA through LDS:
+  // the tile's K rows are loaded key-major and contiguous (16-byte units
+  // f = 64 i + lane), each wave stores them into its own padded LDS tile and
+  // reads the MFMA operand back (lane (grp, col): key col, unit 4 kk + grp).
+  // A load instruction then covers whole 256..512-byte runs of two to eight
+  // keys instead of 64-byte pieces of sixteen, which HBM serves about 10%
+  // faster.  The padding (one unit per key row) spreads both the stores and
+  // the operand reads of a 16-lane group over all LDS banks.  A wave's own
+  // stores and loads are processed in order: no barrier is needed.
+  constexpr bool kStageK = !F8 && !is_paged(M);
+  constexpr int kKUnits = D / 8;        // 16-byte units per key row (one KV head)
+  constexpr int kKPitch = kKUnits + 1;  // LDS row pitch in units
+  [[maybe_unused]] u32x4* s_k = nullptr;
+  if constexpr (kStageK) {
+    __shared__ u32x4 s_kbuf[kWaves * kTileKeys * kKPitch];
+    s_k = s_kbuf + wave * kTileKeys * kKPitch;
+  }
+
   const int n_tiles = (j1 - j0 + kTileKeys - 1) / kTileKeys;
 
   // Keys past j1 read a valid row (j0) and are masked out of the softmax.  A
@@ -435,7 +453,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // wait counts cover exactly the tile being computed.
   auto load_tile = [&](Tile& T, int t) {
     const int jt = j0 + min(t, n_tiles - 1) * kTileKeys;
-    {
+    if constexpr (kStageK) {
+#pragma unroll
+      for (int i = 0; i < KCH; ++i) {
+        const int f = i * kWave + lane;
+        const int j = jt + f / kKUnits;
+        const int r = row_of(j < j1 ? j : j0);
+        T.kx[i] = stream_load<u32x4>(key_row(r) + (f % kKUnits) * 8);
+      }
+    } else {
       const int j = jt + col;
       const int r = row_of(j < j1 ? j : j0);
       if constexpr (F8) {
@@ -503,6 +529,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fp8x8_to_bf16x8(w[2], w[3])),
                                                     qf[2 * kk + 1], s, 0, 0, 0);
       }
+    } else if constexpr (kStageK) {
+#pragma unroll
+      for (int i = 0; i < KCH; ++i) {
+        const int f = i * kWave + lane;
+        s_k[(f / kKUnits) * kKPitch + f % kKUnits] = T.kx[i];
+      }
+#pragma unroll
+      for (int kk = 0; kk < KCH; ++kk)
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, s_k[col * kKPitch + 4 * kk + grp]),
+                                                    qf[kk], s, 0, 0, 0);
     } else {
 #pragma unroll
       for (int kk = 0; kk < KCH; ++kk)
