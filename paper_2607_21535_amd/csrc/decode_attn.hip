@@ -272,10 +272,9 @@ __device__ __forceinline__ T stream_load(const E* p) {
 #endif
 }
 
-// Registers of one 16-key tile on one lane.  bf16: kx holds the key's d
-// chunk kk*32 + grp*8 (8 values) and vx the lane's VEC values of keys
-// 4*grp + i as words.  fp8: kx holds 16-byte pieces kk2*4 + grp of the key
-// (16 codes, two MFMA steps each) and vx the lane's VEC codes of each key.
+// Registers of one 16-key tile on one lane.  kx holds 16-byte units
+// 64 i + lane of the tile's K rows, key-major (8 bf16 values or 16 fp8 codes
+// each); vx holds the lane's VEC values (or codes) of keys 4*grp + i as words.
 template <int D, bool F8>
 struct TileRegs {
   u32x4 kx[D / 32];
@@ -427,23 +426,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 
   using Tile = TileRegs<D, F8>;
 
-  // bf16 keys (dense, ring, tree and step maps) reach the MFMA through LDS:
-  // the tile's K rows are loaded key-major and contiguous (16-byte units
-  // f = 64 i + lane), each wave stores them into its own padded LDS tile and
-  // reads the MFMA operand back (lane (grp, col): key col, unit 4 kk + grp).
-  // A load instruction then covers whole 256..512-byte runs of two to eight
-  // keys instead of 64-byte pieces of sixteen, which HBM serves about 10%
-  // faster.  The padding (one unit per key row) spreads both the stores and
-  // the operand reads of a 16-lane group over all LDS banks.  A wave's own
-  // stores and loads are processed in order: no barrier is needed.
-  constexpr bool kStageK = !F8 && !is_paged(M);
-  constexpr int kKUnits = D / 8;        // 16-byte units per key row (one KV head)
-  constexpr int kKPitch = kKUnits + 1;  // LDS row pitch in units
-  [[maybe_unused]] u32x4* s_k = nullptr;
-  if constexpr (kStageK) {
-    __shared__ u32x4 s_kbuf[kWaves * kTileKeys * kKPitch];
-    s_k = s_kbuf + wave * kTileKeys * kKPitch;
-  }
+  // Keys reach the MFMA through LDS: the tile's K rows are loaded key-major
+  // and contiguous (16-byte units f = 64 i + lane), each wave stores them into
+  // its own padded LDS tile and reads the operand back (lane (grp, col): key
+  // col, unit 4 kk + grp; an fp8 unit holds 16 codes, two MFMA steps).  A load
+  // instruction then covers whole 256..512-byte runs of two to eight keys
+  // instead of 64-byte pieces of sixteen, which HBM serves about 10% faster.
+  // The padding (one unit per key row) spreads both the stores and the
+  // operand reads of a 16-lane group over all LDS banks.  A wave's own stores
+  // and loads are processed in order: no barrier is needed.  The epilogue
+  // reuses the same LDS (after a barrier every wave has passed its last tile).
+  constexpr int kKUnits = F8 ? D / 16 : D / 8;  // 16-byte units per key row (one KV head)
+  constexpr int kKPitch = kKUnits + 1;          // LDS row pitch in units
+  constexpr int kKLoads = kTileKeys * kKUnits / kWave;  // load instructions per tile
+  constexpr int kStageBytes = kWaves * kTileKeys * kKPitch * 16;
+  constexpr int kComboBytes = (D / 4) * OPAD * 4;  // the epilogue's wave-combine buffer
+  __shared__ __align__(16) unsigned char s_lds[kStageBytes > kComboBytes ? kStageBytes : kComboBytes];
+  u32x4* s_k = reinterpret_cast<u32x4*>(s_lds) + wave * kTileKeys * kKPitch;
 
   const int n_tiles = (j1 - j0 + kTileKeys - 1) / kTileKeys;
 
@@ -453,26 +452,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // wait counts cover exactly the tile being computed.
   auto load_tile = [&](Tile& T, int t) {
     const int jt = j0 + min(t, n_tiles - 1) * kTileKeys;
-    if constexpr (kStageK) {
 #pragma unroll
-      for (int i = 0; i < KCH; ++i) {
-        const int f = i * kWave + lane;
-        const int j = jt + f / kKUnits;
-        const int r = row_of(j < j1 ? j : j0);
-        T.kx[i] = stream_load<u32x4>(key_row(r) + (f % kKUnits) * 8);
-      }
-    } else {
-      const int j = jt + col;
+    for (int i = 0; i < kKLoads; ++i) {
+      const int f = i * kWave + lane;
+      const int j = jt + f / kKUnits;
       const int r = row_of(j < j1 ? j : j0);
-      if constexpr (F8) {
-        const KT* p = key_row(r) + grp * 16;
-#pragma unroll
-        for (int kk = 0; kk < D / 64; ++kk) T.kx[kk] = stream_load<u32x4>(p + kk * 64);
-      } else {
-        const KT* p = key_row(r) + grp * 8;
-#pragma unroll
-        for (int kk = 0; kk < KCH; ++kk) T.kx[kk] = stream_load<u32x4>(p + kk * 32);
-      }
+      T.kx[i] = stream_load<u32x4>(key_row(r) + (f % kKUnits) * (16 / static_cast<int>(sizeof(KT))));
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -519,31 +504,26 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   auto compute_tile = [&](const Tile& T, int t) {
     const int jt = j0 + t * kTileKeys;
     floatx4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < kKLoads; ++i) {
+      const int f = i * kWave + lane;
+      s_k[(f / kKUnits) * kKPitch + f % kKUnits] = T.kx[i];
+    }
     if constexpr (F8) {
-      // 16 codes per piece: widened to bf16 (exact), two steps each.
+      // 16 codes per unit: widened to bf16 (exact), two steps each.
 #pragma unroll
       for (int kk = 0; kk < D / 64; ++kk) {
-        const u32x4 w = T.kx[kk];
+        const u32x4 w = s_k[col * kKPitch + 4 * kk + grp];
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fp8x8_to_bf16x8(w[0], w[1])),
                                                     qf[2 * kk], s, 0, 0, 0);
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fp8x8_to_bf16x8(w[2], w[3])),
                                                     qf[2 * kk + 1], s, 0, 0, 0);
       }
-    } else if constexpr (kStageK) {
-#pragma unroll
-      for (int i = 0; i < KCH; ++i) {
-        const int f = i * kWave + lane;
-        s_k[(f / kKUnits) * kKPitch + f % kKUnits] = T.kx[i];
-      }
+    } else {
 #pragma unroll
       for (int kk = 0; kk < KCH; ++kk)
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, s_k[col * kKPitch + 4 * kk + grp]),
                                                     qf[kk], s, 0, 0, 0);
-    } else {
-#pragma unroll
-      for (int kk = 0; kk < KCH; ++kk)
-        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, T.kx[kk]), qf[kk], s,
-                                                    0, 0, 0);
     }
     // s[i] = logit of key jt + 4*grp + i for head col
     float sv[4];
@@ -634,7 +614,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   __shared__ float s_m[kWaves][16];
   __shared__ float s_l[kWaves][16];
   __shared__ float s_z[kWaves][16];
-  __shared__ float s_o[(D / 4) * OPAD];
+  float* s_o = reinterpret_cast<float*>(s_lds);
   if (grp == 0) {
     s_m[wave][col] = m_run;
     s_l[wave][col] = l_run;
