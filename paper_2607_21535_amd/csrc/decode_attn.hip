@@ -286,6 +286,128 @@ struct TileRegs<D, true> {
   uint32_t vx[4][D / 64];
 };
 
+// Online softmax of one wave over 16-key tiles: 16 query heads (the lane's
+// column col), the running maximum m (exp2 domain), the sums l of the
+// bf16-rounded weights (normalises the output) and z of the fp32 weights
+// (the log-sum-exp), and the output O^T[d, heads] in VEC MFMA accumulators:
+// acc[e][jj] of lane (grp, col) holds head col at
+// d = (e / SEG) * 16 * SEG + SEG * (4 grp + jj) + e % SEG, where SEG is the
+// lane's run of contiguous value columns (min(VEC, 8) for bf16, VEC for fp8).
+template <int D, bool F8>
+struct OnlineHeads {
+  static constexpr int VEC = D / 16;
+  floatx4 acc[VEC];
+  float m, l, z;
+
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = floatx4{0.f, 0.f, 0.f, 0.f};
+    m = neg_inf();
+    l = 0.f;
+    z = 0.f;
+  }
+
+  // Takes the logits of NT consecutive 16-key tiles: s[u][i] is the raw
+  // logit of key jt + 16 u + 4 grp + i for head col (keys at or past j_end
+  // are masked out; kLateMask: only when the group reaches j_end, a branch
+  // that pays off where the computation, not the memory, bounds the kernel).
+  // Updates the running maximum, rescales the state when it grows and
+  // returns the weights as the P^T operands of the tiles.
+  template <int NT, bool kLateMask = false>
+  __device__ __forceinline__ void weigh(const floatx4 (&s)[NT], int jt, int j_end, float sl2, int grp,
+                                        bf16x4 (&pop)[NT]) {
+    float sv[NT][4];
+#pragma unroll
+    for (int u = 0; u < NT; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sv[u][i] = s[u][i] * sl2;
+    if (!kLateMask || jt + kTileKeys * NT > j_end) {  // wave-uniform
+#pragma unroll
+      for (int u = 0; u < NT; ++u)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (jt + kTileKeys * u + 4 * grp + i >= j_end) sv[u][i] = neg_inf();
+    }
+    float mt = neg_inf();
+#pragma unroll
+    for (int u = 0; u < NT; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mt = fmaxf(mt, sv[u][i]);
+    mt = fmaxf(mt, __shfl_xor(mt, 16));
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    const float m_new = fmaxf(m, mt);
+    if (__any(m_new > m)) {
+      const float alpha = __builtin_amdgcn_exp2f(m - m_new);
+      l *= alpha;
+      z *= alpha;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] *= alpha;
+    }
+    m = m_new;
+    // The weights of keys 4*grp + i for head col, rounded to bf16; the
+    // denominator sums the same rounded weights.
+#pragma unroll
+    for (int u = 0; u < NT; ++u) {
+      uint32_t pb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const float p0 = __builtin_amdgcn_exp2f(sv[u][2 * i] - m);
+        const float p1 = __builtin_amdgcn_exp2f(sv[u][2 * i + 1] - m);
+        pb[i] = pack_bf16x2(p0, p1);
+        l += bf16_lo(pb[i]) + bf16_hi(pb[i]);
+        z += p0 + p1;
+      }
+      pop[u] = __builtin_bit_cast(bf16x4, u32x2{pb[0], pb[1]});
+    }
+  }
+
+  // O^T += V^T . P^T for one tile: vx holds the lane's value words of keys
+  // 4 grp + i (bf16: VEC values, fp8: VEC codes, per key).
+  template <int NW>
+  __device__ __forceinline__ void accumulate(const bf16x4& pop, const uint32_t (&vx)[4][NW]) {
+    if constexpr (F8) {
+      // V^T operand for output tiles 4w .. 4w+3: interleave the codes of keys
+      // (0, 1) and (2, 3) byte by byte, then widen pairs to bf16.
+#pragma unroll
+      for (int w = 0; w < VEC / 4; ++w) {
+        const uint32_t p01 = __builtin_amdgcn_perm(vx[1][w], vx[0][w], 0x05010400u);
+        const uint32_t q01 = __builtin_amdgcn_perm(vx[1][w], vx[0][w], 0x07030602u);
+        const uint32_t p23 = __builtin_amdgcn_perm(vx[3][w], vx[2][w], 0x05010400u);
+        const uint32_t q23 = __builtin_amdgcn_perm(vx[3][w], vx[2][w], 0x07030602u);
+        const uint32_t lo01[4] = {fp8x2_to_bf16x2<false>(p01), fp8x2_to_bf16x2<true>(p01),
+                                  fp8x2_to_bf16x2<false>(q01), fp8x2_to_bf16x2<true>(q01)};
+        const uint32_t lo23[4] = {fp8x2_to_bf16x2<false>(p23), fp8x2_to_bf16x2<true>(p23),
+                                  fp8x2_to_bf16x2<false>(q23), fp8x2_to_bf16x2<true>(q23)};
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+          acc[4 * w + x] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+              __builtin_bit_cast(bf16x4, u32x2{lo01[x], lo23[x]}), pop, acc[4 * w + x], 0, 0, 0);
+      }
+    } else {
+      // V^T operand for output tile e: this lane's four keys at its value
+      // column e, packed from the loaded rows (low or high halves of a word).
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+        const uint32_t a01 = __builtin_amdgcn_perm(vx[1][e >> 1], vx[0][e >> 1], sel);
+        const uint32_t a23 = __builtin_amdgcn_perm(vx[3][e >> 1], vx[2][e >> 1], sel);
+        acc[e] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, u32x2{a01, a23}),
+                                                          pop, acc[e], 0, 0, 0);
+      }
+    }
+  }
+
+  // One tile: logits s (key jt + 4 grp + i), value words vx.
+  template <int NW>
+  __device__ __forceinline__ void add(const floatx4& s, const uint32_t (&vx)[4][NW], int jt, int j_end,
+                                      float sl2, int grp) {
+    const floatx4 s1[1] = {s};
+    bf16x4 pop[1];
+    weigh(s1, jt, j_end, sl2, grp, pop);
+    accumulate(pop[0], vx);
+  }
+};
+
 // Two waves per SIMD at d = 256 (the kernel fits 256 registers per lane):
 // two workgroups share a CU, so one waits on memory while the other computes.
 template <int D, KeyMap M, bool F8>
@@ -432,12 +554,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // col, unit 4 kk + grp; an fp8 unit holds 16 codes, two MFMA steps).  A load
   // instruction then covers whole 256..512-byte runs of two to eight keys
   // instead of 64-byte pieces of sixteen, which HBM serves about 10% faster.
-  // The padding (one unit per key row) spreads both the stores and the
-  // operand reads of a 16-lane group over all LDS banks.  A wave's own stores
+  // The row pitch (two units of padding) makes the operand reads free of
+  // bank conflicts (gfx950 LDS serves them at its full 256 bytes per clock;
+  // one unit of padding halves that).  A wave's own stores
   // and loads are processed in order: no barrier is needed.  The epilogue
   // reuses the same LDS (after a barrier every wave has passed its last tile).
   constexpr int kKUnits = F8 ? D / 16 : D / 8;  // 16-byte units per key row (one KV head)
-  constexpr int kKPitch = kKUnits + 1;          // LDS row pitch in units
+  constexpr int kKPitch = kKUnits + 2;          // LDS row pitch in units
   constexpr int kKLoads = kTileKeys * kKUnits / kWave;  // load instructions per tile
   constexpr int kStageBytes = kWaves * kTileKeys * kKPitch * 16;
   constexpr int kComboBytes = (D / 4) * OPAD * 4;  // the epilogue's wave-combine buffer
@@ -493,12 +616,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
   };
 
-  floatx4 acc[VEC];
-#pragma unroll
-  for (int e = 0; e < VEC; ++e) acc[e] = floatx4{0.f, 0.f, 0.f, 0.f};
-  float m_run = neg_inf();
-  float l_run = 0.f;  // sum of the bf16-rounded weights (normalises the output)
-  float z_run = 0.f;  // sum of the fp32 weights (the log-sum-exp)
+  OnlineHeads<D, F8> st;
+  st.init();
   const float sl2 = a.scale_log2;
 
   auto compute_tile = [&](const Tile& T, int t) {
@@ -525,68 +644,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, s_k[col * kKPitch + 4 * kk + grp]),
                                                     qf[kk], s, 0, 0, 0);
     }
-    // s[i] = logit of key jt + 4*grp + i for head col
-    float sv[4];
-    float mt = neg_inf();
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int j = jt + 4 * grp + i;
-      sv[i] = j < j1 ? s[i] * sl2 : neg_inf();
-      mt = fmaxf(mt, sv[i]);
-    }
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    if (__any(m_new > m_run)) {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-      z_run *= alpha;
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) acc[e] *= alpha;
-    }
-    m_run = m_new;
-    // P^T operand: the weights of keys 4*grp + i for head col, rounded to
-    // bf16; the denominator sums the same rounded weights.
-    uint32_t pb[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const float p0 = __builtin_amdgcn_exp2f(sv[2 * i] - m_run);
-      const float p1 = __builtin_amdgcn_exp2f(sv[2 * i + 1] - m_run);
-      pb[i] = uint32_t(f32_to_bf16_rne(p0)) | (uint32_t(f32_to_bf16_rne(p1)) << 16);
-      l_run += bf16_lo(pb[i]) + bf16_hi(pb[i]);
-      z_run += p0 + p1;
-    }
-    const bf16x4 pop = __builtin_bit_cast(bf16x4, u32x2{pb[0], pb[1]});
-    if constexpr (F8) {
-      // V^T operand for output tiles 4w .. 4w+3: interleave the codes of keys
-      // (0, 1) and (2, 3) byte by byte, then widen pairs to bf16.
-#pragma unroll
-      for (int w = 0; w < VEC / 4; ++w) {
-        const uint32_t p01 = __builtin_amdgcn_perm(T.vx[1][w], T.vx[0][w], 0x05010400u);
-        const uint32_t q01 = __builtin_amdgcn_perm(T.vx[1][w], T.vx[0][w], 0x07030602u);
-        const uint32_t p23 = __builtin_amdgcn_perm(T.vx[3][w], T.vx[2][w], 0x05010400u);
-        const uint32_t q23 = __builtin_amdgcn_perm(T.vx[3][w], T.vx[2][w], 0x07030602u);
-        const uint32_t lo01[4] = {fp8x2_to_bf16x2<false>(p01), fp8x2_to_bf16x2<true>(p01),
-                                  fp8x2_to_bf16x2<false>(q01), fp8x2_to_bf16x2<true>(q01)};
-        const uint32_t lo23[4] = {fp8x2_to_bf16x2<false>(p23), fp8x2_to_bf16x2<true>(p23),
-                                  fp8x2_to_bf16x2<false>(q23), fp8x2_to_bf16x2<true>(q23)};
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-          acc[4 * w + x] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-              __builtin_bit_cast(bf16x4, u32x2{lo01[x], lo23[x]}), pop, acc[4 * w + x], 0, 0, 0);
-      }
-    } else {
-      // V^T operand for output tile e: this lane's four keys at its value
-      // column e, packed from the loaded rows (low or high halves of a word).
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-        const uint32_t a01 = __builtin_amdgcn_perm(T.vx[1][e >> 1], T.vx[0][e >> 1], sel);
-        const uint32_t a23 = __builtin_amdgcn_perm(T.vx[3][e >> 1], T.vx[2][e >> 1], sel);
-        acc[e] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, u32x2{a01, a23}),
-                                                          pop, acc[e], 0, 0, 0);
-      }
-    }
+    st.add(s, T.vx, jt, j1, sl2, grp);
   };
 
   // Two register buffers: the loads of this wave's next tile are in flight
@@ -607,6 +665,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   if (i < my_tiles) compute_tile(T0, wave + i * kWaves);
 
   // ---- combine the four waves: (m, l) per head, then O in wave order ----
+  float l_run = st.l, z_run = st.z;
+  const float m_run = st.m;
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
   z_run += __shfl_xor(z_run, 16);
@@ -638,7 +698,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
           const int idx = (e * 4 + jj) * OPAD + lane;
-          const float val = acc[e][jj] * f;
+          const float val = st.acc[e][jj] * f;
           s_o[idx] = (w == 0) ? val : s_o[idx] + val;
         }
       }
@@ -666,6 +726,271 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     const int gq = r / 4;
     const int jj = r % 4;
     po[idx] = s_o[(e * 4 + jj) * OPAD + gq * 16 + h];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Full-context attention of several new query rows per sequence (the causal
+// draft-extend, row t of sequence b seeing the first lens[b] - n + t + 1
+// rows).  The rows of one sequence read almost the same keys, so a work item
+// is a key chunk of a sequence rather than of a row: its workgroup streams the
+// chunk once through LDS and each of its eight waves attends one query row
+// over it (further rows take further passes).  The chunk size and the
+// numbering of each row's partials are those of the per-row decomposition
+// (wave_chunk, locate_item): a row's items are the chunks it sees, and the
+// same merge kernel combines them.
+
+constexpr int kRowWaves = 8;                      // query rows per pass, one per wave
+constexpr int kRowThreads = kRowWaves * kWave;
+constexpr int kRowStep = kChunkQuantum;           // keys per LDS step: four 16-key tiles
+#ifndef WMTP_ROW_GROUP
+#define WMTP_ROW_GROUP 4
+#endif
+constexpr int kRowGroup = WMTP_ROW_GROUP;         // tiles per softmax update
+
+// Finds sequence b and chunk c of multi-row work item `item`: sequence b owns
+// as many items as its last row has chunks.  Also returns b's row count n and
+// the number of partials numbered before b's last row.  Returns false for the
+// whole workgroup when `item` lies past the last sequence's items.
+__device__ bool locate_rows_item(const SplitArgs& a, int item, int& b_out, int& c_out, int& n_out,
+                                 int& before_last_out, int& chunk_out) {
+  constexpr KeyMap M = KeyMap::Full;
+  __shared__ int s_b, s_c, s_n, s_before, s_chunk;
+  const int NV = a.B * a.qps;
+  if (threadIdx.x < kWave) {
+    const int lane = threadIdx.x;
+    const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, NV, a.len_cap, a.W, a.sink, a.target,
+                                    a.chunk_cap, a.err, true, a.dd);
+    if (lane == 0) {
+      s_b = -1;
+      s_chunk = chunk;
+    }
+    int carry_items = 0, carry_parts = 0;
+    for (int base = 0; base < NV; base += kWave) {
+      const int v = base + lane;
+      int cnt = 0, own = 0, b = 0, n = 0;
+      if (v < NV) {
+        const int S = visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, false, b, a.dd);
+        cnt = ceil_div_i(S, chunk);
+        n = a.n_q == nullptr ? a.qps : min(max(a.n_q[b], 0), a.qps);
+        own = v - b * a.qps == n - 1 ? cnt : 0;  // the last row: the sequence's items
+      }
+      int incl_own = own, incl_cnt = cnt;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int x = __shfl_up(incl_own, off);
+        const int y = __shfl_up(incl_cnt, off);
+        if (lane >= off) {
+          incl_own += x;
+          incl_cnt += y;
+        }
+      }
+      const int lo = carry_items + incl_own - own;
+      if (own > 0 && item >= lo && item < lo + own) {
+        s_b = b;
+        s_c = item - lo;
+        s_n = n;
+        s_before = carry_parts + incl_cnt - cnt;
+      }
+      carry_items += __shfl(incl_own, kWave - 1);
+      carry_parts += __shfl(incl_cnt, kWave - 1);
+      if (carry_items > item) break;
+    }
+  }
+  __syncthreads();
+  b_out = s_b;
+  c_out = s_c;
+  n_out = s_n;
+  before_last_out = s_before;
+  chunk_out = s_chunk;
+  return b_out >= 0;
+}
+
+template <int D>
+__global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
+  constexpr KeyMap M = KeyMap::Full;
+  constexpr int VEC = D / 16;
+  constexpr int SEG = VEC < 8 ? VEC : 8;  // as in split_kernel
+  constexpr int NSEG = VEC / SEG;
+  constexpr int KCH = D / 32;
+  constexpr int kUnits = D / 8;  // 16-byte units per row of one KV head
+  // LDS row pitches (units) that keep the operand reads free of bank
+  // conflicts on gfx950: the K operand (16 lanes read one unit of 16 rows)
+  // needs two units of padding; the V operand (16 lanes read 16 consecutive
+  // units of one row) needs none, except at d = 64 (8-byte reads), two.
+  constexpr int kPitch = kUnits + 2;
+  constexpr int kVPitch = D == 64 ? kUnits + 2 : kUnits;
+  constexpr int kLoads = kRowStep * kUnits / kRowThreads;  // K (and V) units per thread and step
+  static_assert(kLoads >= 1 && kRowStep * kUnits % kRowThreads == 0, "step must tile the workgroup");
+  // Two buffers of one step's K and V rows: a step is computed from one while
+  // the next step's rows, loaded during that computation, go to the other.
+  __shared__ u32x4 s_k[2][kRowStep * kPitch];
+  __shared__ u32x4 s_v[2][kRowStep * kVPitch];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int grp = lane >> 4;
+  const int col = lane & 15;
+  const int g = blockIdx.x % a.Hkv;
+  const int item = blockIdx.x / a.Hkv;
+
+  int b, c, n, before_last, chunk;
+  if (!locate_rows_item(a, item, b, c, n, before_last, chunk)) return;
+  b = __builtin_amdgcn_readfirstlane(b);
+  c = __builtin_amdgcn_readfirstlane(c);
+  n = __builtin_amdgcn_readfirstlane(n);
+  before_last = __builtin_amdgcn_readfirstlane(before_last);
+  chunk = __builtin_amdgcn_readfirstlane(chunk);
+  auto row_len = [&](int t) {
+    int bb;
+    return visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, b * a.qps + t, false, bb, a.dd);
+  };
+  const int S = __builtin_amdgcn_readfirstlane(row_len(n - 1));  // the last row sees every key
+  const int j0 = c * chunk;
+  const int j1 = min(j0 + chunk, S);
+  const int n_steps = ceil_div_i(j1 - j0, kRowStep);
+
+  const int64_t rs = static_cast<int64_t>(a.Hkv) * D;
+  const int64_t seq_off = (static_cast<int64_t>(b) * a.rows * a.Hkv + g) * D;
+  const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + seq_off;
+  const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + seq_off;
+
+  // Unit f = i * kRowThreads + tid of a step is unit f % kUnits of key
+  // f / kUnits: a load instruction covers whole rows.  Keys past j1 read row
+  // j0 (masked out of every row's softmax).
+  u32x4 rk[kLoads], rv[kLoads];
+  auto load = [&](int s) {
+    const int js = j0 + s * kRowStep;
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int f = i * kRowThreads + tid;
+      const int j = js + f / kUnits;
+      const int64_t off = static_cast<int64_t>(j < j1 ? j : j0) * rs + (f % kUnits) * 8;
+      rk[i] = stream_load<u32x4>(kbase + off);
+      rv[i] = stream_load<u32x4>(vbase + off);
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int f = i * kRowThreads + tid;
+      s_k[buf][(f / kUnits) * kPitch + f % kUnits] = rk[i];
+      s_v[buf][(f / kUnits) * kVPitch + f % kUnits] = rv[i];
+    }
+  };
+  const float sl2 = a.scale_log2;
+
+  for (int t0 = 0; t0 < n; t0 += kRowWaves) {
+    const int t = t0 + wave;
+    const int L = t < n ? row_len(t) : 0;
+    const bool active = L > j0;  // the row sees keys of this chunk
+    if (!__syncthreads_or(active)) continue;
+    const int j_end = min(j1, L);
+
+    // Q^T operand of row t, laid out as in split_kernel.
+    bf16x8 qf[KCH];
+    {
+      const bool live = active && col < a.G;
+      const uint16_t* qp =
+          a.q + ((static_cast<int64_t>(b) * a.qps + (active ? t : 0)) * a.Hq + g * a.G + (col < a.G ? col : 0)) * D;
+#pragma unroll
+      for (int kk = 0; kk < KCH; ++kk) {
+        u32x4 w = live ? *reinterpret_cast<const u32x4*>(qp + kk * 32 + grp * 8) : u32x4{0u, 0u, 0u, 0u};
+        qf[kk] = __builtin_bit_cast(bf16x8, w);
+      }
+    }
+
+    OnlineHeads<D, false> st;
+    st.init();
+    load(0);
+    stash(0);
+    __syncthreads();
+    for (int s = 0; s < n_steps; ++s) {
+      const int buf = s & 1;
+      if (s + 1 < n_steps) load(s + 1);
+      if (active) {
+        const u32x4* sk = s_k[buf];
+        const uint16_t* sv = reinterpret_cast<const uint16_t*>(s_v[buf]);
+        constexpr int NT = kRowGroup;
+#pragma unroll
+        for (int u0 = 0; u0 < kRowStep / kTileKeys; u0 += NT) {
+          const int js = j0 + s * kRowStep + u0 * kTileKeys;
+          if (js >= j_end) break;  // past this row's last key (wave-uniform)
+          // Logits of NT tiles: independent MFMA chains.
+          floatx4 sc[NT];
+#pragma unroll
+          for (int u = 0; u < NT; ++u) sc[u] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int kk = 0; kk < KCH; ++kk)
+#pragma unroll
+            for (int u = 0; u < NT; ++u)
+              sc[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8, sk[((u0 + u) * kTileKeys + col) * kPitch + 4 * kk + grp]), qf[kk],
+                  sc[u], 0, 0, 0);
+          bf16x4 pop[NT];
+          st.template weigh<NT, true>(sc, js, j_end, sl2, grp, pop);
+#pragma unroll
+          for (int u = 0; u < NT; ++u) {
+            // V words of keys 4 grp + i of the tile at this lane's value
+            // columns (as split_kernel loads them).
+            uint32_t vx[4][VEC / 2];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const uint16_t* p = sv + ((u0 + u) * kTileKeys + 4 * grp + i) * kVPitch * 8 + SEG * col;
+#pragma unroll
+              for (int sg = 0; sg < NSEG; ++sg) {
+                if constexpr (SEG == 8) {
+                  const u32x4 x = *reinterpret_cast<const u32x4*>(p + sg * 16 * SEG);
+#pragma unroll
+                  for (int w = 0; w < 4; ++w) vx[i][sg * 4 + w] = x[w];
+                } else {
+                  const u32x2 x = *reinterpret_cast<const u32x2*>(p + sg * 16 * SEG);
+                  vx[i][sg * 2] = x[0];
+                  vx[i][sg * 2 + 1] = x[1];
+                }
+              }
+            }
+            st.accumulate(pop[u], vx);
+          }
+        }
+      }
+      if (s + 1 < n_steps) stash(buf ^ 1);
+      __syncthreads();
+    }
+
+    if (active) {
+      // This row's partial: its items are numbered after those of every
+      // earlier row; rows t .. n-2 precede the last one.
+      int later = 0;
+      for (int t2 = t + lane; t2 < n - 1; t2 += kWave) later += ceil_div_i(row_len(t2), chunk);
+#pragma unroll
+      for (int off = kWave / 2; off > 0; off >>= 1) later += __shfl_xor(later, off);
+      float l = st.l, z = st.z;
+      l += __shfl_xor(l, 16);
+      l += __shfl_xor(l, 32);
+      z += __shfl_xor(z, 16);
+      z += __shfl_xor(z, 32);
+      const int64_t pidx = static_cast<int64_t>(before_last - later + c) * a.Hkv + g;
+      if (col < a.G) {
+        if (grp == 0) {
+          a.pm[pidx * a.G + col] = st.m;
+          a.pl[pidx * a.G + col] = l;
+          a.pz[pidx * a.G + col] = z;
+        }
+        float* po = a.po + (pidx * a.G + col) * D;
+#pragma unroll
+        for (int sg = 0; sg < NSEG; ++sg)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+            for (int w = 0; w < SEG / 4; ++w) {
+              const int e = sg * SEG + 4 * w;
+              *reinterpret_cast<floatx4*>(po + sg * 16 * SEG + SEG * (4 * grp + jj) + 4 * w) =
+                  floatx4{st.acc[e][jj], st.acc[e + 1][jj], st.acc[e + 2][jj], st.acc[e + 3][jj]};
+            }
+      }
+    }
   }
 }
 
@@ -776,8 +1101,8 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
     float r[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) r[i] = n > 0 ? ot[i] / Lt * a.out_scale : 0.f;
-    const uint32_t lo = f32_to_bf16_rne(r[0]) | (uint32_t(f32_to_bf16_rne(r[1])) << 16);
-    const uint32_t hi = f32_to_bf16_rne(r[2]) | (uint32_t(f32_to_bf16_rne(r[3])) << 16);
+    const uint32_t lo = pack_bf16x2(r[0], r[1]);
+    const uint32_t hi = pack_bf16x2(r[2], r[3]);
     *reinterpret_cast<u32x2*>(a.out + (static_cast<int64_t>(v) * a.Hq + h) * D + d0) = u32x2{lo, hi};
     if (a.lse != nullptr && blockIdx.y == 0 && q4 == 0)
       a.lse[static_cast<int64_t>(v) * a.Hq + h] = n > 0 ? (Mx + log2f(s_Z[0])) * kLn2 : neg_inf();
@@ -798,8 +1123,26 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
     a.target = L.target; a.chunk_cap = L.chunk_cap;
     a.scale_log2 = L.scale * L.k_scale * kLog2e;
     a.k2 = L.k2; a.v2 = L.v2; a.rows2 = L.rows2; a.dd = L.dd;
-    const dim3 grid(static_cast<unsigned>(L.max_items) * static_cast<unsigned>(L.Hkv));
-    hipLaunchKernelGGL((split_kernel<D, M, F8>), grid, dim3(kThreads), 0, st, a);
+    if constexpr (M == KeyMap::Full && !F8) {
+      if (L.qps > 1) {
+        // Items of the multi-row kernel: sequence b owns ceil(n(b) / chunk)
+        // of them, n(b) its last row's length; with the chunk of the per-row
+        // decomposition (total over rows / T, clamped to [quantum, cap]) that
+        // is at most min(B ceil(n/quantum), max(T + B, B ceil(n/cap))).
+        const int64_t n = L.len_cap;
+        const int64_t fine = static_cast<int64_t>(L.B) * ((n + kChunkQuantum - 1) / kChunkQuantum);
+        const int64_t coarse = static_cast<int64_t>(L.B) * ((n + L.chunk_cap - 1) / L.chunk_cap);
+        const int64_t items = std::min(fine, std::max<int64_t>(static_cast<int64_t>(L.target) + L.B, coarse));
+        const dim3 grid(static_cast<unsigned>(std::min<int64_t>(items, L.max_items)) * static_cast<unsigned>(L.Hkv));
+        hipLaunchKernelGGL((rows_split_kernel<D>), grid, dim3(kRowThreads), 0, st, a);
+      } else {
+        hipLaunchKernelGGL((split_kernel<D, M, F8>), dim3(static_cast<unsigned>(L.max_items) * L.Hkv),
+                           dim3(kThreads), 0, st, a);
+      }
+    } else {
+      const dim3 grid(static_cast<unsigned>(L.max_items) * static_cast<unsigned>(L.Hkv));
+      hipLaunchKernelGGL((split_kernel<D, M, F8>), grid, dim3(kThreads), 0, st, a);
+    }
   }
   // Items per sequence the plan allows decide the merge shape.
   const int64_t NV = static_cast<int64_t>(L.B) * L.qps;

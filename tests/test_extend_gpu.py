@@ -84,6 +84,29 @@ def test_extend_vs_oracle(dev, d, Hq, Hkv, q_max):
     assert torch.equal(orr, ow)
 
 
+@pytest.mark.parametrize("d,Hq,Hkv", [(128, 12, 2), (256, 32, 2)])
+@pytest.mark.parametrize("q_max", [12, 20])
+def test_full_extend_many_rows(dev, d, Hq, Hkv, q_max):
+    """More new rows than one pass of the multi-row kernel takes (eight), ragged
+    row counts, and rows whose lengths straddle item boundaries."""
+    lens = [q_max + 1, 130, 4099, 20000, 64 * 37 + 5]
+    n_q = [q_max, q_max, 9, q_max - 3, 7]
+    B = len(lens)
+    S_max = max(lens) + 1
+    G.say(f"extend many rows d={d} Hq={Hq} Hkv={Hkv} q_max={q_max} lens={lens} n_q={n_q}")
+    q = I.normal_bf16((B, q_max, Hq, d), 61, dev)
+    k = I.normal_bf16((B, S_max, Hkv, d), 62, dev)
+    v = I.normal_bf16((B, S_max, Hkv, d), 63, dev)
+    lt, nt = G.lens_tensor(lens, dev), G.lens_tensor(n_q, dev)
+    lse = torch.empty(B, q_max, Hq, dtype=torch.float32, device=dev)
+    err = G.err_word(dev)
+    out = W.draft_extend_full(q, k, v, lt, n_q=nt, lse=lse, err=err)
+    torch.cuda.synchronize()
+    o_ref, l_ref = _oracle(q, k, v, lens, n_q, 1.0 / np.sqrt(d), "full")
+    G.assert_attn_close(out, o_ref, lse, l_ref, what="extend many rows", strict=False)
+    assert err.item() == 0
+
+
 def test_one_row_extend_is_the_decode_step(dev):
     Hq, Hkv, d = 32, 2, 256
     lens = [5000, 70000, 1, 3000]
@@ -133,7 +156,7 @@ def test_extend_s1m_draft_depth8(dev):
     o_ref, l_ref = _oracle(q, k, v, [S], [q_max], wl.scale, "windowed", wl.W, wl.sink)
     G.say(f"extend 1M windowed err {G.assert_attn_close(ow, o_ref, lse_w, l_ref, 'extend 1M windowed')}")
     qb = I.bf16_bits(q)
-    for t in (0, q_max - 1):
+    for t in (0, 3, q_max - 1):
         L = S - q_max + t + 1
         o1, l1 = A.attend_sequence(qb[0, t], G.HostRows(k[0]), G.HostRows(v[0]), L, wl.scale, None)
         e = G.assert_attn_close(of[0, t], o1, lse_f[0, t], l1, f"extend 1M full row {t}")
