@@ -3,13 +3,15 @@
 Workload: the million-token draft loop -- B=1, Hq=32, Hkv=2, d=256, a
 1,048,576-token bf16 draft KV cache (2 GiB, first 4 key rows scaled x4),
 gamma=7 draft steps per decode iteration, each appending the draft token's
-K/V row to the cache and then attending.  One benchmark step is one decode
-iteration's draft phase: 7 x (append + attention).
+K/V row to the cache and then attending.  The reported step is one draft
+step (append + attention), timed over --steps decode iterations run back to
+back (7 draft steps each).
 
-Timed variants (each its own timed region of --steps steps):
+Timed variants (each its own timed region of --steps iterations):
   full      full-context attention (the native draft; O(S) read per step),
-            run eagerly with a HIP event pair around every attention call;
-            its achieved HBM bandwidth is the roofline figure;
+            eager, wall clock; then once more with a HIP event pair around
+            every attention call, whose mean gives the achieved HBM
+            bandwidth of the roofline figure;
   windowed  sink(4) + window(2048) attention over the same dense cache;
   ring      the same over the compact ring store (4 + 2048 slots),
 the windowed and ring loops are captured once in a HIP graph and replayed.
@@ -201,15 +203,14 @@ def graph_of(fn):
 
 
 def attention_call_times(loop, steps, warmup):
-    """Full variant, eager: wall time per step and HIP-event time of every
-    attention call (split + merge kernels) in the timed region."""
+    """Full variant, eager: HIP-event time (ms) of every attention call
+    (split + merge kernels) over `steps` draft-loop iterations."""
     for _ in range(warmup):
         loop.step_full()
     torch.cuda.synchronize()
     g = loop.wl.gamma
     pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
              for _ in range(steps * g)]
-    t0 = time.perf_counter()
     it = iter(pairs)
     for _ in range(steps):
         wl = loop.wl
@@ -221,9 +222,7 @@ def attention_call_times(loop, steps, warmup):
                               scale=wl.scale)
             b.record()
     torch.cuda.synchronize()
-    wall = (time.perf_counter() - t0) / steps
-    ms = np.array([a.elapsed_time(b) for a, b in pairs])
-    return wall, ms
+    return np.array([a.elapsed_time(b) for a, b in pairs])
 
 
 def sweep_flatness(loop, lengths, reps=20):
@@ -327,13 +326,29 @@ def cache_figures(loop):
     return res
 
 
-def extras(loop):
+def read_ceiling_gbps(loop, reps=7):
+    """The device's practical HBM read ceiling: the library's streaming-read
+    probe over the bf16 cache (K, then V; 2 x 1 GiB), HIP-event timed."""
+    bufs = [loop.k, loop.v]
+    nbytes = sum(b.numel() * b.element_size() for b in bufs)
+    sink = torch.empty(W.PROBE_BLOCKS, dtype=torch.int32, device=loop.dev)
+    us = event_us(lambda: [W.hbm_read_probe(b, sink) for b in bufs], reps=reps, warm=2)
+    return nbytes / (us * 1e-6) / 1e9
+
+
+def extras(loop, fp8=True):
     """Context measurements at the 1M shape: draft-extend over gamma+1 new
-    rows, and the paged pool (page size 1): the draft's KV-index build
-    (native O(S) vs windowed O(sink+W)) and attention through req_to_token
-    over a pool whose rows are scattered at random."""
+    rows, the paged pool (page size 1) and, optionally, the fp8 cache."""
+    out = {"extend": extend_figures(loop), "paged": paged_figures(loop)}
+    if fp8:
+        out["fp8"] = fp8_figures(loop)
+    return out
+
+
+def extend_figures(loop):
+    """Draft-extend over gamma+1 causal new rows: windowed (graph replay) and
+    full context (one read of the context for all rows)."""
     wl, dev = loop.wl, loop.dev
-    S = wl.S
     loop.lens.copy_(loop.lens0)
     rows = wl.gamma + 1
     qx = I.normal_bf16((1, rows, wl.Hq, wl.d), I.stream_seed(wl.seed, I.STREAM_Q, 99), dev)
@@ -345,7 +360,18 @@ def extras(loop):
         "full_us": round(event_us(lambda: W.draft_extend_full(qx, loop.k, loop.v, loop.lens, n_q=nq,
                                                               scale=wl.scale), reps=5, warm=2), 1),
     }
+    ext["full_hbm_gbps"] = round(wl.S * wl.Hkv * wl.d * 4 / ext["full_us"] / 1e3, 1)
     log(f"extend ({rows} rows): windowed {ext['windowed_us']} us, full {ext['full_us']} us")
+    return ext
+
+
+def paged_figures(loop):
+    """The paged pool (page size 1): the draft's KV-index build (native O(S)
+    vs windowed O(sink+W)) and attention through req_to_token over a pool
+    whose rows are scattered at random."""
+    wl, dev = loop.wl, loop.dev
+    S = wl.S
+    loop.lens.copy_(loop.lens0)
     C = loop.S_max
     g = torch.Generator(device="cpu").manual_seed(wl.seed)
     table = torch.randperm(C, generator=g).to(torch.int32).view(1, C).to(dev)
@@ -374,7 +400,7 @@ def extras(loop):
         f"windowed {paged['windowed_us']} us")
     del kp, vp
     torch.cuda.empty_cache()
-    return {"extend": ext, "paged": paged, "fp8": fp8_figures(loop)}
+    return paged
 
 
 def fp8_figures(loop):
@@ -436,6 +462,16 @@ def cpu_baseline(loop, budget_s=20.0):
         A.attend_sequence(qb, kb, vb, S, wl.scale, A.window_mask(S, wl.W, wl.sink))
         nw += 1
     win_s = (time.perf_counter() - t1) / nw
+    try:  # the same windowed step on one thread
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(1):
+            t2, nw1 = time.perf_counter(), 0
+            while time.perf_counter() - t2 < 1.0:
+                A.attend_sequence(qb, kb, vb, S, wl.scale, A.window_mask(S, wl.W, wl.sink))
+                nw1 += 1
+            win1_us = round((time.perf_counter() - t2) / nw1 * 1e6, 1)
+    except ImportError:  # pragma: no cover
+        win1_us = None
     # the oracle beside the next rows, at the same shape: draft-extend over
     # gamma + 1 causal rows (windowed) and the windowed step over an fp8 cache
     from oracle import fp8 as F
@@ -462,6 +498,7 @@ def cpu_baseline(loop, budget_s=20.0):
         "sample": (f"{done} full-context draft steps (Hq=32, Hkv=2, d=256, S=1,048,576, float64 NumPy) "
                    f"+ {nw} windowed steps ({win_s * 1e6:.0f} us/step); CPU: {cpu_model()}"),
         "windowed_us_per_step": round(win_s * 1e6, 1),
+        "windowed_us_per_step_1_thread": win1_us,
         "extend_windowed_us": round(ext_us, 1),
         "fp8_windowed_us": round(f8_us, 1),
     }
@@ -599,6 +636,8 @@ def main(argv=None):
     ap.add_argument("--no-extras", action="store_true", help="skip the extend / paged context figures")
     ap.add_argument("--only-full", action="store_true", help="time only the full-context loop (profiling)")
     ap.add_argument("--only-fp8", action="store_true", help="time only the fp8-cache calls (profiling)")
+    ap.add_argument("--only-extras", action="store_true",
+                    help="time only the extend and paged figures (profiling)")
     ap.add_argument("--calib-copy", action="store_true", help="also run a 1 GiB device copy (counter calibration)")
     args = ap.parse_args(argv)
 
@@ -625,10 +664,20 @@ def main(argv=None):
     if args.only_fp8:
         print(json.dumps({"fp8": fp8_figures(loop)}), flush=True)
         return 0
-    log("timing full (eager, events per attention call)")
-    wall_full, call_ms = attention_call_times(loop, args.steps, args.warmup)
+    if args.only_extras:
+        print(json.dumps(extras(loop, fp8=False)), flush=True)
+        return 0
+    log("timing full (eager): wall clock per draft step, then HIP events per attention call")
+    loop.lens.copy_(loop.lens0)
+    wall_full = timed(loop.step_full, args.steps, args.warmup)
     us_full_step = wall_full * 1e6 / g
+    loop.lens.copy_(loop.lens0)
+    call_ms = attention_call_times(loop, args.steps, 1)
     call_us = float(call_ms.mean() * 1e3)
+    # the fused form of the same step, timed in the same state of the GPU
+    for pr in loop.lp:
+        pr.copy_(loop.lens0)
+    fused_full_us = timed(loop.step_full_fused, args.steps, args.warmup) * 1e6 / g
     kv_bytes = wl.B * wl.S * wl.Hkv * wl.d * 2 * 2  # K + V rows read per call (S grows by < 0.02%)
     io_bytes = 2 * wl.B * wl.Hq * wl.d * 2  # q read + out written
     alg_bytes = kv_bytes + io_bytes
@@ -657,10 +706,8 @@ def main(argv=None):
         for pr in loop.lp + loop.lp_r:
             pr.copy_(loop.lens0)
         fused = {"windowed_us_per_step": round(timed(gwf.replay, args.steps, args.warmup) * 1e6 / g, 2),
-                 "ring_us_per_step": round(timed(grf.replay, args.steps, args.warmup) * 1e6 / g, 2)}
-        for pr in loop.lp:
-            pr.copy_(loop.lens0)
-        fused["full_us_per_step"] = round(timed(loop.step_full_fused, max(3, args.steps // 2), 1) * 1e6 / g, 2)
+                 "ring_us_per_step": round(timed(grf.replay, args.steps, args.warmup) * 1e6 / g, 2),
+                 "full_us_per_step": round(fused_full_us, 2)}
         log("fused append + attention steps: " + ", ".join(f"{k}={v}" for k, v in fused.items()))
         lengths = [S for S in (131072, 262144, 524288, 1048576) if S <= wl.S]
         if not args.no_sweep and len(lengths) > 1:
@@ -674,13 +721,15 @@ def main(argv=None):
         log(f"cpu oracle: {cpu['value']:.0f} us/step on {cpu['cores']} threads")
 
     traffic = profiled_traffic()
+    ceiling = read_ceiling_gbps(loop)
+    log(f"streaming-read probe: {ceiling:.0f} GB/s; full attention call at {achieved / ceiling:.1%} of it")
     res.update({
         "value": round(us_full_step, 2),
         "unit": "us/step",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(wall_full * 1e3, 4),
+        "ms_per_step": round(us_full_step / 1e3, 5),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -688,7 +737,8 @@ def main(argv=None):
         "data": "synthetic: seeded N(0,1) bf16 KV, first 4 key rows x4",
         "config": {"workload": wl.name, "B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv, "d": wl.d, "S": wl.S,
                    "gamma": g, "W": wl.W, "sink": wl.sink, "ring_slots": wl.sink + loop.R_w,
-                   "step": f"{g} draft steps x (append 1 K/V row + attention)"},
+                   "step": f"one draft step: append 1 K/V row + full-context attention ({g} per draft-loop "
+                           "iteration, timed back to back)"},
         "full_us_per_step": round(us_full_step, 2),
         "full_attention_call_us": round(call_us, 2),
         "full_hbm_gbps": round(achieved, 1),
@@ -709,6 +759,8 @@ def main(argv=None):
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": traffic,
             "algorithmic_bytes_per_launch": alg_bytes,
+            "read_probe_gbps": None if ceiling is None else round(ceiling, 1),
+            "frac_of_read_probe": None if ceiling is None else round(achieved / ceiling, 4),
         },
         "cpu_baseline": cpu,
         "extras": extra,

@@ -394,13 +394,27 @@ int wmtp_cache_append_fp8(void* k, void* v, const void* k_new, const void* v_new
 int wmtp_fp8_quantize(const void* x, int64_t n, float scale, void* codes, void* stream);
 int wmtp_fp8_dequantize(const void* codes, int64_t n, void* out, void* stream);
 
+/*
+ * Measurement helper, not part of the method: one streaming pass over `bytes`
+ * bytes of device memory at `buf` with the attention kernels' load type
+ * (16-byte non-temporal loads), in WMTP_PROBE_BLOCKS workgroups.  Timed by
+ * the caller, its rate is the device's practical HBM read ceiling.
+ *   bytes   a multiple of 16 (0: nothing is launched); buf 16-byte aligned
+ *   sink    uint32[WMTP_PROBE_BLOCKS] device: workgroup i writes the XOR of
+ *           the 32-bit words it read, so the XOR over sink is the XOR of
+ *           every word of the buffer
+ * Returns WMTP_EINVAL for a bad size, pointer or alignment.
+ */
+#define WMTP_PROBE_BLOCKS 512
+int wmtp_hbm_read_probe(const void* buf, int64_t bytes, uint32_t* sink, void* stream);
+
 /* Human-readable name of a wmtp_status value (static string). */
 const char* wmtp_status_string(int status);
 
 /* ABI version of this header, (major << 16) | minor. */
 int wmtp_abi_version(void);
 
-#define WMTP_ABI_VERSION ((1 << 16) | 3)
+#define WMTP_ABI_VERSION ((1 << 16) | 4)
 
 #ifdef __cplusplus
 }

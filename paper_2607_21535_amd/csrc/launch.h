@@ -115,6 +115,10 @@ hipError_t launch_fp8_quantize(const uint16_t* x, int64_t n, float scale, uint8_
                                hipStream_t stream);
 hipError_t launch_fp8_dequantize(const uint8_t* codes, int64_t n, uint16_t* out, hipStream_t stream);
 
+// Streaming-read probe: WMTP_PROBE_BLOCKS workgroups read `bytes` (a multiple
+// of 16) and each writes the XOR of its words to sink[block].
+hipError_t launch_hbm_read(const void* buf, int64_t bytes, uint32_t* sink, hipStream_t stream);
+
 hipError_t launch_select(const int32_t* lens, int B, int W, int sink, int R_w, int32_t* pos_out,
                          int32_t* slot_out, int32_t* n_sel_out, int32_t* err, hipStream_t stream);
 

@@ -576,6 +576,15 @@ WMTP_EXPORT int wmtp_select_indices(const int32_t* lens, int B, int W, int sink,
   return WMTP_OK;
 }
 
+WMTP_EXPORT int wmtp_hbm_read_probe(const void* buf, int64_t bytes, uint32_t* sink, void* stream) {
+  if (bytes < 0 || bytes % 16 != 0) return WMTP_EINVAL;
+  if (bytes == 0) return WMTP_OK;
+  if (buf == nullptr || sink == nullptr || !aligned(buf, 16) || !aligned(sink, 4)) return WMTP_EINVAL;
+  if (wmtp::launch_hbm_read(buf, bytes, sink, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return WMTP_ELAUNCH;
+  return WMTP_OK;
+}
+
 WMTP_EXPORT const char* wmtp_status_string(int status) {
   switch (status) {
     case WMTP_OK: return "WMTP_OK";

@@ -57,6 +57,8 @@ __all__ = [
     "tree_append",
     "tree_attn",
     "tree_reset",
+    "hbm_read_probe",
+    "PROBE_BLOCKS",
     "status_string",
     "EXPORTED_SYMBOLS",
 ]
@@ -65,6 +67,7 @@ VARIANT_FULL, VARIANT_WINDOWED, VARIANT_RING = 0, 1, 2
 VARIANT_PAGED_FULL, VARIANT_PAGED_WINDOWED, VARIANT_TREE = 3, 4, 5
 DERR_LEN_RANGE, DERR_NNEW_RANGE, DERR_CAPACITY, DERR_SLOT_RANGE, DERR_DEPTH = 0x1, 0x2, 0x4, 0x8, 0x10
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, ELAUNCH = 0, 1, 2, 3, 4
+PROBE_BLOCKS = 512  # WMTP_PROBE_BLOCKS
 
 EXPORTED_SYMBOLS = (
     "wmtp_workspace_bytes",
@@ -95,6 +98,7 @@ EXPORTED_SYMBOLS = (
     "wmtp_tree_append",
     "wmtp_tree_attn",
     "wmtp_tree_reset",
+    "wmtp_hbm_read_probe",
     "wmtp_status_string",
     "wmtp_abi_version",
 )
@@ -142,6 +146,7 @@ _SIGNATURES = {
     "wmtp_tree_attn": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _F, _P, _SZ,
                             _P, _P]),
     "wmtp_tree_reset": (_I, [_P, _I, _P]),
+    "wmtp_hbm_read_probe": (_I, [_P, _I64, _P, _P]),
     "wmtp_status_string": (ctypes.c_char_p, [_I]),
     "wmtp_abi_version": (_I, []),
 }
@@ -577,6 +582,26 @@ def fp8_quantize(x, scale=1.0, out=None):
     st = load_library().wmtp_fp8_quantize(_ptr(x), x.numel(), float(scale), _ptr(out), _stream(x.device))
     _check(st, "wmtp_fp8_quantize")
     return out
+
+
+def hbm_read_probe(buf, sink=None):
+    """One streaming read pass over the bytes of the contiguous device tensor
+    `buf` (a measurement helper: timed, it gives the HBM read ceiling).
+    Returns sink, int32[PROBE_BLOCKS]: the XOR of the words each workgroup read."""
+    if not isinstance(buf, torch.Tensor) or not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous device tensor")
+    nbytes = buf.numel() * buf.element_size()
+    if nbytes % 16 or buf.data_ptr() % 16:
+        raise ValueError("buf must be 16-byte aligned and a multiple of 16 bytes")
+    if sink is None:
+        sink = torch.empty(PROBE_BLOCKS, dtype=torch.int32, device=buf.device)
+    else:
+        _need(sink, "sink", torch.int32, 1, buf.device)
+        if sink.numel() < PROBE_BLOCKS:
+            raise ValueError(f"sink must hold {PROBE_BLOCKS} words")
+    st = load_library().wmtp_hbm_read_probe(_ptr(buf), nbytes, _ptr(sink), _stream(buf.device))
+    _check(st, "wmtp_hbm_read_probe")
+    return sink
 
 
 def fp8_dequantize(codes, out=None):

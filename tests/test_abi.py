@@ -55,7 +55,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.wmtp_abi_version() == (1 << 16) | 3
+    assert lib.wmtp_abi_version() == (1 << 16) | 4
     for code in range(5):
         assert W.status_string(code).startswith("WMTP_")
     assert "unknown" in W.status_string(99)
@@ -401,3 +401,14 @@ def test_step_argument_checks(lib, fn):
         assert _step(lib, fn, R_w=7) == W.EINVAL
     if fn == "windowed":  # the fused path numbers the new rows after the cache's: int32
         assert _step(lib, fn, S_max=(1 << 31) - 2, n_max=4) == W.EINVAL
+
+
+@fake_pointers
+def test_read_probe_argument_checks(lib):
+    probe = lib.wmtp_hbm_read_probe
+    assert probe(P, 24, P, None) == W.EINVAL  # a multiple of 16 bytes
+    assert probe(P, -16, P, None) == W.EINVAL
+    assert probe(P + 8, 32, P, None) == W.EINVAL  # 16-byte aligned buffer
+    assert probe(None, 32, P, None) == W.EINVAL
+    assert probe(P, 32, None, None) == W.EINVAL
+    assert probe(None, 0, None, None) == W.OK  # nothing to read: no launch
