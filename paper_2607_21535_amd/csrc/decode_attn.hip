@@ -421,7 +421,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   constexpr int SEG = F8 ? VEC : (VEC < 8 ? VEC : 8);
   constexpr int NSEG = VEC / SEG;
   constexpr int KCH = D / 32;  // 16x16x32 steps over d for the logits
-  constexpr int OPAD = kWave + 1;
 
   const int lane = threadIdx.x & (kWave - 1);
   // Wave-uniform values are moved to scalar registers so that the tile loop
@@ -563,7 +562,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   constexpr int kKPitch = kKUnits + 2;          // LDS row pitch in units
   constexpr int kKLoads = kTileKeys * kKUnits / kWave;  // load instructions per tile
   constexpr int kStageBytes = kWaves * kTileKeys * kKPitch * 16;
-  constexpr int kComboBytes = (D / 4) * OPAD * 4;  // the epilogue's wave-combine buffer
+  constexpr int kComboBytes = 2 * VEC * kWave * 16;  // the epilogue's wave-combine regions
   __shared__ __align__(16) unsigned char s_lds[kStageBytes > kComboBytes ? kStageBytes : kComboBytes];
   u32x4* s_k = reinterpret_cast<u32x4*>(s_lds) + wave * kTileKeys * kKPitch;
 
@@ -674,7 +673,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   __shared__ float s_m[kWaves][16];
   __shared__ float s_l[kWaves][16];
   __shared__ float s_z[kWaves][16];
-  float* s_o = reinterpret_cast<float*>(s_lds);
   if (grp == 0) {
     s_m[wave][col] = m_run;
     s_l[wave][col] = l_run;
@@ -691,41 +689,52 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) Zx += s_z[w][col] * __builtin_amdgcn_exp2f(s_m[w][col] - Mx);
   const float f = __builtin_amdgcn_exp2f(m_run - Mx);  // 0 for a wave with no tile
-  for (int w = 0; w < kWaves; ++w) {
-    if (wave == w) {
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) {
+  for (int e = 0; e < VEC; ++e) st.acc[e] *= f;
+  // O of the four waves, summed as (w0 + w1) + (w2 + w3) in registers: a
+  // wave stores its accumulators (16 bytes per lane and output tile, lane-
+  // contiguous) and its partner adds them; two rounds over two LDS regions.
+  floatx4* s_x = reinterpret_cast<floatx4*>(s_lds);
+  if (wave & 1) {
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          const int idx = (e * 4 + jj) * OPAD + lane;
-          const float val = st.acc[e][jj] * f;
-          s_o[idx] = (w == 0) ? val : s_o[idx] + val;
-        }
-      }
-    }
-    __syncthreads();
+    for (int e = 0; e < VEC; ++e) s_x[((wave >> 1) * VEC + e) * kWave + lane] = st.acc[e];
   }
+  __syncthreads();
+  if (!(wave & 1)) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) st.acc[e] += s_x[((wave >> 1) * VEC + e) * kWave + lane];
+  }
+  __syncthreads();
+  if (wave == 2) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) s_x[e * kWave + lane] = st.acc[e];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) st.acc[e] += s_x[e * kWave + lane];
 
-  // Partial row (item, g) = blockIdx.x: pm/pl/pz [G], po [G, D].  acc[e][jj] of
-  // lane l in any wave held head l&15 and
-  // d = (e/SEG)*16*SEG + SEG*(4*(l>>4) + jj) + e%SEG.
+  // Partial row (item, g) = blockIdx.x: pm/pl/pz [G], po [G, D], written by
+  // wave 0 from its registers (acc[e][jj] of lane (grp, col): head col,
+  // d = (e / SEG) * 16 * SEG + SEG * (4 grp + jj) + e % SEG).
   const int64_t pidx = blockIdx.x;
-  if (threadIdx.x < 16 && col < a.G) {
-    a.pm[pidx * a.G + col] = Mx;
-    a.pl[pidx * a.G + col] = Lx;
-    a.pz[pidx * a.G + col] = Zx;
-  }
-  float* po = a.po + pidx * a.G * D;
-  for (int idx = threadIdx.x; idx < a.G * D; idx += kThreads) {
-    const int h = idx / D;
-    const int d = idx % D;
-    const int sg = d / (16 * SEG);
-    const int rem = d % (16 * SEG);
-    const int r = rem / SEG;  // MFMA output row: r = 4*gq + jj
-    const int e = sg * SEG + rem % SEG;
-    const int gq = r / 4;
-    const int jj = r % 4;
-    po[idx] = s_o[(e * 4 + jj) * OPAD + gq * 16 + h];
+  if (col < a.G) {
+    if (grp == 0) {
+      a.pm[pidx * a.G + col] = Mx;
+      a.pl[pidx * a.G + col] = Lx;
+      a.pz[pidx * a.G + col] = Zx;
+    }
+    float* po = a.po + (pidx * a.G + col) * D;
+#pragma unroll
+    for (int sg = 0; sg < NSEG; ++sg)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+        for (int w = 0; w < SEG / 4; ++w) {
+          const int e = sg * SEG + 4 * w;
+          *reinterpret_cast<floatx4*>(po + sg * 16 * SEG + SEG * (4 * grp + jj) + 4 * w) =
+              floatx4{st.acc[e][jj], st.acc[e + 1][jj], st.acc[e + 2][jj], st.acc[e + 3][jj]};
+        }
   }
 }
 
