@@ -1153,9 +1153,11 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
       hipLaunchKernelGGL((split_kernel<D, M, F8>), grid, dim3(kThreads), 0, st, a);
     }
   }
-  // Items per sequence the plan allows decide the merge shape.
+  // The merge shape: 1024-thread workgroups on 64-wide slices when a row has
+  // many items and their grid fits one round of the device (two per CU);
+  // else one 256-thread workgroup per row and head.
   const int64_t NV = static_cast<int64_t>(L.B) * L.qps;
-  const bool wide = L.max_items >= 32 * NV;
+  const bool wide = L.max_items >= 32 * NV && NV * L.Hq * (D / 64) <= 2 * static_cast<int64_t>(device_cus());
   MergeArgs m;
   m.lens = L.lens; m.n_q = L.n_q; m.qps = L.qps; m.pm = L.pm; m.pl = L.pl; m.pz = L.pz; m.po = L.po;
   m.out = L.out; m.lse = L.lse; m.err = L.err;
@@ -1224,6 +1226,25 @@ int query_resident_groups(int dev) {
                                                    0) != hipSuccess)
     return 0;
   return cus * per_cu;
+}
+
+// Compute units of the current device, queried once per device (MI355X:
+// 256 when no device is visible).
+int device_cus() {
+  static std::atomic<int> cache[kMaxDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) {
+    (void)hipGetLastError();
+    v = 256;
+  }
+  cache[dev].store(v, std::memory_order_relaxed);
+  return v;
 }
 
 int resident_split_groups(int d) {

@@ -62,6 +62,9 @@ struct SplitPlan {
 // sequence); n_keys_max = most keys one query row attends.
 SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_max);
 
+// Compute units of the current device (cached per device).
+int device_cus();
+
 // Index builder: kv_indptr [B+1] and kv_indices (packed) of the kept keys,
 // each entry req_to_token[b][position] (variant: full or windowed key set).
 hipError_t launch_kv_indices(const int32_t* table, int64_t table_stride, const int32_t* lens,
