@@ -188,18 +188,24 @@ __device__ __forceinline__ int visible_len(const int32_t* lens, const int32_t* n
 // selected keys per KV head divided by `target`, rounded up to a multiple of
 // kChunkQuantum and clamped to [kChunkQuantum, chunk_cap]; sequence b owns
 // ceil(n_sel(b) / chunk) consecutive items (per query row, see
-// visible_len).  Runs on one whole wave; every
-// lane returns the same value.
+// visible_len).  Runs on one whole wave; every lane returns the same value.
+// `first` receives the visible length of row `lane` (0 past the last row),
+// so that a scan over the first 64 rows need not read the lengths again.
 template <KeyMap M>
 __device__ int wave_chunk(const int32_t* lens, const int32_t* n_q, int qps, int NV, int64_t len_cap,
-                          int W, int sink, int target, int chunk_cap, int32_t* err, bool report, int dd) {
+                          int W, int sink, int target, int chunk_cap, int32_t* err, bool report, int dd,
+                          int& first) {
   const int lane = threadIdx.x & (kWave - 1);
   long long total = 0;
+  first = 0;
   for (int base = 0; base < NV; base += kWave) {
     const int v = base + lane;
     int b;
-    if (v < NV)
-      total += selected_count<M>(visible_len<M>(lens, n_q, qps, len_cap, err, v, report, b, dd), W, sink);
+    if (v < NV) {
+      const int S = visible_len<M>(lens, n_q, qps, len_cap, err, v, report, b, dd);
+      if (base == 0) first = S;
+      total += selected_count<M>(S, W, sink);
+    }
   }
 #pragma unroll
   for (int off = kWave / 2; off > 0; off >>= 1) total += __shfl_xor(total, off);
@@ -219,8 +225,9 @@ __device__ bool locate_item(const SplitArgs& a, int item, int& v_out, int& c_out
   const int NV = a.B * a.qps;
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
+    int first;
     const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, NV, a.len_cap, a.W, a.sink, a.target,
-                                    a.chunk_cap, a.err, true, a.dd);
+                                    a.chunk_cap, a.err, true, a.dd, first);
     if (lane == 0) {
       s_v = -1;
       s_chunk = chunk;
@@ -231,7 +238,7 @@ __device__ bool locate_item(const SplitArgs& a, int item, int& v_out, int& c_out
       int S = 0, cnt = 0;
       if (v < NV) {
         int b;
-        S = visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, false, b, a.dd);
+        S = base == 0 ? first : visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, false, b, a.dd);
         cnt = ceil_div_i(selected_count<M>(S, a.W, a.sink), chunk);
       }
       int incl = cnt;
@@ -768,8 +775,9 @@ __device__ bool locate_rows_item(const SplitArgs& a, int item, int& b_out, int& 
   const int NV = a.B * a.qps;
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
+    int first;
     const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, NV, a.len_cap, a.W, a.sink, a.target,
-                                    a.chunk_cap, a.err, true, a.dd);
+                                    a.chunk_cap, a.err, true, a.dd, first);
     if (lane == 0) {
       s_b = -1;
       s_chunk = chunk;
@@ -779,7 +787,9 @@ __device__ bool locate_rows_item(const SplitArgs& a, int item, int& b_out, int& 
       const int v = base + lane;
       int cnt = 0, own = 0, b = 0, n = 0;
       if (v < NV) {
-        const int S = visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, false, b, a.dd);
+        b = a.qps == 1 ? v : v / a.qps;
+        const int S =
+            base == 0 ? first : visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, false, b, a.dd);
         cnt = ceil_div_i(S, chunk);
         n = a.n_q == nullptr ? a.qps : min(max(a.n_q[b], 0), a.qps);
         own = v - b * a.qps == n - 1 ? cnt : 0;  // the last row: the sequence's items
@@ -1031,14 +1041,16 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
   __shared__ float s_L[NS];
   __shared__ float s_Z[NS];
   if (tid < kWave) {
+    int first;
     const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, a.B * a.qps, a.len_cap, a.W, a.sink,
-                                    a.target, a.chunk_cap, a.err, false, a.dd);
+                                    a.target, a.chunk_cap, a.err, false, a.dd, first);
     int before = 0, mine = 0;
     for (int base = 0; base <= v; base += kWave) {
       const int vv = base + lane;
       if (vv <= v) {
         int bb;
-        const int S = visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, vv, false, bb, a.dd);
+        const int S =
+            base == 0 ? first : visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, vv, false, bb, a.dd);
         const int cnt = ceil_div_i(selected_count<M>(S, a.W, a.sink), chunk);
         if (vv < v) before += cnt; else mine = cnt;
       }
