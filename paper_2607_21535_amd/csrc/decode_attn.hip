@@ -1037,6 +1037,7 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
 
   __shared__ int s_base, s_cnt;
   __shared__ float s_red[NT / kWave];
+  __shared__ float s_m[NS];
   __shared__ floatx4 s_o[NS][Q];
   __shared__ float s_L[NS];
   __shared__ float s_Z[NS];
@@ -1077,44 +1078,91 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
     }
   }
 
-  // Largest partial maximum.
-  float mx = neg_inf();
-  for (int c = tid; c < n; c += NT) mx = fmaxf(mx, a.pm[prow(c)]);
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-  if (lane == 0) s_red[wave] = mx;
-  __syncthreads();
-  float Mx = s_red[0];
-#pragma unroll
-  for (int w = 1; w < NT / kWave; ++w) Mx = fmaxf(Mx, s_red[w]);
-
-  floatx4 o = {0.f, 0.f, 0.f, 0.f};
-  float L = 0.f, Z = 0.f;
-#pragma unroll 8
-  for (int c = slot; c < n; c += NS) {
-    const int64_t pr = prow(c);
-    const float w = __builtin_amdgcn_exp2f(a.pm[pr] - Mx);
-    const floatx4 v = *reinterpret_cast<const floatx4*>(a.po + pr * D + d0);
-    o += w * v;
-    L += w * a.pl[pr];
-    Z += w * a.pz[pr];
-  }
-  s_o[slot][q4] = o;
-  if (q4 == 0) {
-    s_L[slot] = L;
-    s_Z[slot] = Z;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int half = NS / 2; half > 0; half >>= 1) {
-    if (slot < half) {
-      s_o[slot][q4] += s_o[slot + half][q4];
-      if (q4 == 0) {
-        s_L[slot] += s_L[slot + half];
-        s_Z[slot] += s_Z[slot + half];
-      }
+  float Mx;  // the largest partial maximum (slot 0)
+  if (n <= NS) {
+    // At most one item per slot: one round of loads; the slots are combined
+    // pairwise in a fixed tree order, rescaled to the larger maximum (every
+    // partial has at least one key, so an item's maximum is finite).
+    float m = neg_inf();
+    floatx4 o = {0.f, 0.f, 0.f, 0.f};
+    float L = 0.f, Z = 0.f;
+    if (slot < n) {
+      const int64_t pr = prow(slot);
+      m = a.pm[pr];
+      o = *reinterpret_cast<const floatx4*>(a.po + pr * D + d0);
+      L = a.pl[pr];
+      Z = a.pz[pr];
+    }
+    s_o[slot][q4] = o;
+    if (q4 == 0) {
+      s_m[slot] = m;
+      s_L[slot] = L;
+      s_Z[slot] = Z;
     }
     __syncthreads();
+    // Round `half`: slot s < half takes in slot s + half.  Every thread of a
+    // slot carries the slot's maximum in a register, so a round writes the
+    // maxima of slots below `half` only and reads those at or above it.
+#pragma unroll
+    for (int half = NS / 2; half > 0; half >>= 1) {
+      if (slot < half) {
+        const float m2 = s_m[slot + half];
+        if (m2 != neg_inf()) {
+          const float mn = fmaxf(m, m2);
+          const float f1 = __builtin_amdgcn_exp2f(m - mn);
+          const float f2 = __builtin_amdgcn_exp2f(m2 - mn);
+          s_o[slot][q4] = s_o[slot][q4] * f1 + s_o[slot + half][q4] * f2;
+          if (q4 == 0) {
+            s_m[slot] = mn;
+            s_L[slot] = s_L[slot] * f1 + s_L[slot + half] * f2;
+            s_Z[slot] = s_Z[slot] * f1 + s_Z[slot + half] * f2;
+          }
+          m = mn;
+        }
+      }
+      __syncthreads();
+    }
+    Mx = m;
+  } else {
+    // Largest partial maximum.
+    float mx = neg_inf();
+    for (int c = tid; c < n; c += NT) mx = fmaxf(mx, a.pm[prow(c)]);
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    if (lane == 0) s_red[wave] = mx;
+    __syncthreads();
+    Mx = s_red[0];
+#pragma unroll
+    for (int w = 1; w < NT / kWave; ++w) Mx = fmaxf(Mx, s_red[w]);
+
+    floatx4 o = {0.f, 0.f, 0.f, 0.f};
+    float L = 0.f, Z = 0.f;
+#pragma unroll 8
+    for (int c = slot; c < n; c += NS) {
+      const int64_t pr = prow(c);
+      const float w = __builtin_amdgcn_exp2f(a.pm[pr] - Mx);
+      const floatx4 v = *reinterpret_cast<const floatx4*>(a.po + pr * D + d0);
+      o += w * v;
+      L += w * a.pl[pr];
+      Z += w * a.pz[pr];
+    }
+    s_o[slot][q4] = o;
+    if (q4 == 0) {
+      s_L[slot] = L;
+      s_Z[slot] = Z;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int half = NS / 2; half > 0; half >>= 1) {
+      if (slot < half) {
+        s_o[slot][q4] += s_o[slot + half][q4];
+        if (q4 == 0) {
+          s_L[slot] += s_L[slot + half];
+          s_Z[slot] += s_Z[slot + half];
+        }
+      }
+      __syncthreads();
+    }
   }
   if (slot == 0) {
     const float Lt = s_L[0];
