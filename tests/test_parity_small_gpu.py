@@ -217,3 +217,38 @@ def test_ring_bulk_append_equals_sequential(dev, sink, R_w, L0, n):
     for i, (p, s) in enumerate(sim.append(n)):
         ref[0, s] = knb[0, i]
     assert np.array_equal(I.bf16_bits(kr), ref)
+
+
+def _vs_oracle(dev, d, Hq, Hkv, lens, variant, W_=None, sink=None, seed=7):
+    B = len(lens)
+    q, k, v = _make(dev, B, Hq, Hkv, d, max(lens) + 3, seed)
+    lt = G.lens_tensor(lens, dev)
+    scale = 1.0 / np.sqrt(d)
+    lse = torch.empty(B, Hq, dtype=torch.float32, device=dev)
+    if variant == "full":
+        out = W.draft_attn_full(q, k, v, lt, lse=lse)
+    else:
+        out = W.draft_attn_windowed(q, k, v, lt, W_, sink, lse=lse)
+    torch.cuda.synchronize()
+    qb = I.bf16_bits(q)
+    refs = [G.oracle_seq(qb[b], k[b], v[b], lens[b], scale, variant, W_, sink) for b in range(B)]
+    G.assert_attn_close(out, np.stack([r[0] for r in refs]), lse, np.stack([r[1] for r in refs]),
+                        what=f"{variant} d={d} lens={lens[:6]}", strict=False)
+
+
+@pytest.mark.parametrize("n_sel", [63 * 64, 64 * 64, 64 * 64 + 1, 65 * 64 + 17])
+def test_merge_around_one_item_per_slot_wide(dev, n_sel):
+    """One long row (the 1024-thread merge, 64 item slots): with 64-key items
+    the row has 63, 64, 65 and 66 items -- the merge's one-round path up to 64,
+    its two-pass path beyond."""
+    G.say(f"wide merge boundary n_sel={n_sel}")
+    _vs_oracle(dev, 256, 32, 2, [n_sel], "full")
+    _vs_oracle(dev, 256, 32, 2, [n_sel + 500], "windowed", n_sel - 4, 4)
+
+
+def test_merge_around_one_item_per_slot_rows(dev):
+    """Many short rows (the 256-thread row merge, 4 item slots): rows of 4, 5
+    and 6 items of 64 keys and ragged tails."""
+    lens = [4 * 64 - 1, 4 * 64, 4 * 64 + 1, 5 * 64, 5 * 64 + 3, 6 * 64 + 63, 64, 1] * 4
+    G.say(f"row merge boundary lens={lens[:8]}")
+    _vs_oracle(dev, 128, 16, 2, lens, "full")
