@@ -404,6 +404,28 @@ struct OnlineHeads {
     }
   }
 
+  // O^T += V^T . P^T for two tiles in one 16x16x32 MFMA per output tile
+  // (bf16 values), for the NE output tiles e0 .. e0 + NE - 1 whose value words
+  // vx0 / vx1 hold (word w: tiles e0 + 2 w, e0 + 2 w + 1).  The 32-key index
+  // 8 grp + i stands for key 4 grp + i % 4 of tile i / 4, so each lane's
+  // operands are its own weights and values of both tiles, and the output
+  // layout is that of the 16-key product.
+  template <int NE>
+  __device__ __forceinline__ void accumulate2(const bf16x8& pop, const uint32_t (&vx0)[4][NE / 2],
+                                              const uint32_t (&vx1)[4][NE / 2], int e0) {
+    static_assert(!F8, "bf16 values only");
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+      const uint32_t a01 = __builtin_amdgcn_perm(vx0[1][e >> 1], vx0[0][e >> 1], sel);
+      const uint32_t a23 = __builtin_amdgcn_perm(vx0[3][e >> 1], vx0[2][e >> 1], sel);
+      const uint32_t b01 = __builtin_amdgcn_perm(vx1[1][e >> 1], vx1[0][e >> 1], sel);
+      const uint32_t b23 = __builtin_amdgcn_perm(vx1[3][e >> 1], vx1[2][e >> 1], sel);
+      acc[e0 + e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, u32x4{a01, a23, b01, b23}),
+                                                            pop, acc[e0 + e], 0, 0, 0);
+    }
+  }
+
   // One tile: logits s (key jt + 4 grp + i), value words vx.
   template <int NW>
   __device__ __forceinline__ void add(const floatx4& s, const uint32_t (&vx)[4][NW], int jt, int j_end,
@@ -762,7 +784,8 @@ constexpr int kRowStep = kChunkQuantum;           // keys per LDS step: four 16-
 #ifndef WMTP_ROW_GROUP
 #define WMTP_ROW_GROUP 4
 #endif
-constexpr int kRowGroup = WMTP_ROW_GROUP;         // tiles per softmax update
+constexpr int kRowGroup = WMTP_ROW_GROUP;         // tiles per softmax update (even: PV in tile pairs)
+static_assert(kRowGroup % 2 == 0, "the multi-row kernel's PV product takes tiles in pairs");
 
 // Finds sequence b and chunk c of multi-row work item `item`: sequence b owns
 // as many items as its last row has chunks.  Also returns b's row count n and
@@ -949,28 +972,34 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
                   sc[u], 0, 0, 0);
           bf16x4 pop[NT];
           st.template weigh<NT, true>(sc, js, j_end, sl2, grp, pop);
-#pragma unroll
-          for (int u = 0; u < NT; ++u) {
-            // V words of keys 4 grp + i of the tile at this lane's value
-            // columns (as split_kernel loads them).
-            uint32_t vx[4][VEC / 2];
+          // V words of keys 4 grp + i of tile u at this lane's value columns
+          // (as split_kernel loads them), one run of SEG columns (segment sg)
+          // at a time: output tiles sg * SEG .. sg * SEG + SEG - 1.
+          auto load_v = [&](int u, int sg, uint32_t (&vx)[4][SEG / 2]) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const uint16_t* p = sv + ((u0 + u) * kTileKeys + 4 * grp + i) * kVPitch * 8 + SEG * col;
+              const uint16_t* p = sv + ((u0 + u) * kTileKeys + 4 * grp + i) * kVPitch * 8 + SEG * col + sg * 16 * SEG;
+              if constexpr (SEG == 8) {
+                const u32x4 x = *reinterpret_cast<const u32x4*>(p);
 #pragma unroll
-              for (int sg = 0; sg < NSEG; ++sg) {
-                if constexpr (SEG == 8) {
-                  const u32x4 x = *reinterpret_cast<const u32x4*>(p + sg * 16 * SEG);
-#pragma unroll
-                  for (int w = 0; w < 4; ++w) vx[i][sg * 4 + w] = x[w];
-                } else {
-                  const u32x2 x = *reinterpret_cast<const u32x2*>(p + sg * 16 * SEG);
-                  vx[i][sg * 2] = x[0];
-                  vx[i][sg * 2 + 1] = x[1];
-                }
+                for (int w = 0; w < 4; ++w) vx[i][w] = x[w];
+              } else {
+                const u32x2 x = *reinterpret_cast<const u32x2*>(p);
+                vx[i][0] = x[0];
+                vx[i][1] = x[1];
               }
             }
-            st.accumulate(pop[u], vx);
+          };
+#pragma unroll
+          for (int u = 0; u < NT; u += 2) {
+            const bf16x8 pp = __builtin_shufflevector(pop[u], pop[u + 1], 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+            for (int sg = 0; sg < NSEG; ++sg) {
+              uint32_t vx0[4][SEG / 2], vx1[4][SEG / 2];
+              load_v(u, sg, vx0);
+              load_v(u + 1, sg, vx1);
+              st.template accumulate2<SEG>(pp, vx0, vx1, sg * SEG);
+            }
           }
         }
       }
