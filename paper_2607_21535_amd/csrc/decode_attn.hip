@@ -1,5 +1,6 @@
-// Split-K single-token GQA decode attention for gfx950 (full, windowed and
-// ring key maps), followed by a log-sum-exp merge of the split partials.
+// Split-K GQA decode attention for gfx950 (full, windowed, ring, paged, tree
+// and fused-step key maps; bf16 or fp8 cache), a multi-row variant for the
+// full-context draft-extend, and the log-sum-exp merge of the split partials.
 //
 // What is computed: for every sequence b and query head h, softmax attention
 // of q[b,h] over the keys the variant selects (Windowed-MTP Section 4
@@ -14,7 +15,8 @@
 // the device-resident lengths, so variable-length batches pack without
 // holes) and one 256-thread workgroup handles one (item, KV head).  The four
 // waves of a workgroup take interleaved 16-key tiles, so the group streams
-// one contiguous key range.
+// one contiguous key range; each tile's K rows pass through LDS on their way
+// to the MFMA (whole-row loads), its V values go straight to registers.
 //
 // Per 16-key tile, on one wave:
 //   S^T[16 keys, 16 heads] = K_tile . Q^T   v_mfma_f32_16x16x32_bf16, d/32 steps
@@ -28,9 +30,9 @@
 // with no transpose through LDS.  P is rounded to bf16 for that product; the
 // output is normalised by the sum of the same rounded weights, and the
 // log-sum-exp uses the fp32 weights.
-// The four waves combine their state through LDS in a fixed order, and the
-// merge kernel combines the items of a sequence in a fixed order: results are
-// bitwise reproducible.
+// The four waves combine their state in a fixed order (m, l, z through LDS,
+// O pairwise in registers), and the merge kernel combines the items of a
+// sequence in a fixed order: results are bitwise reproducible.
 //
 // Query heads beyond G in the 16-wide MFMA operand are zero and discarded.
 
@@ -265,18 +267,11 @@ __device__ bool locate_item(const SplitArgs& a, int item, int& v_out, int& c_out
   return v_out >= 0;
 }
 
-#ifndef WMTP_NT_LOADS
-#define WMTP_NT_LOADS 1
-#endif
-
-// Streaming loads of the KV cache (read once per call).
+// Streaming loads of the KV cache: non-temporal (read once per call, kept out
+// of the caches' way).
 template <typename T, typename E>
 __device__ __forceinline__ T stream_load(const E* p) {
-#if WMTP_NT_LOADS
   return __builtin_nontemporal_load(reinterpret_cast<const T*>(p));
-#else
-  return *reinterpret_cast<const T*>(p);
-#endif
 }
 
 // Registers of one 16-key tile on one lane.  kx holds 16-byte units
@@ -781,10 +776,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 constexpr int kRowWaves = 8;                      // query rows per pass, one per wave
 constexpr int kRowThreads = kRowWaves * kWave;
 constexpr int kRowStep = kChunkQuantum;           // keys per LDS step: four 16-key tiles
-#ifndef WMTP_ROW_GROUP
-#define WMTP_ROW_GROUP 4
-#endif
-constexpr int kRowGroup = WMTP_ROW_GROUP;         // tiles per softmax update (even: PV in tile pairs)
+constexpr int kRowGroup = 4;                      // tiles per softmax update (even: PV in tile pairs)
 static_assert(kRowGroup % 2 == 0, "the multi-row kernel's PV product takes tiles in pairs");
 
 // Finds sequence b and chunk c of multi-row work item `item`: sequence b owns
