@@ -246,8 +246,10 @@ def attention_call_times(loop, steps, warmup):
     return np.array([a.elapsed_time(b) for a, b in pairs])
 
 
-def sweep_flatness(loop, lengths, reps=20):
-    """Per-draft-step time (append + attention, graph replay) vs length."""
+def sweep_flatness(loop, lengths, steps, warmup):
+    """Per-draft-step time (append + attention) vs length: at each starting
+    length, the captured gamma-step loop replayed back to back (as the
+    windowed and ring figures at 1M are timed)."""
     wl = loop.wl
     rows = []
     for S in lengths:
@@ -255,19 +257,8 @@ def sweep_flatness(loop, lengths, reps=20):
         for name, body in (("windowed", loop.step_windowed), ("full", loop.step_full)):
             loop.lens.fill_(S)
             g = graph_of(body)
-            for _ in range(3):
-                loop.lens.fill_(S)
-                g.replay()
-            torch.cuda.synchronize()
-            ts = []
-            for _ in range(reps):
-                loop.lens.fill_(S)
-                torch.cuda.synchronize()
-                t0 = time.perf_counter()
-                g.replay()
-                torch.cuda.synchronize()
-                ts.append(time.perf_counter() - t0)
-            res[name] = float(np.median(ts)) * 1e6 / wl.gamma
+            loop.lens.fill_(S)
+            res[name] = timed(g.replay, steps, warmup) * 1e6 / wl.gamma
         rows.append({"S": S, "windowed_us_per_step": round(res["windowed"], 2),
                      "full_us_per_step": round(res["full"], 2)})
         log(f"sweep S={S}: windowed {res['windowed']:.2f} us/step, full {res['full']:.2f} us/step")
@@ -735,7 +726,7 @@ def main(argv=None):
         log("fused append + attention steps: " + ", ".join(f"{k}={v}" for k, v in fused.items()))
         lengths = [S for S in (131072, 262144, 524288, 1048576) if S <= wl.S]
         if not args.no_sweep and len(lengths) > 1:
-            sweep = sweep_flatness(loop, lengths)
+            sweep = sweep_flatness(loop, lengths, args.steps, args.warmup)
         caches = cache_figures(loop)
     extra = None if (args.only_full or args.no_extras) else extras(loop)
 
