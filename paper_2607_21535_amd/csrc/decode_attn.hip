@@ -399,28 +399,6 @@ struct OnlineHeads {
     }
   }
 
-  // O^T += V^T . P^T for two tiles in one 16x16x32 MFMA per output tile
-  // (bf16 values), for the NE output tiles e0 .. e0 + NE - 1 whose value words
-  // vx0 / vx1 hold (word w: tiles e0 + 2 w, e0 + 2 w + 1).  The 32-key index
-  // 8 grp + i stands for key 4 grp + i % 4 of tile i / 4, so each lane's
-  // operands are its own weights and values of both tiles, and the output
-  // layout is that of the 16-key product.
-  template <int NE>
-  __device__ __forceinline__ void accumulate2(const bf16x8& pop, const uint32_t (&vx0)[4][NE / 2],
-                                              const uint32_t (&vx1)[4][NE / 2], int e0) {
-    static_assert(!F8, "bf16 values only");
-#pragma unroll
-    for (int e = 0; e < NE; ++e) {
-      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-      const uint32_t a01 = __builtin_amdgcn_perm(vx0[1][e >> 1], vx0[0][e >> 1], sel);
-      const uint32_t a23 = __builtin_amdgcn_perm(vx0[3][e >> 1], vx0[2][e >> 1], sel);
-      const uint32_t b01 = __builtin_amdgcn_perm(vx1[1][e >> 1], vx1[0][e >> 1], sel);
-      const uint32_t b23 = __builtin_amdgcn_perm(vx1[3][e >> 1], vx1[2][e >> 1], sel);
-      acc[e0 + e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, u32x4{a01, a23, b01, b23}),
-                                                            pop, acc[e0 + e], 0, 0, 0);
-    }
-  }
-
   // One tile: logits s (key jt + 4 grp + i), value words vx.
   template <int NW>
   __device__ __forceinline__ void add(const floatx4& s, const uint32_t (&vx)[4][NW], int jt, int j_end,
@@ -738,10 +716,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
   for (int e = 0; e < VEC; ++e) st.acc[e] += s_x[e * kWave + lane];
 
-  // Partial row (item, g) = blockIdx.x: pm/pl/pz [G], po [G, D], written by
+  // Partial row item * Hkv + g: pm/pl/pz [G], po [G, D], written by
   // wave 0 from its registers (acc[e][jj] of lane (grp, col): head col,
   // d = (e / SEG) * 16 * SEG + SEG * (4 grp + jj) + e % SEG).
-  const int64_t pidx = blockIdx.x;
+  const int64_t pidx = static_cast<int64_t>(item) * a.Hkv + g;
   if (col < a.G) {
     if (grp == 0) {
       a.pm[pidx * a.G + col] = Mx;
@@ -848,18 +826,32 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
   constexpr int NSEG = VEC / SEG;
   constexpr int KCH = D / 32;
   constexpr int kUnits = D / 8;  // 16-byte units per row of one KV head
-  // LDS row pitches (units) that keep the operand reads free of bank
-  // conflicts on gfx950: the K operand (16 lanes read one unit of 16 rows)
-  // needs two units of padding; the V operand (16 lanes read 16 consecutive
-  // units of one row) needs none, except at d = 64 (8-byte reads), two.
+  // K rows are staged key-major at a pitch of kUnits + 2 units: the K
+  // operand read (16 lanes take one unit of 16 rows) is then free of bank
+  // conflicts on gfx950.
   constexpr int kPitch = kUnits + 2;
-  constexpr int kVPitch = D == 64 ? kUnits + 2 : kUnits;
   constexpr int kLoads = kRowStep * kUnits / kRowThreads;  // K (and V) units per thread and step
-  static_assert(kLoads >= 1 && kRowStep * kUnits % kRowThreads == 0, "step must tile the workgroup");
+  static_assert(kLoads == 1 || kLoads == 2 || kLoads == 4, "a thread's keys must sit in one 4-key run");
+  static_assert(kRowStep * kUnits % kRowThreads == 0, "step must tile the workgroup");
+  // V is staged transposed, in the order of the PV product's operand: one
+  // LDS row per value column d, holding the step's 64 keys as
+  // k' = 32 pair + 8 grp + 4 (tile % 2) + i for key 4 grp + i of tile
+  // 2 pair + tile % 2.  A 16x16x32 MFMA then takes two tiles at once: its
+  // 32-key index 8 grp + i stands for key 4 grp + i % 4 of tile i / 4, so
+  // each lane's weights (P^T operand) are its own of both tiles, and the
+  // output layout is that of the 16-key product.  Lane (grp, col)
+  // then reads the operand of output tile e of segment sg (value column
+  // d = 16 SEG sg + SEG col + e, keys 8 grp .. 8 grp + 7 of a tile pair) as
+  // one 16-byte unit, with no byte permutes: the transposition is done once
+  // per workgroup when the rows are stored, not once per query row.  Row
+  // r(d) = (NSEG e + sg) * 16 + col puts the 16 lanes of one read on 16
+  // consecutive rows; an odd pitch (8 units of keys + 1) keeps those reads
+  // free of bank conflicts.
+  constexpr int kVTPitch = kRowStep * 2 / 16 + 1;
   // Two buffers of one step's K and V rows: a step is computed from one while
   // the next step's rows, loaded during that computation, go to the other.
   __shared__ u32x4 s_k[2][kRowStep * kPitch];
-  __shared__ u32x4 s_v[2][kRowStep * kVPitch];
+  __shared__ u32x4 s_vt[2][D * kVTPitch];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -890,27 +882,45 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
   const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + seq_off;
   const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + seq_off;
 
-  // Unit f = i * kRowThreads + tid of a step is unit f % kUnits of key
-  // f / kUnits: a load instruction covers whole rows.  Keys past j1 read row
-  // j0 (masked out of every row's softmax).
+  // Thread tid holds unit tid % kUnits of the kLoads consecutive keys
+  // kLoads * (tid / kUnits) + i of a step (a run inside one 4-key group of a
+  // tile); the lanes of a load instruction cover whole rows of several keys.
+  // Keys past j1 read row j0 (masked out of every row's softmax).
+  const int my_unit = tid % kUnits;
+  const int my_key0 = kLoads * (tid / kUnits);
+  // Where this thread's keys and value columns land in the transposed V:
+  // k' of its first key, and the row of value column 8 my_unit + x.
+  const int my_kq = ((my_key0 >> 5) << 5) + ((my_key0 & 15) >> 2) * 8 + ((my_key0 >> 4) & 1) * 4 + (my_key0 & 3);
+  auto vt_row = [](int dd) { return ((dd % SEG) * NSEG + dd / (16 * SEG)) * 16 + (dd / SEG) % 16; };
   u32x4 rk[kLoads], rv[kLoads];
   auto load = [&](int s) {
-    const int js = j0 + s * kRowStep;
+    const int js = j0 + s * kRowStep + my_key0;
 #pragma unroll
     for (int i = 0; i < kLoads; ++i) {
-      const int f = i * kRowThreads + tid;
-      const int j = js + f / kUnits;
-      const int64_t off = static_cast<int64_t>(j < j1 ? j : j0) * rs + (f % kUnits) * 8;
+      const int j = js + i;
+      const int64_t off = static_cast<int64_t>(j < j1 ? j : j0) * rs + my_unit * 8;
       rk[i] = stream_load<u32x4>(kbase + off);
       rv[i] = stream_load<u32x4>(vbase + off);
     }
   };
   auto stash = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      const int f = i * kRowThreads + tid;
-      s_k[buf][(f / kUnits) * kPitch + f % kUnits] = rk[i];
-      s_v[buf][(f / kUnits) * kVPitch + f % kUnits] = rv[i];
+    for (int i = 0; i < kLoads; ++i) s_k[buf][(my_key0 + i) * kPitch + my_unit] = rk[i];
+    unsigned char* vt = reinterpret_cast<unsigned char*>(s_vt[buf]) + my_kq * 2;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {  // value column 8 my_unit + x: this thread's keys, in k' order
+      const int w = x >> 1;
+      unsigned char* dst = vt + vt_row(8 * my_unit + x) * (kVTPitch * 16);
+      if constexpr (kLoads == 4) {
+        const uint32_t sel = (x & 1) ? 0x07060302u : 0x05040100u;
+        *reinterpret_cast<u32x2*>(dst) = u32x2{__builtin_amdgcn_perm(rv[1][w], rv[0][w], sel),
+                                               __builtin_amdgcn_perm(rv[3][w], rv[2][w], sel)};
+      } else if constexpr (kLoads == 2) {
+        const uint32_t sel = (x & 1) ? 0x07060302u : 0x05040100u;
+        *reinterpret_cast<uint32_t*>(dst) = __builtin_amdgcn_perm(rv[1][w], rv[0][w], sel);
+      } else {
+        *reinterpret_cast<uint16_t*>(dst) = static_cast<uint16_t>(rv[0][w] >> (16 * (x & 1)));
+      }
     }
   };
   const float sl2 = a.scale_log2;
@@ -945,7 +955,7 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
       if (s + 1 < n_steps) load(s + 1);
       if (active) {
         const u32x4* sk = s_k[buf];
-        const uint16_t* sv = reinterpret_cast<const uint16_t*>(s_v[buf]);
+        const u32x4* svt = s_vt[buf];
         constexpr int NT = kRowGroup;
 #pragma unroll
         for (int u0 = 0; u0 < kRowStep / kTileKeys; u0 += NT) {
@@ -964,34 +974,21 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
                   sc[u], 0, 0, 0);
           bf16x4 pop[NT];
           st.template weigh<NT, true>(sc, js, j_end, sl2, grp, pop);
-          // V words of keys 4 grp + i of tile u at this lane's value columns
-          // (as split_kernel loads them), one run of SEG columns (segment sg)
-          // at a time: output tiles sg * SEG .. sg * SEG + SEG - 1.
-          auto load_v = [&](int u, int sg, uint32_t (&vx)[4][SEG / 2]) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const uint16_t* p = sv + ((u0 + u) * kTileKeys + 4 * grp + i) * kVPitch * 8 + SEG * col + sg * 16 * SEG;
-              if constexpr (SEG == 8) {
-                const u32x4 x = *reinterpret_cast<const u32x4*>(p);
-#pragma unroll
-                for (int w = 0; w < 4; ++w) vx[i][w] = x[w];
-              } else {
-                const u32x2 x = *reinterpret_cast<const u32x2*>(p);
-                vx[i][0] = x[0];
-                vx[i][1] = x[1];
-              }
-            }
-          };
+          // O^T += V^T . P^T over tile pairs: output tile sg * SEG + e takes
+          // the transposed V unit of value column 16 SEG sg + SEG col + e,
+          // keys 8 grp .. 8 grp + 7 of the pair.
 #pragma unroll
           for (int u = 0; u < NT; u += 2) {
             const bf16x8 pp = __builtin_shufflevector(pop[u], pop[u + 1], 0, 1, 2, 3, 4, 5, 6, 7);
+            const int unit = 2 * (u0 + u) + grp;  // 16-byte unit of keys 8 grp.. of pair (u0 + u) / 2
 #pragma unroll
-            for (int sg = 0; sg < NSEG; ++sg) {
-              uint32_t vx0[4][SEG / 2], vx1[4][SEG / 2];
-              load_v(u, sg, vx0);
-              load_v(u + 1, sg, vx1);
-              st.template accumulate2<SEG>(pp, vx0, vx1, sg * SEG);
-            }
+            for (int sg = 0; sg < NSEG; ++sg)
+#pragma unroll
+              for (int e = 0; e < SEG; ++e) {
+                const u32x4 w = svt[((e * NSEG + sg) * 16 + col) * kVTPitch + unit];
+                st.acc[sg * SEG + e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), pp,
+                                                                                st.acc[sg * SEG + e], 0, 0, 0);
+              }
           }
         }
       }
