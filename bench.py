@@ -447,8 +447,9 @@ def fp8_figures(loop):
 
 
 def cpu_baseline(loop, budget_s=20.0):
-    """The float64 oracle on this host: full-context draft steps at 1M on a
-    bounded sample (as many whole steps as fit the budget, at least one)."""
+    """The float64 oracle on this host: full-context draft steps at the
+    workload's shape on a bounded sample (as many whole steps as fit the
+    budget, at least one)."""
     from oracle import attention as A
 
     try:
@@ -508,7 +509,7 @@ def cpu_baseline(loop, budget_s=20.0):
         "unit": "us/step",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"{done} full-context draft steps (Hq=32, Hkv=2, d=256, S=1,048,576, float64 NumPy) "
+        "sample": (f"{done} full-context draft steps (Hq={wl.Hq}, Hkv={wl.Hkv}, d={wl.d}, S={S:,}, float64 NumPy) "
                    f"+ {nw} windowed steps ({win_s * 1e6:.0f} us/step); CPU: {cpu_model()}"),
         "windowed_us_per_step": round(win_s * 1e6, 1),
         "windowed_us_per_step_1_thread": win1_us,
@@ -749,7 +750,8 @@ def main(argv=None):
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic: seeded N(0,1) bf16 KV, first 4 key rows x4",
+        "data": "synthetic: seeded N(0,1) bf16 KV" + (
+            f", first {wl.bias_rows} key rows x{wl.sink_bias:g}" if wl.bias_rows else ""),
         "config": {"workload": wl.name, "B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv, "d": wl.d, "S": wl.S,
                    "gamma": g, "W": wl.W, "sink": wl.sink, "ring_slots": wl.sink + loop.R_w,
                    "step": f"one draft step: append 1 K/V row + full-context attention ({g} per draft-loop "
