@@ -20,7 +20,8 @@ Also reported: windowed/full time per draft step at 128K, 256K, 512K and 1M
 the float64 CPU oracle timed on a bounded sample on this host, the fused
 append + attention steps, and context figures: draft-extend over gamma+1 new
 rows, the paged pool's KV-index build (native vs windowed), paged attention
-over a shuffled pool, and the same attention over an fp8 cache.
+over a shuffled pool, and the same attention over an fp8 cache and an fp8
+pool.
 
 --workload selects another configuration: decode_s8k and draft_loop_s128k
 run the same loop at their shapes; batch32_varlen times one decode call over
@@ -441,7 +442,23 @@ def fp8_figures(loop):
            "windowed_attention_call_us": round(win, 2), "ring_attention_call_us": round(ring, 2),
            "algorithmic_bytes_full": alg}
     log(f"fp8: full {full:.1f} us ({res['full_hbm_gbps']} GB/s), windowed {win:.2f} us, ring {ring:.2f} us")
-    del k8, v8, kr8, vr8
+    del kr8, vr8
+    # the same codes in a token pool at a random permutation of its rows
+    C = loop.S_max
+    g = torch.Generator(device="cpu").manual_seed(wl.seed + 1)
+    table = torch.randperm(C, generator=g).to(torch.int32).view(1, C).to(dev)
+    kp8 = torch.empty((C, wl.Hkv, wl.d), dtype=torch.uint8, device=dev)
+    vp8 = torch.empty_like(kp8)
+    kp8[table[0].long()] = k8[0]
+    vp8[table[0].long()] = v8[0]
+    del k8, v8
+    pfull = event_us(lambda: W.paged_attn_full_fp8(q, kp8, vp8, table, loop.lens, scale=wl.scale), reps=10, warm=3)
+    pwin = graph_us(lambda: W.paged_attn_windowed_fp8(q, kp8, vp8, table, loop.lens, wl.W, wl.sink,
+                                                      scale=wl.scale))
+    res.update({"paged_full_us": round(pfull, 1), "paged_full_hbm_gbps": round(alg / pfull / 1e3, 1),
+                "paged_windowed_us": round(pwin, 2)})
+    log(f"fp8 paged pool: full {pfull:.1f} us, windowed {pwin:.2f} us")
+    del kp8, vp8
     torch.cuda.empty_cache()
     return res
 

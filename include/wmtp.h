@@ -369,6 +369,26 @@ int wmtp_ring_attn_fp8(const void* q, const void* k_ring, const void* v_ring, co
                        size_t ws_bytes, int32_t* err, void* stream);
 
 /*
+ * fp8 paged draft attention (Section 7 KV-cache quantization over the paged
+ * pool of Section 4 / Appendix A): wmtp_paged_attn_full / _windowed over a
+ * pool of E4M3 codes, k_pool and v_pool [pool_rows, Hkv, d] uint8 (16-byte
+ * aligned), with the per-tensor scales of the fp8 cache calls.  Results
+ * equal, bit for bit, the fp8 dense call over a cache holding the same rows.
+ * Workspace and error bits as for the bf16 paged calls.
+ */
+int wmtp_paged_attn_full_fp8(const void* q, const void* k_pool, const void* v_pool,
+                             const int32_t* req_to_token, const int32_t* lens, void* out,
+                             float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
+                             int64_t table_stride, float scale, float k_scale, float v_scale,
+                             void* ws, size_t ws_bytes, int32_t* err, void* stream);
+int wmtp_paged_attn_windowed_fp8(const void* q, const void* k_pool, const void* v_pool,
+                                 const int32_t* req_to_token, const int32_t* lens, void* out,
+                                 float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
+                                 int64_t table_stride, int W, int sink, float scale,
+                                 float k_scale, float v_scale, void* ws, size_t ws_bytes,
+                                 int32_t* err, void* stream);
+
+/*
  * fp8 appends: as wmtp_ring_append / wmtp_cache_append, with the bf16 rows
  * quantised on the way in.  Element x of a key row is stored as the E4M3
  * code nearest to x / k_scale (division in float32, correctly rounded),
@@ -414,7 +434,7 @@ const char* wmtp_status_string(int status);
 /* ABI version of this header, (major << 16) | minor. */
 int wmtp_abi_version(void);
 
-#define WMTP_ABI_VERSION ((1 << 16) | 4)
+#define WMTP_ABI_VERSION ((1 << 16) | 5)
 
 #ifdef __cplusplus
 }

@@ -1262,7 +1262,9 @@ hipError_t launch_d(const AttnLaunch& L, hipStream_t st) {
       case WMTP_VARIANT_FULL: return launch_typed<D, KeyMap::Full, true>(L, st);
       case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::Window, true>(L, st);
       case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::Ring, true>(L, st);
-      default: return hipErrorInvalidValue;  // no fp8 paged kernels
+      case WMTP_VARIANT_PAGED_FULL: return launch_typed<D, KeyMap::PagedFull, true>(L, st);
+      case WMTP_VARIANT_PAGED_WINDOWED: return launch_typed<D, KeyMap::PagedWindow, true>(L, st);
+      default: return hipErrorInvalidValue;  // no fp8 tree kernels
     }
   }
   if (L.step) {

@@ -90,10 +90,7 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
     if (static_cast<int64_t>(R_w) < static_cast<int64_t>(W) + dd) return WMTP_EINVAL;
     if (static_cast<int64_t>(sink) + R_w + rows2 > INT_MAX) return WMTP_EINVAL;
   }
-  if (fp8) {
-    if (paged_variant(variant)) return WMTP_EUNSUPPORTED;
-    if (!valid_scale(k_scale) || !valid_scale(v_scale)) return WMTP_EINVAL;
-  }
+  if (fp8 && (!valid_scale(k_scale) || !valid_scale(v_scale))) return WMTP_EINVAL;
   if (q_max < 1 || q_max > kMaxQueryRows) return WMTP_EINVAL;
   if (static_cast<int64_t>(B) * q_max > INT_MAX / 64) return WMTP_EINVAL;
   if (windowed_variant(variant)) {
@@ -387,6 +384,28 @@ WMTP_EXPORT int wmtp_draft_attn_windowed_fp8(const void* q, const void* k, const
   return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv,
                           d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream, nullptr, 0, true,
                           k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_paged_attn_full_fp8(const void* q, const void* k_pool, const void* v_pool,
+                                          const int32_t* req_to_token, const int32_t* lens, void* out,
+                                          float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
+                                          int64_t table_stride, float scale, float k_scale,
+                                          float v_scale, void* ws, size_t ws_bytes, int32_t* err,
+                                          void* stream) {
+  return attention_common(WMTP_VARIANT_PAGED_FULL, q, k_pool, v_pool, lens, nullptr, 1, out, lse, B,
+                          Hq, Hkv, d, table_stride, 1, 0, 1, scale, ws, ws_bytes, err, stream,
+                          req_to_token, pool_rows, true, k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_paged_attn_windowed_fp8(const void* q, const void* k_pool, const void* v_pool,
+                                              const int32_t* req_to_token, const int32_t* lens,
+                                              void* out, float* lse, int B, int Hq, int Hkv, int d,
+                                              int64_t pool_rows, int64_t table_stride, int W,
+                                              int sink, float scale, float k_scale, float v_scale,
+                                              void* ws, size_t ws_bytes, int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_PAGED_WINDOWED, q, k_pool, v_pool, lens, nullptr, 1, out,
+                          lse, B, Hq, Hkv, d, table_stride, W, sink, W, scale, ws, ws_bytes, err,
+                          stream, req_to_token, pool_rows, true, k_scale, v_scale);
 }
 
 WMTP_EXPORT int wmtp_ring_attn_fp8(const void* q, const void* k_ring, const void* v_ring,

@@ -46,6 +46,8 @@ __all__ = [
     "draft_attn_full_fp8",
     "draft_attn_windowed_fp8",
     "ring_attn_fp8",
+    "paged_attn_full_fp8",
+    "paged_attn_windowed_fp8",
     "cache_append_fp8",
     "ring_append_fp8",
     "fp8_quantize",
@@ -87,6 +89,8 @@ EXPORTED_SYMBOLS = (
     "wmtp_draft_attn_full_fp8",
     "wmtp_draft_attn_windowed_fp8",
     "wmtp_ring_attn_fp8",
+    "wmtp_paged_attn_full_fp8",
+    "wmtp_paged_attn_windowed_fp8",
     "wmtp_ring_append_fp8",
     "wmtp_cache_append_fp8",
     "wmtp_fp8_quantize",
@@ -131,6 +135,10 @@ _SIGNATURES = {
     "wmtp_draft_attn_windowed_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _F, _F, _F, _P, _SZ,
                                           _P, _P]),
     "wmtp_ring_attn_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _F, _F, _P, _SZ, _P, _P]),
+    "wmtp_paged_attn_full_fp8": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I64, _F, _F, _F, _P, _SZ, _P,
+                                      _P]),
+    "wmtp_paged_attn_windowed_fp8": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I64, _I, _I, _F, _F, _F,
+                                          _P, _SZ, _P, _P]),
     "wmtp_ring_append_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _F, _P, _P]),
     "wmtp_cache_append_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I64, _I, _F, _F, _P, _P]),
     "wmtp_fp8_quantize": (_I, [_P, _I64, _F, _P, _P]),
@@ -379,11 +387,12 @@ def ring_extend(q, k_ring, v_ring, lens, W, sink, R_w, n_q=None, out=None, lse=N
     return out
 
 
-def _paged_io(q, k_pool, v_pool, table, lens, out, lse):
+def _paged_io(q, k_pool, v_pool, table, lens, out, lse, fp8=False):
     _need(q, "q", torch.bfloat16, 3)
     dev = q.device
-    _need(k_pool, "k_pool", torch.bfloat16, 3, dev)
-    _need(v_pool, "v_pool", torch.bfloat16, 3, dev)
+    pool_dtype = torch.uint8 if fp8 else torch.bfloat16
+    _need(k_pool, "k_pool", pool_dtype, 3, dev)
+    _need(v_pool, "v_pool", pool_dtype, 3, dev)
     _need(table, "req_to_token", torch.int32, 2, dev)
     _need(lens, "lens", torch.int32, 1, dev)
     B, Hq, d = q.shape
@@ -545,6 +554,36 @@ def ring_attn_fp8(q, k_ring, v_ring, lens, W, sink, R_w, k_scale=1.0, v_scale=1.
         _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, W, sink, R_w,
         scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
     _check(st, "wmtp_ring_attn_fp8")
+    return out
+
+
+def paged_attn_full_fp8(q, k_pool, v_pool, req_to_token, lens, k_scale=1.0, v_scale=1.0, out=None, lse=None,
+                        scale=None, ws=None, err=None):
+    """Full-context draft attention over an fp8 (E4M3) token pool [P, Hkv, d] read through req_to_token."""
+    dev, B, Hq, d, out = _paged_io(q, k_pool, v_pool, req_to_token, lens, out, lse, fp8=True)
+    P, Hkv = k_pool.shape[0], k_pool.shape[1]
+    C = req_to_token.shape[1]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_PAGED_FULL, B, Hq, Hkv, d, C), dev)
+    st = load_library().wmtp_paged_attn_full_fp8(
+        _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(req_to_token), _ptr(lens), _ptr(out), _ptr(lse), B, Hq,
+        Hkv, d, P, C, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_paged_attn_full_fp8")
+    return out
+
+
+def paged_attn_windowed_fp8(q, k_pool, v_pool, req_to_token, lens, W, sink, k_scale=1.0, v_scale=1.0, out=None,
+                            lse=None, scale=None, ws=None, err=None):
+    """Sink + window draft attention over an fp8 (E4M3) token pool read through req_to_token."""
+    dev, B, Hq, d, out = _paged_io(q, k_pool, v_pool, req_to_token, lens, out, lse, fp8=True)
+    P, Hkv = k_pool.shape[0], k_pool.shape[1]
+    C = req_to_token.shape[1]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_PAGED_WINDOWED, B, Hq, Hkv, d, C, W, sink), dev)
+    st = load_library().wmtp_paged_attn_windowed_fp8(
+        _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(req_to_token), _ptr(lens), _ptr(out), _ptr(lse), B, Hq,
+        Hkv, d, P, C, W, sink, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_paged_attn_windowed_fp8")
     return out
 
 

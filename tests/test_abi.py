@@ -55,7 +55,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.wmtp_abi_version() == (1 << 16) | 4
+    assert lib.wmtp_abi_version() == (1 << 16) | 5
     for code in range(5):
         assert W.status_string(code).startswith("WMTP_")
     assert "unknown" in W.status_string(99)
@@ -274,6 +274,43 @@ def test_fp8_attention_argument_checks(lib, call):
     assert call(lib, q=None) == W.EINVAL
     assert call(lib, ws_bytes=1) == W.EWORKSPACE
     assert call(lib, B=0, q=None, k=None, v=None, lens=None, out=None) == W.OK
+
+
+def _paged(lib, fp8, windowed, **kw):
+    a = dict(q=P, k=P, v=P, table=P, lens=P, out=P, lse=None, B=2, Hq=16, Hkv=2, d=128, pool_rows=1000,
+             table_stride=100)
+    if windowed:
+        a.update(W=8, sink=4)
+    a.update(scale=0.1)
+    if fp8:
+        a.update(k_scale=0.5, v_scale=2.0)
+    a.update(ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    a.update(kw)
+    name = "wmtp_paged_attn_" + ("windowed" if windowed else "full") + ("_fp8" if fp8 else "")
+    return getattr(lib, name)(*a.values())
+
+
+@fake_pointers
+@pytest.mark.parametrize("fp8", [False, True])
+@pytest.mark.parametrize("windowed", [False, True])
+def test_paged_attention_argument_checks(lib, fp8, windowed):
+    def call(**kw):
+        return _paged(lib, fp8, windowed, **kw)
+    assert call(table=None) == W.EINVAL
+    assert call(table=P + 2) == W.EINVAL  # int32 table, 4-byte alignment
+    assert call(pool_rows=0) == W.EINVAL
+    assert call(table_stride=-1) == W.EINVAL
+    assert call(d=96) == W.EUNSUPPORTED
+    assert call(Hq=64, Hkv=2) == W.EUNSUPPORTED
+    assert call(k=P + 8) == W.EINVAL
+    assert call(ws_bytes=1) == W.EWORKSPACE
+    if windowed:
+        assert call(W=0) == W.EINVAL
+    if fp8:
+        for bad in (0.0, -1.0, float("nan")):
+            assert call(k_scale=bad) == W.EINVAL
+            assert call(v_scale=bad) == W.EINVAL
+    assert call(B=0, q=None, k=None, v=None, table=None, lens=None, out=None) == W.OK
 
 
 def _rapp8(lib, **kw):

@@ -6,13 +6,16 @@ builder and attention read through req_to_token.
 * paged attention equals dense attention over the same rows bit for bit (same
   kept keys, same order, same split) and the oracle within tolerance;
 * a table entry outside the pool is flagged and never dereferenced;
-* a 1M-token request scattered over a shuffled pool.
+* a 1M-token request scattered over a shuffled pool;
+* an fp8 (E4M3) pool: equal bit for bit to the fp8 dense cache over the same
+  rows, and to the oracle's paged attention over the dequantized pool.
 """
 
 import numpy as np
 import pytest
 import torch
 
+from oracle import fp8 as F
 from oracle import paged as Pg
 from paper_2607_21535_amd import inputs as I
 from paper_2607_21535_amd import wmtp as W
@@ -139,3 +142,60 @@ def _dense_v(vp, table, S, C):
     v = torch.zeros((1, C) + tuple(vp.shape[1:]), dtype=vp.dtype, device=vp.device)
     v[0, :S] = vp[table[0, :S].long()]
     return v
+
+
+class _HostCodes:
+    """Host view of a device fp8 pool [P, Hkv, d]: indexing returns the rows'
+    codes as a uint8 numpy array."""
+
+    def __init__(self, t: torch.Tensor):
+        self.t = t
+        self.shape = tuple(t.shape)
+
+    def __getitem__(self, rows):
+        idx = torch.from_numpy(np.ascontiguousarray(rows, dtype=np.int64)).to(self.t.device)
+        return self.t.index_select(0, idx).cpu().numpy()
+
+
+@pytest.mark.parametrize("d,Hq,Hkv", [(128, 16, 2), (256, 32, 2), (64, 6, 2)])
+def test_paged_fp8_equals_dense_fp8(dev, d, Hq, Hkv):
+    lens = [0, 1, 3, 68, 69, 1000, 5003, 12000]
+    B, C = len(lens), max(lens) + 5
+    P = B * C + 333
+    ks, vs = 0.75, 1.5
+    G.say(f"paged fp8 d={d} Hq={Hq} Hkv={Hkv}")
+    q = I.normal_bf16((B, Hq, d), 71, dev)
+    kd = I.normal_fp8((B, C, Hkv, d), 72, dev)
+    vd = I.normal_fp8((B, C, Hkv, d), 73, dev)
+    kp, table = _scatter(kd, lens, P, 2)
+    vp, _ = _scatter(vd, lens, P, 2)
+    lt = G.lens_tensor(lens, dev)
+    err = G.err_word(dev)
+    Wn, sink = 64, 4
+    scale = 1.0 / np.sqrt(d)
+    lse_p = torch.empty(B, Hq, dtype=torch.float32, device=dev)
+    lse_d = torch.empty_like(lse_p)
+    qb = I.bf16_bits(q)
+    for variant in ("full", "windowed"):
+        if variant == "full":
+            op = W.paged_attn_full_fp8(q, kp, vp, table, lt, ks, vs, lse=lse_p, err=err)
+            od = W.draft_attn_full_fp8(q, kd, vd, lt, ks, vs, lse=lse_d)
+        else:
+            op = W.paged_attn_windowed_fp8(q, kp, vp, table, lt, Wn, sink, ks, vs, lse=lse_p, err=err)
+            od = W.draft_attn_windowed_fp8(q, kd, vd, lt, Wn, sink, ks, vs, lse=lse_d)
+        torch.cuda.synchronize()
+        assert torch.equal(op, od), variant
+        assert torch.equal(lse_p, lse_d), variant
+        kv = F.DequantizedRows(_HostCodes(kp), ks), F.DequantizedRows(_HostCodes(vp), vs)
+        refs = [Pg.attend_paged(qb[b], kv[0], kv[1], table[b].cpu().numpy(), S, scale, variant, Wn, sink)
+                for b, S in enumerate(lens)]
+        G.assert_attn_close(op, np.stack([r[0] for r in refs]), lse_p, np.stack([r[1] for r in refs]),
+                            what=f"paged fp8 {variant}", strict=False)
+        assert torch.count_nonzero(op[0]) == 0
+    assert err.item() == 0
+    # a table entry outside the pool is flagged
+    bad = table.clone()
+    bad[7, 11] = P + 5
+    W.paged_attn_full_fp8(q, kp, vp, bad, lt, ks, vs, err=err)
+    torch.cuda.synchronize()
+    assert err.item() & W.DERR_SLOT_RANGE
