@@ -442,6 +442,15 @@ def fp8_figures(loop):
            "windowed_attention_call_us": round(win, 2), "ring_attention_call_us": round(ring, 2),
            "algorithmic_bytes_full": alg}
     log(f"fp8: full {full:.1f} us ({res['full_hbm_gbps']} GB/s), windowed {win:.2f} us, ring {ring:.2f} us")
+    # draft-extend over gamma + 1 causal rows of the fp8 cache
+    rows = wl.gamma + 1
+    qx = I.normal_bf16((1, rows, wl.Hq, wl.d), I.stream_seed(wl.seed, I.STREAM_Q, 99), dev)
+    nq = torch.full((1,), rows, dtype=torch.int32, device=dev)
+    ext_w = graph_us(lambda: W.draft_extend_windowed_fp8(qx, k8, v8, loop.lens, wl.W, wl.sink, n_q=nq,
+                                                         scale=wl.scale))
+    ext_f = event_us(lambda: W.draft_extend_full_fp8(qx, k8, v8, loop.lens, n_q=nq, scale=wl.scale), reps=3, warm=1)
+    res.update({"extend_rows": rows, "extend_windowed_us": round(ext_w, 2), "extend_full_us": round(ext_f, 1)})
+    log(f"fp8 extend ({rows} rows): windowed {ext_w:.2f} us, full {ext_f:.1f} us (per-row items)")
     del kr8, vr8
     # the same codes in a token pool at a random permutation of its rows
     C = loop.S_max

@@ -376,6 +376,29 @@ int wmtp_ring_attn_fp8(const void* q, const void* k_ring, const void* v_ring, co
  * equal, bit for bit, the fp8 dense call over a cache holding the same rows.
  * Workspace and error bits as for the bf16 paged calls.
  */
+/*
+ * fp8 draft-extend: the draft-extend calls (several causal new rows per
+ * sequence, as wmtp_draft_extend_full / _windowed / wmtp_ring_extend) over
+ * an fp8 dense cache or ring, with the per-tensor scales of the fp8 calls.
+ * The full-context form computes each new row's items separately (it reads
+ * the context once per row; the bf16 form reads it once for all rows).
+ */
+int wmtp_draft_extend_full_fp8(const void* q, const void* k, const void* v, const int32_t* lens,
+                               const int32_t* n_q, void* out, float* lse, int B, int q_max,
+                               int Hq, int Hkv, int d, int64_t S_max, float scale, float k_scale,
+                               float v_scale, void* ws, size_t ws_bytes, int32_t* err,
+                               void* stream);
+int wmtp_draft_extend_windowed_fp8(const void* q, const void* k, const void* v,
+                                   const int32_t* lens, const int32_t* n_q, void* out, float* lse,
+                                   int B, int q_max, int Hq, int Hkv, int d, int64_t S_max, int W,
+                                   int sink, float scale, float k_scale, float v_scale, void* ws,
+                                   size_t ws_bytes, int32_t* err, void* stream);
+int wmtp_ring_extend_fp8(const void* q, const void* k_ring, const void* v_ring,
+                         const int32_t* lens, const int32_t* n_q, void* out, float* lse, int B,
+                         int q_max, int Hq, int Hkv, int d, int W, int sink, int R_w, float scale,
+                         float k_scale, float v_scale, void* ws, size_t ws_bytes, int32_t* err,
+                         void* stream);
+
 int wmtp_paged_attn_full_fp8(const void* q, const void* k_pool, const void* v_pool,
                              const int32_t* req_to_token, const int32_t* lens, void* out,
                              float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
@@ -434,7 +457,7 @@ const char* wmtp_status_string(int status);
 /* ABI version of this header, (major << 16) | minor. */
 int wmtp_abi_version(void);
 
-#define WMTP_ABI_VERSION ((1 << 16) | 5)
+#define WMTP_ABI_VERSION ((1 << 16) | 6)
 
 #ifdef __cplusplus
 }

@@ -386,6 +386,39 @@ WMTP_EXPORT int wmtp_draft_attn_windowed_fp8(const void* q, const void* k, const
                           k_scale, v_scale);
 }
 
+WMTP_EXPORT int wmtp_draft_extend_full_fp8(const void* q, const void* k, const void* v,
+                                           const int32_t* lens, const int32_t* n_q, void* out,
+                                           float* lse, int B, int q_max, int Hq, int Hkv, int d,
+                                           int64_t S_max, float scale, float k_scale, float v_scale,
+                                           void* ws, size_t ws_bytes, int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_FULL, q, k, v, lens, n_q, q_max, out, lse, B, Hq, Hkv, d,
+                          S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream, nullptr, 0, true,
+                          k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_draft_extend_windowed_fp8(const void* q, const void* k, const void* v,
+                                               const int32_t* lens, const int32_t* n_q, void* out,
+                                               float* lse, int B, int q_max, int Hq, int Hkv,
+                                               int d, int64_t S_max, int W, int sink, float scale,
+                                               float k_scale, float v_scale, void* ws,
+                                               size_t ws_bytes, int32_t* err, void* stream) {
+  return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, n_q, q_max, out, lse, B, Hq, Hkv,
+                          d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream, nullptr, 0, true,
+                          k_scale, v_scale);
+}
+
+WMTP_EXPORT int wmtp_ring_extend_fp8(const void* q, const void* k_ring, const void* v_ring,
+                                     const int32_t* lens, const int32_t* n_q, void* out,
+                                     float* lse, int B, int q_max, int Hq, int Hkv, int d, int W,
+                                     int sink, int R_w, float scale, float k_scale, float v_scale,
+                                     void* ws, size_t ws_bytes, int32_t* err, void* stream) {
+  if (check_window(W, sink) == WMTP_OK && static_cast<int64_t>(sink) + R_w > INT_MAX)
+    return WMTP_EINVAL;
+  return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, n_q, q_max, out, lse, B, Hq,
+                          Hkv, d, static_cast<int64_t>(sink) + R_w, W, sink, R_w, scale, ws,
+                          ws_bytes, err, stream, nullptr, 0, true, k_scale, v_scale);
+}
+
 WMTP_EXPORT int wmtp_paged_attn_full_fp8(const void* q, const void* k_pool, const void* v_pool,
                                           const int32_t* req_to_token, const int32_t* lens, void* out,
                                           float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,

@@ -48,6 +48,9 @@ __all__ = [
     "ring_attn_fp8",
     "paged_attn_full_fp8",
     "paged_attn_windowed_fp8",
+    "draft_extend_full_fp8",
+    "draft_extend_windowed_fp8",
+    "ring_extend_fp8",
     "cache_append_fp8",
     "ring_append_fp8",
     "fp8_quantize",
@@ -89,6 +92,9 @@ EXPORTED_SYMBOLS = (
     "wmtp_draft_attn_full_fp8",
     "wmtp_draft_attn_windowed_fp8",
     "wmtp_ring_attn_fp8",
+    "wmtp_draft_extend_full_fp8",
+    "wmtp_draft_extend_windowed_fp8",
+    "wmtp_ring_extend_fp8",
     "wmtp_paged_attn_full_fp8",
     "wmtp_paged_attn_windowed_fp8",
     "wmtp_ring_append_fp8",
@@ -135,6 +141,12 @@ _SIGNATURES = {
     "wmtp_draft_attn_windowed_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _F, _F, _F, _P, _SZ,
                                           _P, _P]),
     "wmtp_ring_attn_fp8": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _F, _F, _P, _SZ, _P, _P]),
+    "wmtp_draft_extend_full_fp8": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I64, _F, _F, _F, _P, _SZ,
+                                        _P, _P]),
+    "wmtp_draft_extend_windowed_fp8": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I64, _I, _I, _F, _F,
+                                            _F, _P, _SZ, _P, _P]),
+    "wmtp_ring_extend_fp8": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _F, _F, _P, _SZ,
+                                  _P, _P]),
     "wmtp_paged_attn_full_fp8": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I64, _F, _F, _F, _P, _SZ, _P,
                                       _P]),
     "wmtp_paged_attn_windowed_fp8": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I64, _I, _I, _F, _F, _F,
@@ -310,11 +322,12 @@ def ring_attn(q, k_ring, v_ring, lens, W, sink, R_w, out=None, lse=None, scale=N
     return out
 
 
-def _extend_io(q, k, v, lens, n_q, out, lse):
+def _extend_io(q, k, v, lens, n_q, out, lse, fp8=False):
     _need(q, "q", torch.bfloat16, 4)
     dev = q.device
-    _need(k, "k", torch.bfloat16, 4, dev)
-    _need(v, "v", torch.bfloat16, 4, dev)
+    cache_dtype = torch.uint8 if fp8 else torch.bfloat16
+    _need(k, "k", cache_dtype, 4, dev)
+    _need(v, "v", cache_dtype, 4, dev)
     _need(lens, "lens", torch.int32, 1, dev)
     B, q_max, Hq, d = q.shape
     if k.shape != v.shape or k.shape[0] != B or k.shape[3] != d or lens.shape[0] != B:
@@ -584,6 +597,50 @@ def paged_attn_windowed_fp8(q, k_pool, v_pool, req_to_token, lens, W, sink, k_sc
         _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(req_to_token), _ptr(lens), _ptr(out), _ptr(lse), B, Hq,
         Hkv, d, P, C, W, sink, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
     _check(st, "wmtp_paged_attn_windowed_fp8")
+    return out
+
+
+def draft_extend_full_fp8(q, k, v, lens, k_scale=1.0, v_scale=1.0, n_q=None, out=None, lse=None, scale=None,
+                          ws=None, err=None):
+    """Causal multi-row draft attention over the full context of an fp8 (E4M3) cache."""
+    dev, B, q_max, Hq, d, out = _extend_io(q, k, v, lens, n_q, out, lse, fp8=True)
+    S_max, Hkv = k.shape[1], k.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_FULL, B * q_max, Hq, Hkv, d, S_max), dev)
+    st = load_library().wmtp_draft_extend_full_fp8(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq, Hkv, d,
+        S_max, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_extend_full_fp8")
+    return out
+
+
+def draft_extend_windowed_fp8(q, k, v, lens, W, sink, k_scale=1.0, v_scale=1.0, n_q=None, out=None, lse=None,
+                              scale=None, ws=None, err=None):
+    """Causal multi-row draft attention over an fp8 (E4M3) cache, each row under its own sink + window."""
+    dev, B, q_max, Hq, d, out = _extend_io(q, k, v, lens, n_q, out, lse, fp8=True)
+    S_max, Hkv = k.shape[1], k.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_WINDOWED, B * q_max, Hq, Hkv, d, S_max, W, sink), dev)
+    st = load_library().wmtp_draft_extend_windowed_fp8(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq, Hkv, d,
+        S_max, W, sink, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_extend_windowed_fp8")
+    return out
+
+
+def ring_extend_fp8(q, k_ring, v_ring, lens, W, sink, R_w, k_scale=1.0, v_scale=1.0, n_q=None, out=None,
+                    lse=None, scale=None, ws=None, err=None):
+    """Causal multi-row windowed draft attention over an fp8 (E4M3) ring (R_w >= W + q_max - 1)."""
+    dev, B, q_max, Hq, d, out = _extend_io(q, k_ring, v_ring, lens, n_q, out, lse, fp8=True)
+    if k_ring.shape[1] != sink + R_w:
+        raise ValueError(f"ring must hold sink + R_w = {sink + R_w} rows, has {k_ring.shape[1]}")
+    Hkv = k_ring.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ws = _workspace(ws, workspace_bytes(VARIANT_RING, B * q_max, Hq, Hkv, d, sink + R_w, W, sink), dev)
+    st = load_library().wmtp_ring_extend_fp8(
+        _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq,
+        Hkv, d, W, sink, R_w, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
+    _check(st, "wmtp_ring_extend_fp8")
     return out
 
 

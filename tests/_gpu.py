@@ -65,13 +65,22 @@ def oracle_seq(q_bits, k_dev_seq, v_dev_seq, S, scale, variant, W_=None, sink=No
     return A.attend_sequence(q_bits, HostRows(k_dev_seq), HostRows(v_dev_seq), S, scale, mask)
 
 
-def assert_attn_close(out, o_ref, lse=None, lse_ref=None, what="", strict=True):
+def assert_attn_close(out, o_ref, lse=None, lse_ref=None, what="", strict=True, v_max=None):
+    """Output within the contract's max-abs tolerance (strict) or, for small
+    cases with large outputs, within the bf16 rounding of the output itself;
+    v_max (the largest |value| the call can combine) adds the error of the
+    weights entering the PV product rounded to bf16: each moves by at most
+    2^-9 relative, so the output moves by at most 2^-9 max_i |v_i - o|, and
+    that is at most 2^-8 v_max.  Rows with few keys and a wide spread of
+    values reach it.  Also checks the normwise error per row and the lse."""
     o = out.detach().float().cpu().numpy().astype(np.float64)
     o_ref = np.asarray(o_ref, dtype=np.float64).reshape(o.shape)
     d = o.shape[-1]
     err = np.abs(o - o_ref)
     assert np.all(np.isfinite(o)), f"{what}: non-finite output"
     bound = ATOL if strict else np.maximum(ATOL, BF16_REL * np.abs(o_ref) + 1e-4)
+    if v_max is not None:
+        bound = bound + 2.0 ** -8 * float(v_max)
     assert np.all(err <= bound), f"{what}: max abs err {err.max():.3e} (|o_ref| max {np.abs(o_ref).max():.2f})"
     num = np.linalg.norm((o - o_ref).reshape(-1, d), axis=1)
     den = np.linalg.norm(o_ref.reshape(-1, d), axis=1)

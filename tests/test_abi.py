@@ -55,7 +55,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.wmtp_abi_version() == (1 << 16) | 5
+    assert lib.wmtp_abi_version() == (1 << 16) | 6
     for code in range(5):
         assert W.status_string(code).startswith("WMTP_")
     assert "unknown" in W.status_string(99)
@@ -208,7 +208,7 @@ def test_binding_rejects_host_tensors():
         W.draft_attn_full(q, k, k, lens)
 
 
-def _ext(lib, which, **kw):
+def _ext(lib, which, fp8=False, **kw):
     base = dict(q=P, k=P, v=P, lens=P, n_q=P, out=P, lse=None, B=1, q_max=4, Hq=16, Hkv=2, d=128)
     if which == "full":
         base.update(S_max=100)
@@ -216,11 +216,31 @@ def _ext(lib, which, **kw):
         base.update(S_max=100, W=8, sink=4)
     else:
         base.update(W=8, sink=4, R_w=11)
-    base.update(scale=0.1, ws=P, ws_bytes=1 << 30, err=None, stream=None)
+    base.update(scale=0.1)
+    if fp8:
+        base.update(k_scale=0.5, v_scale=2.0)
+    base.update(ws=P, ws_bytes=1 << 30, err=None, stream=None)
     base.update(kw)
-    fn = {"full": lib.wmtp_draft_extend_full, "windowed": lib.wmtp_draft_extend_windowed,
-          "ring": lib.wmtp_ring_extend}[which]
-    return fn(*base.values())
+    name = {"full": "wmtp_draft_extend_full", "windowed": "wmtp_draft_extend_windowed",
+            "ring": "wmtp_ring_extend"}[which] + ("_fp8" if fp8 else "")
+    return getattr(lib, name)(*base.values())
+
+
+@fake_pointers
+@pytest.mark.parametrize("which", ["full", "windowed", "ring"])
+def test_fp8_extend_argument_checks(lib, which):
+    def call(**kw):
+        return _ext(lib, which, fp8=True, **kw)
+    assert call(q_max=0) == W.EINVAL
+    assert call(d=96) == W.EUNSUPPORTED
+    assert call(k=P + 8) == W.EINVAL
+    assert call(ws_bytes=1) == W.EWORKSPACE
+    for bad in (0.0, float("nan")):
+        assert call(k_scale=bad) == W.EINVAL
+        assert call(v_scale=bad) == W.EINVAL
+    if which == "ring":
+        assert call(R_w=10) == W.EINVAL
+    assert call(B=0, q=None, k=None, v=None, lens=None, n_q=None, out=None) == W.OK
 
 
 @fake_pointers

@@ -10,6 +10,8 @@
   and degenerate lengths, non-trivial scales; ring == windowed bitwise;
 * closed-form index encoding through fp8 codes (zero keys, value rows that
   encode their position), windowed at 1M + 7 keys and the ring after wraps;
+* fp8 draft-extend (full, windowed, ring) against the oracle's per-row
+  causal attention over the dequantized cache; ring == windowed bitwise;
 * the million-token draft loop with an fp8 cache: gamma quantising appends,
   windowed attention every step and full attention at the last, against
   the oracle (appended rows taken from the oracle's own quantisation).
@@ -314,3 +316,43 @@ def test_fp8_draft_loop_1m(dev):
             G.say(f"fp8 1M full: max err {e}")
     assert lens.item() == S0 + g
     assert err.item() == 0
+
+
+@pytest.mark.parametrize("d,Hq,Hkv", [(64, 6, 2), (128, 16, 2), (256, 32, 2)])
+@pytest.mark.parametrize("q_max", [3, 8])
+def test_fp8_extend_vs_oracle(dev, d, Hq, Hkv, q_max):
+    W_, sink, ks, vs = 64, 4, 0.75, 1.5
+    rng = np.random.default_rng(3 * d + q_max)
+    lens = [1, q_max, 50, sink + W_, sink + W_ + 2, 700, 4099]
+    n_q = [1] + [int(rng.integers(1, q_max + 1)) for _ in lens[1:]]
+    n_q = [min(n, S) for n, S in zip(n_q, lens)]
+    B, S_max = len(lens), max(lens) + 3
+    G.say(f"fp8 extend d={d} Hq={Hq} Hkv={Hkv} q_max={q_max} lens={lens} n_q={n_q}")
+    q = I.normal_bf16((B, q_max, Hq, d), 41, dev)
+    k8 = I.normal_fp8((B, S_max, Hkv, d), 42, dev)
+    v8 = I.normal_fp8((B, S_max, Hkv, d), 43, dev)
+    lt, nt = G.lens_tensor(lens, dev), G.lens_tensor(n_q, dev)
+    scale = 1.0 / np.sqrt(d)
+    qb = I.bf16_bits(q)
+    v_max = float(np.abs(F.dequantize(v8.cpu().numpy(), vs)).max())
+    err = G.err_word(dev)
+    for variant in ("full", "windowed"):
+        lse = torch.empty(B, q_max, Hq, dtype=torch.float32, device=dev)
+        if variant == "full":
+            out = W.draft_extend_full_fp8(q, k8, v8, lt, ks, vs, n_q=nt, lse=lse, err=err)
+        else:
+            out = W.draft_extend_windowed_fp8(q, k8, v8, lt, W_, sink, ks, vs, n_q=nt, lse=lse, err=err)
+        torch.cuda.synchronize()
+        refs = [A.attend_extend(qb[b], F.DequantizedRows(HostCodes(k8[b]), ks),
+                                F.DequantizedRows(HostCodes(v8[b]), vs), S, n, scale, variant, W_, sink)
+                for b, (S, n) in enumerate(zip(lens, n_q))]
+        G.assert_attn_close(out, np.stack([r[0] for r in refs]), lse, np.stack([r[1] for r in refs]),
+                            what=f"fp8 extend {variant}", strict=False, v_max=v_max)
+    assert err.item() == 0
+    # a ring sized exactly W + q_max - 1 gives the windowed result bit for bit
+    R_w = W_ + q_max - 1
+    kr, vr = _ring_from_dense(k8, lens, sink, R_w), _ring_from_dense(v8, lens, sink, R_w)
+    ow = W.draft_extend_windowed_fp8(q, k8, v8, lt, W_, sink, ks, vs, n_q=nt)
+    orr = W.ring_extend_fp8(q, kr, vr, lt, W_, sink, R_w, ks, vs, n_q=nt)
+    torch.cuda.synchronize()
+    assert torch.equal(orr, ow)
