@@ -380,8 +380,8 @@ int wmtp_ring_attn_fp8(const void* q, const void* k_ring, const void* v_ring, co
  * fp8 draft-extend: the draft-extend calls (several causal new rows per
  * sequence, as wmtp_draft_extend_full / _windowed / wmtp_ring_extend) over
  * an fp8 dense cache or ring, with the per-tensor scales of the fp8 calls.
- * The full-context form computes each new row's items separately (it reads
- * the context once per row; the bf16 form reads it once for all rows).
+ * The full-context form reads the context once for all new rows, as the
+ * bf16 form (at d = 64, once per row).
  */
 int wmtp_draft_extend_full_fp8(const void* q, const void* k, const void* v, const int32_t* lens,
                                const int32_t* n_q, void* out, float* lse, int B, int q_max,

@@ -819,19 +819,26 @@ __device__ bool locate_rows_item(const SplitArgs& a, int item, int& b_out, int& 
   return b_out >= 0;
 }
 
-template <int D>
+// F8: the cache holds E4M3 codes; a step's codes are widened to bf16 when
+// they are stored into LDS (the same layouts as for a bf16 cache), so the
+// compute is the same; the key scale is folded into the logit scale and the
+// value scale into the merge's normalisation.
+template <int D, bool F8>
 __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
   constexpr KeyMap M = KeyMap::Full;
+  using KT = std::conditional_t<F8, uint8_t, uint16_t>;  // one cached K/V element
   constexpr int VEC = D / 16;
   constexpr int SEG = VEC < 8 ? VEC : 8;  // as in split_kernel
   constexpr int NSEG = VEC / SEG;
   constexpr int KCH = D / 32;
-  constexpr int kUnits = D / 8;  // 16-byte units per row of one KV head
+  constexpr int kUnits = D / 8;  // 16-byte bf16 units per row of one KV head (in LDS)
   // K rows are staged key-major at a pitch of kUnits + 2 units: the K
   // operand read (16 lanes take one unit of 16 rows) is then free of bank
   // conflicts on gfx950.
   constexpr int kPitch = kUnits + 2;
-  constexpr int kLoads = kRowStep * kUnits / kRowThreads;  // K (and V) units per thread and step
+  constexpr int kLUnits = F8 ? D / 16 : kUnits;  // 16-byte units per row as loaded (codes or bf16)
+  constexpr int kPer = 16 / static_cast<int>(sizeof(KT));  // elements per loaded unit
+  constexpr int kLoads = kRowStep * kLUnits / kRowThreads;  // K (and V) units per thread and step
   static_assert(kLoads == 1 || kLoads == 2 || kLoads == 4, "a thread's keys must sit in one 4-key run");
   static_assert(kRowStep * kUnits % kRowThreads == 0, "step must tile the workgroup");
   // V is staged transposed, in the order of the PV product's operand: one
@@ -880,15 +887,15 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
 
   const int64_t rs = static_cast<int64_t>(a.Hkv) * D;
   const int64_t seq_off = (static_cast<int64_t>(b) * a.rows * a.Hkv + g) * D;
-  const uint16_t* kbase = static_cast<const uint16_t*>(a.k) + seq_off;
-  const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + seq_off;
+  const KT* kbase = static_cast<const KT*>(a.k) + seq_off;
+  const KT* vbase = static_cast<const KT*>(a.v) + seq_off;
 
-  // Thread tid holds unit tid % kUnits of the kLoads consecutive keys
-  // kLoads * (tid / kUnits) + i of a step (a run inside one 4-key group of a
+  // Thread tid holds loaded unit tid % kLUnits of the kLoads consecutive keys
+  // kLoads * (tid / kLUnits) + i of a step (a run inside one 4-key group of a
   // tile); the lanes of a load instruction cover whole rows of several keys.
   // Keys past j1 read row j0 (masked out of every row's softmax).
-  const int my_unit = tid % kUnits;
-  const int my_key0 = kLoads * (tid / kUnits);
+  const int my_unit = tid % kLUnits;
+  const int my_key0 = kLoads * (tid / kLUnits);
   // Where this thread's keys and value columns land in the transposed V:
   // k' of its first key, and the row of value column 8 my_unit + x.
   const int my_kq = ((my_key0 >> 5) << 5) + ((my_key0 & 15) >> 2) * 8 + ((my_key0 >> 4) & 1) * 4 + (my_key0 & 3);
@@ -899,12 +906,39 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
 #pragma unroll
     for (int i = 0; i < kLoads; ++i) {
       const int j = js + i;
-      const int64_t off = static_cast<int64_t>(j < j1 ? j : j0) * rs + my_unit * 8;
+      const int64_t off = static_cast<int64_t>(j < j1 ? j : j0) * rs + my_unit * kPer;
       rk[i] = stream_load<u32x4>(kbase + off);
       rv[i] = stream_load<u32x4>(vbase + off);
     }
   };
   auto stash = [&](int buf) {
+    if constexpr (F8) {
+      // 16 codes per unit: K widened into two bf16 units of its row; V
+      // column by column (16 my_unit + x) into the transposed rows.
+#pragma unroll
+      for (int i = 0; i < kLoads; ++i) {
+        u32x4* dst = s_k[buf] + (my_key0 + i) * kPitch + 2 * my_unit;
+        dst[0] = fp8x8_to_bf16x8(rk[i][0], rk[i][1]);
+        dst[1] = fp8x8_to_bf16x8(rk[i][2], rk[i][3]);
+      }
+      unsigned char* vt = reinterpret_cast<unsigned char*>(s_vt[buf]) + my_kq * 2;
+      auto widen = [](uint32_t w, int x) {  // codes x & ~1, x | 1 of word w -> two bf16 (x & 2 picks the half)
+        return (x & 2) ? fp8x2_to_bf16x2<true>(w) : fp8x2_to_bf16x2<false>(w);
+      };
+#pragma unroll
+      for (int x = 0; x < 16; ++x) {
+        unsigned char* dst = vt + vt_row(16 * my_unit + x) * (kVTPitch * 16);
+        const uint32_t b0 = widen(rv[0][x >> 2], x);
+        if constexpr (kLoads == 2) {
+          const uint32_t b1 = widen(rv[1][x >> 2], x);
+          *reinterpret_cast<uint32_t*>(dst) = __builtin_amdgcn_perm(b1, b0, (x & 1) ? 0x07060302u : 0x05040100u);
+        } else {
+          static_assert(kLoads == 1, "fp8 runs are one or two keys");
+          *reinterpret_cast<uint16_t*>(dst) = static_cast<uint16_t>(b0 >> (16 * (x & 1)));
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < kLoads; ++i) s_k[buf][(my_key0 + i) * kPitch + my_unit] = rk[i];
     unsigned char* vt = reinterpret_cast<unsigned char*>(s_vt[buf]) + my_kq * 2;
@@ -1211,7 +1245,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
     a.target = L.target; a.chunk_cap = L.chunk_cap;
     a.scale_log2 = L.scale * L.k_scale * kLog2e;
     a.k2 = L.k2; a.v2 = L.v2; a.rows2 = L.rows2; a.dd = L.dd;
-    if constexpr (M == KeyMap::Full && !F8) {
+    if constexpr (M == KeyMap::Full && (!F8 || D >= 128)) {
       if (L.qps > 1) {
         // Items of the multi-row kernel: sequence b owns ceil(n(b) / chunk)
         // of them, n(b) its last row's length; with the chunk of the per-row
@@ -1222,7 +1256,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
         const int64_t coarse = static_cast<int64_t>(L.B) * ((n + L.chunk_cap - 1) / L.chunk_cap);
         const int64_t items = std::min(fine, std::max<int64_t>(static_cast<int64_t>(L.target) + L.B, coarse));
         const dim3 grid(static_cast<unsigned>(std::min<int64_t>(items, L.max_items)) * static_cast<unsigned>(L.Hkv));
-        hipLaunchKernelGGL((rows_split_kernel<D>), grid, dim3(kRowThreads), 0, st, a);
+        hipLaunchKernelGGL((rows_split_kernel<D, F8>), grid, dim3(kRowThreads), 0, st, a);
       } else {
         hipLaunchKernelGGL((split_kernel<D, M, F8>), dim3(static_cast<unsigned>(L.max_items) * L.Hkv),
                            dim3(kThreads), 0, st, a);

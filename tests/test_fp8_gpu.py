@@ -319,7 +319,7 @@ def test_fp8_draft_loop_1m(dev):
 
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(64, 6, 2), (128, 16, 2), (256, 32, 2)])
-@pytest.mark.parametrize("q_max", [3, 8])
+@pytest.mark.parametrize("q_max", [3, 8, 12])
 def test_fp8_extend_vs_oracle(dev, d, Hq, Hkv, q_max):
     W_, sink, ks, vs = 64, 4, 0.75, 1.5
     rng = np.random.default_rng(3 * d + q_max)
