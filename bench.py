@@ -502,7 +502,7 @@ def cpu_baseline(loop, budget_s=20.0):
         A.attend_sequence(qb, kb, vb, S, wl.scale, A.window_mask(S, wl.W, wl.sink))
         nw += 1
     win_s = (time.perf_counter() - t1) / nw
-    try:  # the same windowed step on one thread
+    try:  # the same windowed step, and one full-context step, on one thread
         from threadpoolctl import threadpool_limits
         with threadpool_limits(1):
             t2, nw1 = time.perf_counter(), 0
@@ -510,8 +510,11 @@ def cpu_baseline(loop, budget_s=20.0):
                 A.attend_sequence(qb, kb, vb, S, wl.scale, A.window_mask(S, wl.W, wl.sink))
                 nw1 += 1
             win1_us = round((time.perf_counter() - t2) / nw1 * 1e6, 1)
+            t3 = time.perf_counter()
+            A.attend_sequence(qb, kb, vb, S, wl.scale, None)
+            full1_us = round((time.perf_counter() - t3) * 1e6, 1)
     except ImportError:  # pragma: no cover
-        win1_us = None
+        win1_us = full1_us = None
     # the oracle beside the next rows, at the same shape: draft-extend over
     # gamma + 1 causal rows (windowed) and the windowed step over an fp8 cache
     from oracle import fp8 as F
@@ -539,6 +542,7 @@ def cpu_baseline(loop, budget_s=20.0):
                    f"+ {nw} windowed steps ({win_s * 1e6:.0f} us/step); CPU: {cpu_model()}"),
         "windowed_us_per_step": round(win_s * 1e6, 1),
         "windowed_us_per_step_1_thread": win1_us,
+        "full_us_per_step_1_thread": full1_us,
         "extend_windowed_us": round(ext_us, 1),
         "fp8_windowed_us": round(f8_us, 1),
     }
@@ -790,6 +794,9 @@ def main(argv=None):
         "fused_step": fused,
         "windowed_speedup_vs_full": None if win_us is None else round(us_full_step / win_us, 1),
         "flatness_sweep": sweep,
+        "flatness_sweep_timing": None if not sweep else (
+            "each row: the captured gamma-step loop (append + attention) replayed back to back as a graph "
+            "from that starting length; value and full_us_per_step above time the full step with eager launches"),
         "windowed_hot_cold": caches,
         "windowed_flatness_max_over_min": None if not sweep else round(
             max(r["windowed_us_per_step"] for r in sweep) / min(r["windowed_us_per_step"] for r in sweep), 3),
