@@ -1353,10 +1353,10 @@ SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_
   // most `chunk_max` keys, so that a long single sequence runs in one
   // balanced round and many or variable-length sequences are cut finely
   // enough to pack without a long tail.  Measured on MI355X against two per
-  // CU (the kernel's occupancy): the 1M call 1.4% faster, the 128K call 3%,
-  // an 8-row windowed extend 16%, a batch of 8 rings 13%; fewer items also
-  // mean fewer partials for the merge.  The kernels pick the item
-  // size from the actual lengths; the workspace covers every choice they can
+  // CU (the kernel's occupancy): the 1M call 1.4% faster (fp8 cache: 3%),
+  // the 128K call 3%, an 8-row windowed extend 16%, a batch of 8 rings 13%;
+  // fewer items also mean fewer partials for the merge.  The kernels pick the
+  // item size from the actual lengths; the workspace covers every choice they can
   // make: with per-head target T and chunk in [quantum, cap], the item count
   // is at most min(B*ceil(n/quantum), max(T + B, B*ceil(n/cap))).
   static const int target_env = env_int("WMTP_TARGET_ITEMS", 0);
