@@ -92,6 +92,15 @@ def profiled_traffic(workload):
     return float(m_val.group(1))
 
 
+def full_call_bytes(wl) -> int:
+    """Algorithmic HBM bytes of one full-context attention call at the
+    workload's starting length: every K and V row read once (Hkv * d * 2
+    values of 2 bytes per token), the query read and the output written."""
+    kv_bytes = wl.B * wl.S * wl.Hkv * wl.d * 2 * 2
+    io_bytes = 2 * wl.B * wl.Hq * wl.d * 2
+    return kv_bytes + io_bytes
+
+
 class DraftLoop:
     """Inputs and buffers of the draft loop on one device."""
 
@@ -724,9 +733,7 @@ def main(argv=None):
     for pr in loop.lp:
         pr.copy_(loop.lens0)
     fused_full_us = timed(loop.step_full_fused, args.steps, args.warmup) * 1e6 / g
-    kv_bytes = wl.B * wl.S * wl.Hkv * wl.d * 2 * 2  # K + V rows read per call (S grows by < 0.02%)
-    io_bytes = 2 * wl.B * wl.Hq * wl.d * 2  # q read + out written
-    alg_bytes = kv_bytes + io_bytes
+    alg_bytes = full_call_bytes(wl)  # at the starting length (S grows by < 0.02% over the loop)
     achieved = alg_bytes / (call_us * 1e-6) / 1e9
     log(f"full: {us_full_step:.1f} us/draft step (wall), attention call {call_us:.1f} us (events), "
         f"{achieved:.0f} GB/s")
