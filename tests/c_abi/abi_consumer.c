@@ -1,0 +1,165 @@
+/*
+ * A plain C consumer of libwmtp's C ABI: device buffers from the HIP
+ * runtime, the hot path's calls on the default stream, no torch.  It checks
+ * closed forms that hold at any length:
+ *
+ *   K = 0 makes every selected logit 0, so the softmax over the selected keys
+ *   is uniform; with V = 1 the output is exactly 1 and the log-sum-exp is the
+ *   log of the number of selected keys: ln S (full context) and
+ *   ln min(S, sink + W) (windowed; ring after appending S rows).
+ *
+ * and that malformed arguments return their status before anything is
+ * enqueued.  Prints one line per check; exit status 0 when all hold.
+ */
+#include <hip/hip_runtime_api.h>
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+
+#include "wmtp.h"
+
+#define B 2
+#define HQ 16
+#define HKV 2
+#define D 128
+#define S_MAX 70000
+#define W 512
+#define SINK 4
+#define R_W 512
+#define N_MAX 600
+
+static int failures = 0;
+
+static void check(int ok, const char* what) {
+  printf("%s %s\n", ok ? "ok  " : "FAIL", what);
+  if (!ok) failures++;
+}
+
+static void* dev_alloc(size_t bytes) {
+  void* p = NULL;
+  if (hipMalloc(&p, bytes) != hipSuccess) {
+    printf("FAIL hipMalloc(%zu)\n", bytes);
+    exit(2);
+  }
+  return p;
+}
+
+static void hip_ok(hipError_t e, const char* what) {
+  if (e != hipSuccess) {
+    printf("FAIL %s: %s\n", what, hipGetErrorString(e));
+    exit(2);
+  }
+}
+
+/* Output all ones (bf16 0x3F80) and lse[b, h] == ln(n_sel[b]). */
+static void check_uniform(const void* out, const float* lse, const int n_sel[B], const char* what) {
+  static uint16_t o[B * HQ * D];
+  float l[B * HQ];
+  hip_ok(hipMemcpy(o, out, sizeof(o), hipMemcpyDeviceToHost), "copy out");
+  hip_ok(hipMemcpy(l, lse, sizeof(l), hipMemcpyDeviceToHost), "copy lse");
+  int ones = 1;
+  for (int i = 0; i < B * HQ * D; ++i) ones &= o[i] == 0x3F80;
+  double worst = 0.0;
+  for (int b = 0; b < B; ++b)
+    for (int h = 0; h < HQ; ++h) {
+      const double e = fabs((double)l[b * HQ + h] - log((double)n_sel[b]));
+      if (e > worst) worst = e;
+    }
+  char msg[160];
+  snprintf(msg, sizeof(msg), "%s: output == 1 everywhere", what);
+  check(ones, msg);
+  snprintf(msg, sizeof(msg), "%s: lse == ln(selected keys) (worst error %.2e)", what, worst);
+  check(worst <= 1e-5, msg);
+}
+
+int main(void) {
+  check(wmtp_abi_version() == WMTP_ABI_VERSION, "library ABI version matches the header");
+
+  const size_t row = (size_t)HKV * D * 2; /* bytes of one K or V row */
+  const int lens_h[B] = {S_MAX, 300};
+  void* q = dev_alloc((size_t)B * HQ * D * 2);
+  void* k = dev_alloc((size_t)B * S_MAX * row);
+  void* v = dev_alloc((size_t)B * S_MAX * row);
+  void* out = dev_alloc((size_t)B * HQ * D * 2);
+  float* lse = (float*)dev_alloc((size_t)B * HQ * sizeof(float));
+  int32_t* lens = (int32_t*)dev_alloc(sizeof(lens_h));
+  int32_t* err = (int32_t*)dev_alloc(sizeof(int32_t));
+  hip_ok(hipMemset(q, 0, (size_t)B * HQ * D * 2), "q = 0");
+  hip_ok(hipMemset(k, 0, (size_t)B * S_MAX * row), "K = 0");
+  hip_ok(hipMemsetD16((hipDeviceptr_t)v, 0x3F80, (size_t)B * S_MAX * row / 2), "V = 1");
+  hip_ok(hipMemcpy(lens, lens_h, sizeof(lens_h), hipMemcpyHostToDevice), "lens");
+  hip_ok(hipMemset(err, 0, sizeof(int32_t)), "err = 0");
+
+  size_t ws_bytes = wmtp_workspace_bytes(WMTP_VARIANT_FULL, B, HQ, HKV, D, S_MAX, W, SINK);
+  const size_t ws_win = wmtp_workspace_bytes(WMTP_VARIANT_WINDOWED, B, HQ, HKV, D, S_MAX, W, SINK);
+  const size_t ws_ring = wmtp_workspace_bytes(WMTP_VARIANT_RING, B, HQ, HKV, D, SINK + R_W, W, SINK);
+  check(ws_bytes > 0 && ws_win > 0 && ws_ring > 0, "workspace sizes are positive");
+  if (ws_win > ws_bytes) ws_bytes = ws_win;
+  if (ws_ring > ws_bytes) ws_bytes = ws_ring;
+  void* ws = dev_alloc(ws_bytes);
+  const float scale = 1.0f / sqrtf((float)D);
+
+  /* Full context: every key. */
+  int st = wmtp_draft_attn_full(q, k, v, lens, out, lse, B, HQ, HKV, D, S_MAX, scale, ws, ws_bytes, err, NULL);
+  check(st == WMTP_OK, "wmtp_draft_attn_full returns OK");
+  hip_ok(hipDeviceSynchronize(), "full");
+  const int sel_full[B] = {S_MAX, 300};
+  check_uniform(out, lse, sel_full, "full context");
+
+  /* Windowed: the sink and the last W keys (all 300 keys of the short one). */
+  st = wmtp_draft_attn_windowed(q, k, v, lens, out, lse, B, HQ, HKV, D, S_MAX, W, SINK, scale, ws,
+                                ws_bytes, err, NULL);
+  check(st == WMTP_OK, "wmtp_draft_attn_windowed returns OK");
+  hip_ok(hipDeviceSynchronize(), "windowed");
+  const int sel_win[B] = {SINK + W, 300};
+  check_uniform(out, lse, sel_win, "windowed");
+
+  /* Ring: append 600 and 300 rows (K = 0, V = 1) to empty rings, attend. */
+  const int n_new_h[B] = {N_MAX, 300};
+  const int zero_h[B] = {0, 0};
+  void* k_ring = dev_alloc((size_t)B * (SINK + R_W) * row);
+  void* v_ring = dev_alloc((size_t)B * (SINK + R_W) * row);
+  void* k_new = dev_alloc((size_t)B * N_MAX * row);
+  void* v_new = dev_alloc((size_t)B * N_MAX * row);
+  int32_t* n_new = (int32_t*)dev_alloc(sizeof(n_new_h));
+  int32_t* lens_ring = (int32_t*)dev_alloc(sizeof(zero_h));
+  hip_ok(hipMemset(k_new, 0, (size_t)B * N_MAX * row), "k_new = 0");
+  hip_ok(hipMemsetD16((hipDeviceptr_t)v_new, 0x3F80, (size_t)B * N_MAX * row / 2), "v_new = 1");
+  hip_ok(hipMemcpy(n_new, n_new_h, sizeof(n_new_h), hipMemcpyHostToDevice), "n_new");
+  hip_ok(hipMemcpy(lens_ring, zero_h, sizeof(zero_h), hipMemcpyHostToDevice), "ring lens");
+  st = wmtp_ring_append(k_ring, v_ring, k_new, v_new, n_new, lens_ring, B, HKV, D, SINK, R_W, N_MAX, err, NULL);
+  check(st == WMTP_OK, "wmtp_ring_append returns OK");
+  st = wmtp_ring_attn(q, k_ring, v_ring, lens_ring, out, lse, B, HQ, HKV, D, W, SINK, R_W, scale, ws,
+                      ws_bytes, err, NULL);
+  check(st == WMTP_OK, "wmtp_ring_attn returns OK");
+  hip_ok(hipDeviceSynchronize(), "ring");
+  int lens_after[B];
+  hip_ok(hipMemcpy(lens_after, lens_ring, sizeof(lens_after), hipMemcpyDeviceToHost), "ring lens back");
+  check(lens_after[0] == N_MAX && lens_after[1] == 300, "ring lengths advanced by n_new on the device");
+  const int sel_ring[B] = {SINK + W, 300};
+  check_uniform(out, lse, sel_ring, "ring");
+
+  int32_t err_h = -1;
+  hip_ok(hipMemcpy(&err_h, err, sizeof(err_h), hipMemcpyDeviceToHost), "err back");
+  check(err_h == 0, "no device-side error bits");
+
+  /* Host-side argument errors: returned before anything is enqueued. */
+  st = wmtp_draft_attn_windowed(q, k, v, lens, out, lse, B, HQ, HKV, D, S_MAX, 0, SINK, scale, ws,
+                                ws_bytes, err, NULL);
+  check(st == WMTP_EINVAL, "W = 0 -> WMTP_EINVAL");
+  st = wmtp_draft_attn_full(q, k, v, lens, out, lse, B, HQ, HKV, 96, S_MAX, scale, ws, ws_bytes, err, NULL);
+  check(st == WMTP_EUNSUPPORTED, "d = 96 -> WMTP_EUNSUPPORTED");
+  st = wmtp_draft_attn_full(q, k, v, lens, out, lse, B, HQ, HKV, D, S_MAX, scale, ws, 0, err, NULL);
+  check(st == WMTP_EWORKSPACE, "no workspace -> WMTP_EWORKSPACE");
+  st = wmtp_draft_attn_full(q, k, v, lens, out, lse, B, 12, 5, D, S_MAX, scale, ws, ws_bytes, err, NULL);
+  check(st == WMTP_EINVAL, "Hq not a multiple of Hkv -> WMTP_EINVAL");
+  check(wmtp_status_string(WMTP_EWORKSPACE) != NULL && wmtp_status_string(WMTP_OK) != NULL,
+        "status strings");
+
+  hip_ok(hipDeviceSynchronize(), "final");
+  hipFree(q); hipFree(k); hipFree(v); hipFree(out); hipFree(lse); hipFree(lens); hipFree(err); hipFree(ws);
+  hipFree(k_ring); hipFree(v_ring); hipFree(k_new); hipFree(v_new); hipFree(n_new); hipFree(lens_ring);
+  printf("%d failure(s)\n", failures);
+  return failures == 0 ? 0 : 1;
+}
