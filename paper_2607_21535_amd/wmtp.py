@@ -178,6 +178,11 @@ class WmtpError(RuntimeError):
         super().__init__(f"{where}: {status_string(status)} (status {status})")
 
 
+# The version of include/wmtp.h these signatures follow, (major << 16) | minor:
+# a library of another major version, or an older minor one, is refused.
+ABI_VERSION = (1 << 16) | 6
+
+
 def lib_path() -> str:
     return os.environ.get("WMTP_LIB", os.path.join(_HERE, "libwmtp.so"))
 
@@ -190,6 +195,12 @@ def load_library():
         if not os.path.exists(path):
             raise OSError(f"{path} not found: build it with `python -m paper_2607_21535_amd.build`")
         lib = ctypes.CDLL(path)
+        lib.wmtp_abi_version.restype = ctypes.c_int
+        lib.wmtp_abi_version.argtypes = []
+        v = int(lib.wmtp_abi_version())
+        if v >> 16 != ABI_VERSION >> 16 or (v & 0xFFFF) < (ABI_VERSION & 0xFFFF):
+            raise OSError(f"{path} has ABI {v >> 16}.{v & 0xFFFF}; this binding needs "
+                          f"{ABI_VERSION >> 16}.{ABI_VERSION & 0xFFFF} (rebuild the library)")
         for name, (res, args) in _SIGNATURES.items():
             fn = getattr(lib, name)
             fn.restype = res

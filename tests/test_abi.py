@@ -56,6 +56,10 @@ def test_library_exports_every_declared_symbol(lib):
 
 def test_abi_version_and_status_strings(lib):
     assert lib.wmtp_abi_version() == (1 << 16) | 6
+    # the header, the library and the binding's signatures agree
+    with open(os.path.join(ROOT, "include", "wmtp.h")) as f:
+        m = re.search(r"#define WMTP_ABI_VERSION \(\(1 << 16\) \| (\d+)\)", f.read())
+    assert m is not None and W.ABI_VERSION == (1 << 16) | int(m.group(1)) == lib.wmtp_abi_version()
     for code in range(5):
         assert W.status_string(code).startswith("WMTP_")
     assert "unknown" in W.status_string(99)
