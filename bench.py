@@ -362,10 +362,70 @@ def read_ceiling_gbps(loop, reps=7):
 def extras(loop, fp8=True):
     """Context measurements at the 1M shape: draft-extend over gamma+1 new
     rows, the paged pool (page size 1) and, optionally, the fp8 cache."""
-    out = {"extend": extend_figures(loop), "paged": paged_figures(loop)}
+    out = {"extend": extend_figures(loop), "paged": paged_figures(loop), "spec": spec_figures(loop)}
     if fp8:
         out["fp8"] = fp8_figures(loop)
     return out
+
+
+def spec_figures(loop, width=4):
+    """Speculative draft rows at the 1M shape (Section 7 tree speculation),
+    each round captured in a graph and replayed.  Tree: `width` candidates
+    over a ring of sink + W + d slots (d = gamma + 1) and private runs of d
+    rows for candidates 1 .. width-1; a round is gamma draft steps (every
+    candidate's row appended, then the windowed attention of all candidates
+    in one call) and the depth reset.  Chain: gamma steps of one appended row
+    and ring attention, then the rollback of the rejected rows (half of
+    them).  The committed length stays at the workload's 1M: windowed cost
+    does not depend on it."""
+    wl, dev = loop.wl, loop.dev
+    B, dd = 1, wl.gamma + 1
+    R_w = wl.W + dd
+    slots = wl.sink + R_w
+    seed = I.stream_seed(wl.seed, I.STREAM_KNEW, 77)
+    kr = I.normal_bf16((B, slots, wl.Hkv, wl.d), seed, dev)
+    vr = I.normal_bf16((B, slots, wl.Hkv, wl.d), seed + 1, dev)
+    kb = I.normal_bf16((B, (width - 1) * dd, wl.Hkv, wl.d), seed + 2, dev)
+    vb = I.normal_bf16((B, (width - 1) * dd, wl.Hkv, wl.d), seed + 3, dev)
+    kn = I.normal_bf16((B, width, wl.Hkv, wl.d), seed + 4, dev)
+    vn = I.normal_bf16((B, width, wl.Hkv, wl.d), seed + 5, dev)
+    q = I.normal_bf16((B, width, wl.Hq, wl.d), I.stream_seed(wl.seed, I.STREAM_Q, 77), dev)
+    lens = torch.full((B,), wl.S, dtype=torch.int32, device=dev)
+    depth = torch.zeros((B,), dtype=torch.int32, device=dev)
+    out = torch.empty_like(q)
+    ws = torch.empty(W.workspace_bytes(W.VARIANT_TREE, B * width, wl.Hq, wl.Hkv, wl.d, 0, wl.W, wl.sink),
+                     dtype=torch.uint8, device=dev)
+
+    def tree_round():
+        for _ in range(wl.gamma):
+            W.tree_append(kr, vr, kb, vb, kn, vn, lens, depth, wl.W, wl.sink, R_w, dd)
+            W.tree_attn(q, kr, vr, kb, vb, lens, depth, wl.W, wl.sink, R_w, dd, out=out, scale=wl.scale, ws=ws)
+        W.tree_reset(depth)
+
+    # chain: one candidate in the ring itself, lens advancing with each row
+    q1 = q[:, 0].contiguous()
+    out1 = torch.empty_like(q1)
+    ones = torch.ones((B,), dtype=torch.int32, device=dev)
+    drop = torch.full((B,), wl.gamma // 2, dtype=torch.int32, device=dev)
+    ws1 = torch.empty(W.workspace_bytes(W.VARIANT_RING, B, wl.Hq, wl.Hkv, wl.d, slots, wl.W, wl.sink),
+                      dtype=torch.uint8, device=dev)
+    kn1, vn1 = kn[:, :1].contiguous(), vn[:, :1].contiguous()
+    lens_c = lens.clone()
+
+    def chain_round():
+        for _ in range(wl.gamma):
+            W.ring_append(kr, vr, kn1, vn1, ones, lens_c, wl.sink, R_w)
+            W.ring_attn(q1, kr, vr, lens_c, wl.W, wl.sink, R_w, out=out1, scale=wl.scale, ws=ws1)
+        W.ring_rollback(lens_c, drop)
+
+    tree_us = graph_us(tree_round, calls=5)
+    chain_us = graph_us(chain_round, calls=5)
+    res = {"width": width, "depth_max": dd, "ring_slots": slots, "steps_per_round": wl.gamma,
+           "tree_round_us": round(tree_us, 2), "tree_step_us": round(tree_us / wl.gamma, 2),
+           "chain_round_us": round(chain_us, 2), "chain_step_us": round(chain_us / wl.gamma, 2),
+           "rolled_back_rows_per_round": wl.gamma // 2}
+    log(f"speculation: tree of {width} {res['tree_step_us']} us/step, chain {res['chain_step_us']} us/step")
+    return res
 
 
 def extend_figures(loop):
