@@ -1267,10 +1267,11 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
     }
   }
   // The merge shape: 1024-thread workgroups on 64-wide slices when a row has
-  // many items and their grid fits one round of the device (two per CU);
-  // else one 256-thread workgroup per row and head.
+  // many items and their grid fits one workgroup per CU; else one 256-thread
+  // workgroup per row and head (a tree of 4 speculation candidates at
+  // Hq = 32, 512 wide workgroups: 22.4 -> 20.8 us per draft step).
   const int64_t NV = static_cast<int64_t>(L.B) * L.qps;
-  const bool wide = L.max_items >= 32 * NV && NV * L.Hq * (D / 64) <= 2 * static_cast<int64_t>(device_cus());
+  const bool wide = L.max_items >= 32 * NV && NV * L.Hq * (D / 64) <= static_cast<int64_t>(device_cus());
   MergeArgs m;
   m.lens = L.lens; m.n_q = L.n_q; m.qps = L.qps; m.pm = L.pm; m.pl = L.pl; m.pz = L.pz; m.po = L.po;
   m.out = L.out; m.lse = L.lse; m.err = L.err;
