@@ -418,13 +418,30 @@ def spec_figures(loop, width=4):
             W.ring_attn(q1, kr, vr, lens_c, wl.W, wl.sink, R_w, out=out1, scale=wl.scale, ws=ws1)
         W.ring_rollback(lens_c, drop)
 
+    # the same chain with each step's append and attention in one call
+    # (wmtp_ring_step; old and new lengths in two arrays, alternating)
+    lens_a, lens_b = lens.clone(), lens.clone()
+
+    def chain_round_fused():
+        src, dst = lens_a, lens_b
+        for _ in range(wl.gamma):
+            W.ring_step(q1, kr, vr, kn1, vn1, ones, src, dst, wl.W, wl.sink, R_w, out=out1, scale=wl.scale,
+                        ws=ws1)
+            src, dst = dst, src
+        W.ring_rollback(src, drop)
+        if src is not lens_a:
+            lens_a.copy_(src)
+
     tree_us = graph_us(tree_round, calls=5)
     chain_us = graph_us(chain_round, calls=5)
+    chain_fused_us = graph_us(chain_round_fused, calls=5)
     res = {"width": width, "depth_max": dd, "ring_slots": slots, "steps_per_round": wl.gamma,
            "tree_round_us": round(tree_us, 2), "tree_step_us": round(tree_us / wl.gamma, 2),
            "chain_round_us": round(chain_us, 2), "chain_step_us": round(chain_us / wl.gamma, 2),
+           "chain_fused_step_us": round(chain_fused_us / wl.gamma, 2),
            "rolled_back_rows_per_round": wl.gamma // 2}
-    log(f"speculation: tree of {width} {res['tree_step_us']} us/step, chain {res['chain_step_us']} us/step")
+    log(f"speculation: tree of {width} {res['tree_step_us']} us/step, chain {res['chain_step_us']} us/step "
+        f"({res['chain_fused_step_us']} us/step with the fused ring step)")
     return res
 
 
