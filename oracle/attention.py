@@ -26,7 +26,7 @@ Everything else is the textbook single-query softmax attention, written out:
     m   = max_p z_p,  w_p = exp(z_p - m),  l = sum_p w_p
     o_h = sum_p (w_p / l) v_p,  lse_h = m + ln l
 
-Readings where the paper is silent (each is listed in the design doc as well):
+Readings where the paper is silent:
   * GQA grouping: query head h uses KV head g = h // G with G = Hq / Hkv
     (consecutive grouping).
   * W counts only the recent window, not the sink: |keep| = n_sink + W.

@@ -7,7 +7,7 @@ What the paper fixes (Windowed-MTP, Section 7 "Robustness to KV-cache
 quantization"): the draft may read an fp8 KV cache; windowing changes which
 entries are read, the KV dtype only the bytes per entry, and the attention
 result is the same masked-softmax attention over the dequantized entries.
-The paper does not spell out the format.  Readings (listed in the design doc too):
+The paper does not spell out the format.  Readings:
 
   * Format: OCP 8-bit floating point, E4M3 variant ("e4m3fn"): 1 sign bit,
     4 exponent bits with bias 7, 3 mantissa bits; exponent field 0 encodes

@@ -11,8 +11,8 @@ Paper facts this follows (Windowed-MTP):
     ring_base(r) plus a slot derived from the logical position, with modulus
     n_sink + W + d.
 
-Reading of that comment (the paper gives no further detail; listed in
-DESIGN.md): the sink rows are pinned to slots [0, sink) and never overwritten;
+Reading of that comment (the paper gives no further detail): the sink rows
+are pinned to slots [0, sink) and never overwritten;
 the other positions cycle through a circular region of R_w slots that follows
 the sink, R_w = W + d in the paper's chain setting (any R_w >= W keeps the
 whole window resident):

@@ -14,7 +14,7 @@ Paper facts this follows (Windowed-MTP):
   * Section 3 (per-step latency model): each draft step writes its token's
     K/V row, then attends.
 
-Readings (the paper gives no more detail; listed in the design doc):
+Readings (the paper gives no more detail):
   * Per request the state is the committed length S (rows the target has
     accepted) and the speculative depth i (draft steps since the last
     verify, 0 <= i <= d).  Candidate b's sequence is the committed rows
