@@ -6,7 +6,10 @@
  *   K = 0 makes every selected logit 0, so the softmax over the selected keys
  *   is uniform; with V = 1 the output is exactly 1 and the log-sum-exp is the
  *   log of the number of selected keys: ln S (full context) and
- *   ln min(S, sink + W) (windowed; ring after appending S rows).
+ *   ln min(S, sink + W) (windowed; ring after appending S rows; the paged
+ *   pool through an identity token table; a draft-extend row t of n new
+ *   rows at its own length S - n + t + 1, padding rows 0 and -inf; an fp8
+ *   cache of codes 0 and 1.0 with value scale 2 gives exactly 2).
  *
  * and that malformed arguments return their status before anything is
  * enqueued.  Prints one line per check; exit status 0 when all hold.
@@ -52,25 +55,41 @@ static void hip_ok(hipError_t e, const char* what) {
   }
 }
 
-/* Output all ones (bf16 0x3F80) and lse[b, h] == ln(n_sel[b]). */
-static void check_uniform(const void* out, const float* lse, const int n_sel[B], const char* what) {
-  static uint16_t o[B * HQ * D];
-  float l[B * HQ];
-  hip_ok(hipMemcpy(o, out, sizeof(o), hipMemcpyDeviceToHost), "copy out");
-  hip_ok(hipMemcpy(l, lse, sizeof(l), hipMemcpyDeviceToHost), "copy lse");
-  int ones = 1;
-  for (int i = 0; i < B * HQ * D; ++i) ones &= o[i] == 0x3F80;
+#define QMAX 3
+
+/* Query rows r < nrows ([nrows, HQ, D] out, [nrows, HQ] lse): the output is
+ * `value` (a bf16 word) and lse == ln(n_sel[r]) where n_sel[r] > 0; a row
+ * with no keys gives 0 and -inf. */
+static void check_rows(const void* out, const float* lse, const int* n_sel, int nrows, uint16_t value,
+                       const char* what) {
+  static uint16_t o[B * QMAX * HQ * D];
+  static float l[B * QMAX * HQ];
+  hip_ok(hipMemcpy(o, out, (size_t)nrows * HQ * D * 2, hipMemcpyDeviceToHost), "copy out");
+  hip_ok(hipMemcpy(l, lse, (size_t)nrows * HQ * sizeof(float), hipMemcpyDeviceToHost), "copy lse");
+  int values = 1, empty = 1;
   double worst = 0.0;
-  for (int b = 0; b < B; ++b)
+  for (int r = 0; r < nrows; ++r) {
+    const uint16_t want = n_sel[r] > 0 ? value : 0;
+    for (int i = 0; i < HQ * D; ++i) values &= o[(size_t)r * HQ * D + i] == want;
     for (int h = 0; h < HQ; ++h) {
-      const double e = fabs((double)l[b * HQ + h] - log((double)n_sel[b]));
-      if (e > worst) worst = e;
+      const float x = l[r * HQ + h];
+      if (n_sel[r] > 0) {
+        const double e = fabs((double)x - log((double)n_sel[r]));
+        if (e > worst) worst = e;
+      } else {
+        empty &= isinf(x) && x < 0.0f;
+      }
     }
-  char msg[160];
-  snprintf(msg, sizeof(msg), "%s: output == 1 everywhere", what);
-  check(ones, msg);
-  snprintf(msg, sizeof(msg), "%s: lse == ln(selected keys) (worst error %.2e)", what, worst);
-  check(worst <= 1e-5, msg);
+  }
+  char msg[200];
+  snprintf(msg, sizeof(msg), "%s: output == 0x%04x at every kept row (0 where none)", what, (unsigned)value);
+  check(values, msg);
+  snprintf(msg, sizeof(msg), "%s: lse == ln(selected keys) (worst error %.2e), -inf without keys", what, worst);
+  check(worst <= 1e-5 && empty, msg);
+}
+
+static void check_uniform(const void* out, const float* lse, const int n_sel[B], const char* what) {
+  check_rows(out, lse, n_sel, B, 0x3F80, what);
 }
 
 int main(void) {
@@ -94,9 +113,13 @@ int main(void) {
   size_t ws_bytes = wmtp_workspace_bytes(WMTP_VARIANT_FULL, B, HQ, HKV, D, S_MAX, W, SINK);
   const size_t ws_win = wmtp_workspace_bytes(WMTP_VARIANT_WINDOWED, B, HQ, HKV, D, S_MAX, W, SINK);
   const size_t ws_ring = wmtp_workspace_bytes(WMTP_VARIANT_RING, B, HQ, HKV, D, SINK + R_W, W, SINK);
-  check(ws_bytes > 0 && ws_win > 0 && ws_ring > 0, "workspace sizes are positive");
+  const size_t ws_ext = wmtp_workspace_bytes(WMTP_VARIANT_WINDOWED, B * QMAX, HQ, HKV, D, S_MAX, W, SINK);
+  const size_t ws_pool = wmtp_workspace_bytes(WMTP_VARIANT_PAGED_WINDOWED, B, HQ, HKV, D, S_MAX, W, SINK);
+  check(ws_bytes > 0 && ws_win > 0 && ws_ring > 0 && ws_ext > 0 && ws_pool > 0, "workspace sizes are positive");
   if (ws_win > ws_bytes) ws_bytes = ws_win;
   if (ws_ring > ws_bytes) ws_bytes = ws_ring;
+  if (ws_ext > ws_bytes) ws_bytes = ws_ext;
+  if (ws_pool > ws_bytes) ws_bytes = ws_pool;
   void* ws = dev_alloc(ws_bytes);
   const float scale = 1.0f / sqrtf((float)D);
 
@@ -140,6 +163,61 @@ int main(void) {
   const int sel_ring[B] = {SINK + W, 300};
   check_uniform(out, lse, sel_ring, "ring");
 
+  /* Paged pool: the dense cache's rows as one pool, req_to_token[b][p] = b S_MAX + p. */
+  int32_t* table_h = (int32_t*)malloc(sizeof(int32_t) * B * S_MAX);
+  if (table_h == NULL) return 2;
+  for (int b = 0; b < B; ++b)
+    for (int p = 0; p < S_MAX; ++p) table_h[b * S_MAX + p] = b * S_MAX + p;
+  int32_t* table = (int32_t*)dev_alloc(sizeof(int32_t) * B * S_MAX);
+  hip_ok(hipMemcpy(table, table_h, sizeof(int32_t) * B * S_MAX, hipMemcpyHostToDevice), "table");
+  free(table_h);
+  st = wmtp_paged_attn_windowed(q, k, v, table, lens, out, lse, B, HQ, HKV, D, (int64_t)B * S_MAX, S_MAX, W, SINK,
+                                scale, ws, ws_bytes, err, NULL);
+  check(st == WMTP_OK, "wmtp_paged_attn_windowed returns OK");
+  hip_ok(hipDeviceSynchronize(), "paged");
+  check_uniform(out, lse, sel_win, "paged windowed");
+
+  /* Windowed draft-extend: 3 and 2 new rows (q_max 3), the third row of the
+   * short sequence is padding. */
+  const int n_q_h[B] = {3, 2};
+  int sel_ext[B * QMAX];
+  for (int b = 0; b < B; ++b)
+    for (int t = 0; t < QMAX; ++t) {
+      const int L = t < n_q_h[b] ? lens_h[b] - n_q_h[b] + t + 1 : 0;
+      sel_ext[b * QMAX + t] = L > SINK + W ? SINK + W : L;
+    }
+  void* q3 = dev_alloc((size_t)B * QMAX * HQ * D * 2);
+  void* out3 = dev_alloc((size_t)B * QMAX * HQ * D * 2);
+  float* lse3 = (float*)dev_alloc((size_t)B * QMAX * HQ * sizeof(float));
+  int32_t* n_q = (int32_t*)dev_alloc(sizeof(n_q_h));
+  hip_ok(hipMemset(q3, 0, (size_t)B * QMAX * HQ * D * 2), "q3 = 0");
+  hip_ok(hipMemcpy(n_q, n_q_h, sizeof(n_q_h), hipMemcpyHostToDevice), "n_q");
+  st = wmtp_draft_extend_windowed(q3, k, v, lens, n_q, out3, lse3, B, QMAX, HQ, HKV, D, S_MAX, W, SINK, scale, ws,
+                                  ws_bytes, err, NULL);
+  check(st == WMTP_OK, "wmtp_draft_extend_windowed returns OK");
+  hip_ok(hipDeviceSynchronize(), "extend");
+  check_rows(out3, lse3, sel_ext, B * QMAX, 0x3F80, "windowed extend");
+
+  /* fp8 cache: K codes 0, V codes 0x38 (E4M3 1.0), value scale 2 -> output 2. */
+  const size_t row8 = (size_t)HKV * D;
+  void* k8 = dev_alloc((size_t)B * S_MAX * row8);
+  void* v8 = dev_alloc((size_t)B * S_MAX * row8);
+  hip_ok(hipMemset(k8, 0, (size_t)B * S_MAX * row8), "K codes = 0");
+  hip_ok(hipMemset(v8, 0x38, (size_t)B * S_MAX * row8), "V codes = 1.0");
+  st = wmtp_draft_attn_full_fp8(q, k8, v8, lens, out, lse, B, HQ, HKV, D, S_MAX, scale, 0.5f, 2.0f, ws, ws_bytes,
+                                err, NULL);
+  check(st == WMTP_OK, "wmtp_draft_attn_full_fp8 returns OK");
+  hip_ok(hipDeviceSynchronize(), "fp8 full");
+  check_rows(out, lse, sel_full, B, 0x4000, "fp8 full context");
+  st = wmtp_draft_attn_windowed_fp8(q, k8, v8, lens, out, lse, B, HQ, HKV, D, S_MAX, W, SINK, scale, 0.5f, 2.0f, ws,
+                                    ws_bytes, err, NULL);
+  check(st == WMTP_OK, "wmtp_draft_attn_windowed_fp8 returns OK");
+  hip_ok(hipDeviceSynchronize(), "fp8 windowed");
+  check_rows(out, lse, sel_win, B, 0x4000, "fp8 windowed");
+  st = wmtp_draft_attn_full_fp8(q, k8, v8, lens, out, lse, B, HQ, HKV, D, S_MAX, scale, 0.5f, -1.0f, ws, ws_bytes,
+                                err, NULL);
+  check(st == WMTP_EINVAL, "fp8 value scale -1 -> WMTP_EINVAL");
+
   int32_t err_h = -1;
   hip_ok(hipMemcpy(&err_h, err, sizeof(err_h), hipMemcpyDeviceToHost), "err back");
   check(err_h == 0, "no device-side error bits");
@@ -160,6 +238,7 @@ int main(void) {
   hip_ok(hipDeviceSynchronize(), "final");
   hipFree(q); hipFree(k); hipFree(v); hipFree(out); hipFree(lse); hipFree(lens); hipFree(err); hipFree(ws);
   hipFree(k_ring); hipFree(v_ring); hipFree(k_new); hipFree(v_new); hipFree(n_new); hipFree(lens_ring);
+  hipFree(table); hipFree(q3); hipFree(out3); hipFree(lse3); hipFree(n_q); hipFree(k8); hipFree(v8);
   printf("%d failure(s)\n", failures);
   return failures == 0 ? 0 : 1;
 }
