@@ -56,6 +56,8 @@ static void hip_ok(hipError_t e, const char* what) {
 }
 
 #define QMAX 3
+#define WIDTH 2 /* speculation candidates */
+#define DD 4    /* largest speculative depth */
 
 /* Query rows r < nrows ([nrows, HQ, D] out, [nrows, HQ] lse): the output is
  * `value` (a bf16 word) and lse == ln(n_sel[r]) where n_sel[r] > 0; a row
@@ -115,11 +117,13 @@ int main(void) {
   const size_t ws_ring = wmtp_workspace_bytes(WMTP_VARIANT_RING, B, HQ, HKV, D, SINK + R_W, W, SINK);
   const size_t ws_ext = wmtp_workspace_bytes(WMTP_VARIANT_WINDOWED, B * QMAX, HQ, HKV, D, S_MAX, W, SINK);
   const size_t ws_pool = wmtp_workspace_bytes(WMTP_VARIANT_PAGED_WINDOWED, B, HQ, HKV, D, S_MAX, W, SINK);
+  const size_t ws_tree = wmtp_workspace_bytes(WMTP_VARIANT_TREE, B * WIDTH, HQ, HKV, D, 0, W, SINK);
   check(ws_bytes > 0 && ws_win > 0 && ws_ring > 0 && ws_ext > 0 && ws_pool > 0, "workspace sizes are positive");
   if (ws_win > ws_bytes) ws_bytes = ws_win;
   if (ws_ring > ws_bytes) ws_bytes = ws_ring;
   if (ws_ext > ws_bytes) ws_bytes = ws_ext;
   if (ws_pool > ws_bytes) ws_bytes = ws_pool;
+  if (ws_tree > ws_bytes) ws_bytes = ws_tree;
   void* ws = dev_alloc(ws_bytes);
   const float scale = 1.0f / sqrtf((float)D);
 
@@ -218,6 +222,71 @@ int main(void) {
                                 err, NULL);
   check(st == WMTP_EINVAL, "fp8 value scale -1 -> WMTP_EINVAL");
 
+  /* Speculation: a ring of sink + W + DD slots holding 600 and 300 committed
+   * rows, WIDTH candidates (candidate 1 in a private run), one draft step:
+   * every candidate sees min(S + 1, sink + W) keys.  Then the depth reset
+   * and a chain rollback of 5 and 7 rows. */
+  const int R_WT = W + DD;
+  void* kt = dev_alloc((size_t)B * (SINK + R_WT) * row);
+  void* vt = dev_alloc((size_t)B * (SINK + R_WT) * row);
+  void* kbr = dev_alloc((size_t)B * (WIDTH - 1) * DD * row);
+  void* vbr = dev_alloc((size_t)B * (WIDTH - 1) * DD * row);
+  void* q_t = dev_alloc((size_t)B * WIDTH * HQ * D * 2);
+  void* out_t = dev_alloc((size_t)B * WIDTH * HQ * D * 2);
+  float* lse_t = (float*)dev_alloc((size_t)B * WIDTH * HQ * sizeof(float));
+  int32_t* lens_t = (int32_t*)dev_alloc(sizeof(zero_h));
+  int32_t* depth = (int32_t*)dev_alloc(sizeof(zero_h));
+  int32_t* n_drop = (int32_t*)dev_alloc(sizeof(zero_h));
+  const int drop_h[B] = {5, 7};
+  hip_ok(hipMemset(q_t, 0, (size_t)B * WIDTH * HQ * D * 2), "q_t = 0");
+  hip_ok(hipMemcpy(lens_t, zero_h, sizeof(zero_h), hipMemcpyHostToDevice), "tree lens");
+  hip_ok(hipMemcpy(depth, zero_h, sizeof(zero_h), hipMemcpyHostToDevice), "depth");
+  hip_ok(hipMemcpy(n_drop, drop_h, sizeof(drop_h), hipMemcpyHostToDevice), "n_drop");
+  st = wmtp_ring_append(kt, vt, k_new, v_new, n_new, lens_t, B, HKV, D, SINK, R_WT, N_MAX, err, NULL);
+  check(st == WMTP_OK, "committed rows appended to the tree ring");
+  /* the candidates' rows: the first WIDTH rows of k_new / v_new viewed as [B, WIDTH, Hkv, d] */
+  st = wmtp_tree_append(kt, vt, kbr, vbr, k_new, v_new, lens_t, depth, B, WIDTH, HKV, D, W, SINK, R_WT, DD, err,
+                        NULL);
+  check(st == WMTP_OK, "wmtp_tree_append returns OK");
+  st = wmtp_tree_attn(q_t, kt, vt, kbr, vbr, lens_t, depth, out_t, lse_t, B, WIDTH, HQ, HKV, D, W, SINK, R_WT, DD,
+                      scale, ws, ws_bytes, err, NULL);
+  check(st == WMTP_OK, "wmtp_tree_attn returns OK");
+  hip_ok(hipDeviceSynchronize(), "tree");
+  int sel_tree[B * WIDTH];
+  for (int b = 0; b < B; ++b)
+    for (int c = 0; c < WIDTH; ++c) sel_tree[b * WIDTH + c] = n_new_h[b] + 1 > SINK + W ? SINK + W : n_new_h[b] + 1;
+  check_rows(out_t, lse_t, sel_tree, B * WIDTH, 0x3F80, "tree candidates at depth 1");
+  int back[B];
+  hip_ok(hipMemcpy(back, depth, sizeof(back), hipMemcpyDeviceToHost), "depth back");
+  check(back[0] == 1 && back[1] == 1, "tree append advanced the depth on the device");
+  st = wmtp_tree_reset(depth, B, NULL);
+  check(st == WMTP_OK, "wmtp_tree_reset returns OK");
+  st = wmtp_ring_rollback(lens_t, n_drop, B, err, NULL);
+  check(st == WMTP_OK, "wmtp_ring_rollback returns OK");
+  hip_ok(hipDeviceSynchronize(), "reset / rollback");
+  hip_ok(hipMemcpy(back, depth, sizeof(back), hipMemcpyDeviceToHost), "depth back");
+  check(back[0] == 0 && back[1] == 0, "depth reset to 0");
+  hip_ok(hipMemcpy(back, lens_t, sizeof(back), hipMemcpyDeviceToHost), "lens back");
+  check(back[0] == N_MAX - 5 && back[1] == 300 - 7, "rollback lens -= n_drop");
+
+  /* Fused windowed draft step on the dense cache: one row appended at
+   * 60000 and 300, attended at the new length in the same call. */
+  const int lens_in_h[B] = {60000, 300};
+  const int one_h[B] = {1, 1};
+  int32_t* lens_in = (int32_t*)dev_alloc(sizeof(lens_in_h));
+  int32_t* lens_out = (int32_t*)dev_alloc(sizeof(lens_in_h));
+  int32_t* n_one = (int32_t*)dev_alloc(sizeof(one_h));
+  hip_ok(hipMemcpy(lens_in, lens_in_h, sizeof(lens_in_h), hipMemcpyHostToDevice), "lens_in");
+  hip_ok(hipMemcpy(n_one, one_h, sizeof(one_h), hipMemcpyHostToDevice), "n_one");
+  st = wmtp_draft_step_windowed(q, k, v, k_new, v_new, n_one, lens_in, lens_out, out, lse, B, HQ, HKV, D, S_MAX, 1,
+                                W, SINK, scale, ws, ws_bytes, err, NULL);
+  check(st == WMTP_OK, "wmtp_draft_step_windowed returns OK");
+  hip_ok(hipDeviceSynchronize(), "fused step");
+  const int sel_step[B] = {SINK + W, 301};
+  check_uniform(out, lse, sel_step, "fused windowed step");
+  hip_ok(hipMemcpy(back, lens_out, sizeof(back), hipMemcpyDeviceToHost), "lens_out back");
+  check(back[0] == 60001 && back[1] == 301, "fused step wrote the new lengths");
+
   int32_t err_h = -1;
   hip_ok(hipMemcpy(&err_h, err, sizeof(err_h), hipMemcpyDeviceToHost), "err back");
   check(err_h == 0, "no device-side error bits");
@@ -239,6 +308,8 @@ int main(void) {
   hipFree(q); hipFree(k); hipFree(v); hipFree(out); hipFree(lse); hipFree(lens); hipFree(err); hipFree(ws);
   hipFree(k_ring); hipFree(v_ring); hipFree(k_new); hipFree(v_new); hipFree(n_new); hipFree(lens_ring);
   hipFree(table); hipFree(q3); hipFree(out3); hipFree(lse3); hipFree(n_q); hipFree(k8); hipFree(v8);
+  hipFree(kt); hipFree(vt); hipFree(kbr); hipFree(vbr); hipFree(q_t); hipFree(out_t); hipFree(lse_t);
+  hipFree(lens_t); hipFree(depth); hipFree(n_drop); hipFree(lens_in); hipFree(lens_out); hipFree(n_one);
   printf("%d failure(s)\n", failures);
   return failures == 0 ? 0 : 1;
 }
