@@ -118,10 +118,10 @@ class DraftLoop:
         self.ones = torch.ones(wl.B, dtype=torch.int32, device=dev)
         B, Hq, d = wl.B, wl.Hq, wl.d
         self.out = torch.empty((g, B, Hq, d), dtype=torch.bfloat16, device=dev)
-        self.ws_full = torch.empty(max(1, W.workspace_bytes(W.VARIANT_FULL, B, Hq, wl.Hkv, d, self.S_max)),
+        self.ws_full = torch.zeros(max(1, W.workspace_bytes(B, Hq, wl.Hkv, d, self.S_max, variant=W.VARIANT_FULL)),
                                    dtype=torch.uint8, device=dev)
-        self.ws_win = torch.empty(max(1, W.workspace_bytes(W.VARIANT_WINDOWED, B, Hq, wl.Hkv, d, self.S_max,
-                                                           wl.W, wl.sink)), dtype=torch.uint8, device=dev)
+        self.ws_win = torch.zeros(max(1, W.workspace_bytes(B, Hq, wl.Hkv, d, self.S_max,
+                                                           wl.W, wl.sink, variant=W.VARIANT_WINDOWED)), dtype=torch.uint8, device=dev)
         # ring holding the same logical rows (built by torch from the inputs)
         R_w = wl.W + g + 1  # the paper's chain sizing: window + draft depth
         self.R_w = R_w
@@ -393,7 +393,7 @@ def spec_figures(loop, width=4):
     lens = torch.full((B,), wl.S, dtype=torch.int32, device=dev)
     depth = torch.zeros((B,), dtype=torch.int32, device=dev)
     out = torch.empty_like(q)
-    ws = torch.empty(W.workspace_bytes(W.VARIANT_TREE, B * width, wl.Hq, wl.Hkv, wl.d, 0, wl.W, wl.sink),
+    ws = torch.zeros(W.workspace_bytes(B * width, wl.Hq, wl.Hkv, wl.d, 0, wl.W, wl.sink, variant=W.VARIANT_TREE),
                      dtype=torch.uint8, device=dev)
 
     def tree_round():
@@ -407,7 +407,7 @@ def spec_figures(loop, width=4):
     out1 = torch.empty_like(q1)
     ones = torch.ones((B,), dtype=torch.int32, device=dev)
     drop = torch.full((B,), wl.gamma // 2, dtype=torch.int32, device=dev)
-    ws1 = torch.empty(W.workspace_bytes(W.VARIANT_RING, B, wl.Hq, wl.Hkv, wl.d, slots, wl.W, wl.sink),
+    ws1 = torch.zeros(W.workspace_bytes(B, wl.Hq, wl.Hkv, wl.d, slots, wl.W, wl.sink, variant=W.VARIANT_RING),
                       dtype=torch.uint8, device=dev)
     kn1, vn1 = kn[:, :1].contiguous(), vn[:, :1].contiguous()
     lens_c = lens.clone()
@@ -643,8 +643,8 @@ def bench_batch(wl, dev, args):
     lens = torch.as_tensor(case["lens"], device=dev)
     S_max = case["S_max"]
     B, Hq, Hkv, d = wl.B, wl.Hq, wl.Hkv, wl.d
-    ws_f = torch.empty(W.workspace_bytes(W.VARIANT_FULL, B, Hq, Hkv, d, S_max), dtype=torch.uint8, device=dev)
-    ws_w = torch.empty(W.workspace_bytes(W.VARIANT_WINDOWED, B, Hq, Hkv, d, S_max, wl.W, wl.sink),
+    ws_f = torch.zeros(W.workspace_bytes(B, Hq, Hkv, d, S_max, variant=W.VARIANT_FULL), dtype=torch.uint8, device=dev)
+    ws_w = torch.zeros(W.workspace_bytes(B, Hq, Hkv, d, S_max, wl.W, wl.sink, variant=W.VARIANT_WINDOWED),
                        dtype=torch.uint8, device=dev)
     out = torch.empty_like(q)
     full = event_us(lambda: W.draft_attn_full(q, k, v, lens, out=out, ws=ws_f, scale=wl.scale),
@@ -686,7 +686,7 @@ def bench_ring(wl, dev, args):
     lens = torch.zeros(B, dtype=torch.int32, device=dev)
     lp = [torch.zeros_like(lens), torch.zeros_like(lens)]
     out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
-    ws = torch.empty(W.workspace_bytes(W.VARIANT_RING, B, Hq, Hkv, d, wl.sink + R_w, wl.W, wl.sink),
+    ws = torch.zeros(W.workspace_bytes(B, Hq, Hkv, d, wl.sink + R_w, wl.W, wl.sink, variant=W.VARIANT_RING),
                      dtype=torch.uint8, device=dev)
 
     def unfused(lo, hi):

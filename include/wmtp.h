@@ -46,6 +46,11 @@
 #include <stddef.h>
 #include <stdint.h>
 
+/* The HIP stream handle: the same declaration as the HIP runtime header's,
+ * so this header is usable with or without it (C11 and C++ accept the
+ * repeated typedef).  NULL is the default stream. */
+typedef struct ihipStream_t* hipStream_t;
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -80,15 +85,19 @@ typedef enum {
  * Workspace (device bytes) that one attention call of the given variant and
  * shape needs for its split-K partial results (per work item and query head:
  * the running maximum, two softmax denominators and the unnormalised output
- * row, in fp32), sized for the current device.
+ * row, in fp32) and its work counters, sized for the current device.
  * B counts query rows: the batch for the single-row calls, B * q_max for the
  * extend calls.  S_max is the dense cache capacity (ignored for the ring); W
- * and sink are ignored for the full variant.  Returns 0 for arguments the attention calls
- * would reject.  The workspace needs no initialisation and may be reused by
- * successive calls on one stream.
+ * and sink are ignored for the full variant.  Returns 0 for arguments the
+ * attention calls would reject.
+ * A workspace must be zero-filled once before its first use (for example
+ * with hipMemset when it is allocated); every call leaves it ready for the
+ * next call, so one workspace serves successive calls on one stream, also
+ * replays of a captured graph.  Calls that may overlap in time need
+ * separate workspaces.
  */
-size_t wmtp_workspace_bytes(int variant, int B, int Hq, int Hkv, int d, int64_t S_max, int W,
-                            int sink);
+size_t wmtp_workspace_bytes(int B, int Hq, int Hkv, int d, int64_t S_max, int W, int sink,
+                            int variant);
 
 /*
  * Full-context draft decode attention (the native MTP draft; Section 3 and
@@ -105,7 +114,7 @@ size_t wmtp_workspace_bytes(int variant, int B, int Hq, int Hkv, int d, int64_t 
  */
 int wmtp_draft_attn_full(const void* q, const void* k, const void* v, const int32_t* lens,
                          void* out, float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
-                         float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream);
+                         float scale, void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream);
 
 /*
  * Windowed draft decode attention over the dense cache (Section 4
@@ -120,7 +129,7 @@ int wmtp_draft_attn_full(const void* q, const void* k, const void* v, const int3
 int wmtp_draft_attn_windowed(const void* q, const void* k, const void* v, const int32_t* lens,
                              void* out, float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
                              int W, int sink, float scale, void* ws, size_t ws_bytes,
-                             int32_t* err, void* stream);
+                             int32_t* err, hipStream_t stream);
 
 /*
  * Windowed draft decode attention over the compact ring store (Section 4 and
@@ -139,7 +148,7 @@ int wmtp_draft_attn_windowed(const void* q, const void* k, const void* v, const 
  */
 int wmtp_ring_attn(const void* q, const void* k_ring, const void* v_ring, const int32_t* lens,
                    void* out, float* lse, int B, int Hq, int Hkv, int d, int W, int sink, int R_w,
-                   float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream);
+                   float scale, void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream);
 
 /*
  * Draft-extend attention: several new query rows per sequence, attending
@@ -161,15 +170,15 @@ int wmtp_ring_attn(const void* q, const void* k_ring, const void* v_ring, const 
 int wmtp_draft_extend_full(const void* q, const void* k, const void* v, const int32_t* lens,
                            const int32_t* n_q, void* out, float* lse, int B, int q_max, int Hq,
                            int Hkv, int d, int64_t S_max, float scale, void* ws, size_t ws_bytes,
-                           int32_t* err, void* stream);
+                           int32_t* err, hipStream_t stream);
 int wmtp_draft_extend_windowed(const void* q, const void* k, const void* v, const int32_t* lens,
                                const int32_t* n_q, void* out, float* lse, int B, int q_max, int Hq,
                                int Hkv, int d, int64_t S_max, int W, int sink, float scale,
-                               void* ws, size_t ws_bytes, int32_t* err, void* stream);
+                               void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream);
 int wmtp_ring_extend(const void* q, const void* k_ring, const void* v_ring, const int32_t* lens,
                      const int32_t* n_q, void* out, float* lse, int B, int q_max, int Hq, int Hkv,
                      int d, int W, int sink, int R_w, float scale, void* ws, size_t ws_bytes,
-                     int32_t* err, void* stream);
+                     int32_t* err, hipStream_t stream);
 
 /*
  * Paged draft KV (a shared token pool with page size 1, as in the paper's
@@ -187,12 +196,12 @@ int wmtp_ring_extend(const void* q, const void* k_ring, const void* v_ring, cons
 int wmtp_paged_attn_full(const void* q, const void* k_pool, const void* v_pool,
                          const int32_t* req_to_token, const int32_t* lens, void* out, float* lse,
                          int B, int Hq, int Hkv, int d, int64_t pool_rows, int64_t table_stride,
-                         float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream);
+                         float scale, void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream);
 int wmtp_paged_attn_windowed(const void* q, const void* k_pool, const void* v_pool,
                              const int32_t* req_to_token, const int32_t* lens, void* out,
                              float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
                              int64_t table_stride, int W, int sink, float scale, void* ws,
-                             size_t ws_bytes, int32_t* err, void* stream);
+                             size_t ws_bytes, int32_t* err, hipStream_t stream);
 
 /*
  * The draft's KV-index builder (the step Windowed-MTP modifies, Appendix A
@@ -207,7 +216,7 @@ int wmtp_paged_attn_windowed(const void* q, const void* k_pool, const void* v_po
 int64_t wmtp_kv_indices_capacity(int variant, int B, int64_t table_stride, int W, int sink);
 int wmtp_build_kv_indices(const int32_t* req_to_token, const int32_t* lens, int B,
                           int64_t table_stride, int variant, int W, int sink, int32_t* kv_indptr,
-                          int32_t* kv_indices, int64_t capacity, int32_t* err, void* stream);
+                          int32_t* kv_indices, int64_t capacity, int32_t* err, hipStream_t stream);
 
 /*
  * Append draft KV rows to the ring store (the draft forward writes the K/V
@@ -222,7 +231,7 @@ int wmtp_build_kv_indices(const int32_t* req_to_token, const int32_t* lens, int 
  */
 int wmtp_ring_append(void* k_ring, void* v_ring, const void* k_new, const void* v_new,
                      const int32_t* n_new, int32_t* lens, int B, int Hkv, int d, int sink, int R_w,
-                     int n_max, int32_t* err, void* stream);
+                     int n_max, int32_t* err, hipStream_t stream);
 
 /*
  * Append draft KV rows to a dense cache [B, S_max, Hkv, d]: rows go to
@@ -232,7 +241,7 @@ int wmtp_ring_append(void* k_ring, void* v_ring, const void* k_new, const void* 
  */
 int wmtp_cache_append(void* k, void* v, const void* k_new, const void* v_new,
                       const int32_t* n_new, int32_t* lens, int B, int Hkv, int d, int64_t S_max,
-                      int n_max, int32_t* err, void* stream);
+                      int n_max, int32_t* err, hipStream_t stream);
 
 /*
  * Export of the windowed key selection and ring slot map that the attention
@@ -244,7 +253,7 @@ int wmtp_cache_append(void* k, void* v, const void* k_new, const void* v_new,
  * slot_out and must then be >= W.
  */
 int wmtp_select_indices(const int32_t* lens, int B, int W, int sink, int R_w, int32_t* pos_out,
-                        int32_t* slot_out, int32_t* n_sel_out, int32_t* err, void* stream);
+                        int32_t* slot_out, int32_t* n_sel_out, int32_t* err, hipStream_t stream);
 
 /*
  * Fused draft step: the append and the attention of one draft step in one
@@ -272,17 +281,17 @@ int wmtp_draft_step_full(const void* q, void* k, void* v, const void* k_new, con
                          const int32_t* n_new, const int32_t* lens_in, int32_t* lens_out,
                          void* out, float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
                          int n_max, float scale, void* ws, size_t ws_bytes, int32_t* err,
-                         void* stream);
+                         hipStream_t stream);
 int wmtp_draft_step_windowed(const void* q, void* k, void* v, const void* k_new,
                              const void* v_new, const int32_t* n_new, const int32_t* lens_in,
                              int32_t* lens_out, void* out, float* lse, int B, int Hq, int Hkv,
                              int d, int64_t S_max, int n_max, int W, int sink, float scale,
-                             void* ws, size_t ws_bytes, int32_t* err, void* stream);
+                             void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream);
 int wmtp_ring_step(const void* q, void* k_ring, void* v_ring, const void* k_new,
                    const void* v_new, const int32_t* n_new, const int32_t* lens_in,
                    int32_t* lens_out, void* out, float* lse, int B, int Hq, int Hkv, int d, int W,
                    int sink, int R_w, int n_max, float scale, void* ws, size_t ws_bytes,
-                   int32_t* err, void* stream);
+                   int32_t* err, hipStream_t stream);
 
 /*
  * Speculative draft rows.
@@ -297,12 +306,13 @@ int wmtp_ring_step(const void* q, void* k_ring, void* v_ring, const void* k_new,
  * n_sink + W + d slots (Section 7, tree speculation; Appendix A ring
  * comment).
  */
-int wmtp_ring_rollback(int32_t* lens, const int32_t* n_drop, int B, int32_t* err, void* stream);
+int wmtp_ring_rollback(int32_t* lens, const int32_t* n_drop, int B, int32_t* err, hipStream_t stream);
 
 /*
- * Tree-width rings (Section 7, tree speculation: the candidates share the
- * sink + window prefix and differ only over their last d positions, so a
- * tree of width k reserves n_sink + W + d k slots per request).
+ * Tree-width rings (Section 7, tree speculation).  Sizing rule: every
+ * candidate of a tree reads the same sink and window rows; only its own most
+ * recent d draft rows are private to it, so k candidates need the chain's
+ * n_sink + W + d slots plus d more for each further candidate, d k in all.
  *   State per request: lens[b] = committed length S (rows the target has
  *   accepted), depth[b] = speculative depth i (0 .. depth_max), both on the
  *   device.  Candidate c's sequence is rows [0, S) followed by its own rows
@@ -330,13 +340,13 @@ int wmtp_ring_rollback(int32_t* lens, const int32_t* n_drop, int B, int32_t* err
 int wmtp_tree_append(void* k_ring, void* v_ring, void* k_branch, void* v_branch, const void* k_new,
                      const void* v_new, const int32_t* lens, int32_t* depth, int B, int width,
                      int Hkv, int d, int W, int sink, int R_w, int depth_max, int32_t* err,
-                     void* stream);
+                     hipStream_t stream);
 int wmtp_tree_attn(const void* q, const void* k_ring, const void* v_ring, const void* k_branch,
                    const void* v_branch, const int32_t* lens, const int32_t* depth, void* out,
                    float* lse, int B, int width, int Hq, int Hkv, int d, int W, int sink, int R_w,
                    int depth_max, float scale, void* ws, size_t ws_bytes, int32_t* err,
-                   void* stream);
-int wmtp_tree_reset(int32_t* depth, int B, void* stream);
+                   hipStream_t stream);
+int wmtp_tree_reset(int32_t* depth, int B, hipStream_t stream);
 
 /*
  * fp8 draft KV cache (Section 7, KV-cache quantization: the windowing
@@ -357,16 +367,16 @@ int wmtp_tree_reset(int32_t* depth, int B, void* stream);
 int wmtp_draft_attn_full_fp8(const void* q, const void* k, const void* v, const int32_t* lens,
                              void* out, float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
                              float scale, float k_scale, float v_scale, void* ws, size_t ws_bytes,
-                             int32_t* err, void* stream);
+                             int32_t* err, hipStream_t stream);
 int wmtp_draft_attn_windowed_fp8(const void* q, const void* k, const void* v, const int32_t* lens,
                                  void* out, float* lse, int B, int Hq, int Hkv, int d,
                                  int64_t S_max, int W, int sink, float scale, float k_scale,
                                  float v_scale, void* ws, size_t ws_bytes, int32_t* err,
-                                 void* stream);
+                                 hipStream_t stream);
 int wmtp_ring_attn_fp8(const void* q, const void* k_ring, const void* v_ring, const int32_t* lens,
                        void* out, float* lse, int B, int Hq, int Hkv, int d, int W, int sink,
                        int R_w, float scale, float k_scale, float v_scale, void* ws,
-                       size_t ws_bytes, int32_t* err, void* stream);
+                       size_t ws_bytes, int32_t* err, hipStream_t stream);
 
 /*
  * fp8 paged draft attention (Section 7 KV-cache quantization over the paged
@@ -387,29 +397,29 @@ int wmtp_draft_extend_full_fp8(const void* q, const void* k, const void* v, cons
                                const int32_t* n_q, void* out, float* lse, int B, int q_max,
                                int Hq, int Hkv, int d, int64_t S_max, float scale, float k_scale,
                                float v_scale, void* ws, size_t ws_bytes, int32_t* err,
-                               void* stream);
+                               hipStream_t stream);
 int wmtp_draft_extend_windowed_fp8(const void* q, const void* k, const void* v,
                                    const int32_t* lens, const int32_t* n_q, void* out, float* lse,
                                    int B, int q_max, int Hq, int Hkv, int d, int64_t S_max, int W,
                                    int sink, float scale, float k_scale, float v_scale, void* ws,
-                                   size_t ws_bytes, int32_t* err, void* stream);
+                                   size_t ws_bytes, int32_t* err, hipStream_t stream);
 int wmtp_ring_extend_fp8(const void* q, const void* k_ring, const void* v_ring,
                          const int32_t* lens, const int32_t* n_q, void* out, float* lse, int B,
                          int q_max, int Hq, int Hkv, int d, int W, int sink, int R_w, float scale,
                          float k_scale, float v_scale, void* ws, size_t ws_bytes, int32_t* err,
-                         void* stream);
+                         hipStream_t stream);
 
 int wmtp_paged_attn_full_fp8(const void* q, const void* k_pool, const void* v_pool,
                              const int32_t* req_to_token, const int32_t* lens, void* out,
                              float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
                              int64_t table_stride, float scale, float k_scale, float v_scale,
-                             void* ws, size_t ws_bytes, int32_t* err, void* stream);
+                             void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream);
 int wmtp_paged_attn_windowed_fp8(const void* q, const void* k_pool, const void* v_pool,
                                  const int32_t* req_to_token, const int32_t* lens, void* out,
                                  float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
                                  int64_t table_stride, int W, int sink, float scale,
                                  float k_scale, float v_scale, void* ws, size_t ws_bytes,
-                                 int32_t* err, void* stream);
+                                 int32_t* err, hipStream_t stream);
 
 /*
  * fp8 appends: as wmtp_ring_append / wmtp_cache_append, with the bf16 rows
@@ -421,11 +431,11 @@ int wmtp_paged_attn_windowed_fp8(const void* q, const void* k_pool, const void* 
 int wmtp_ring_append_fp8(void* k_ring, void* v_ring, const void* k_new, const void* v_new,
                          const int32_t* n_new, int32_t* lens, int B, int Hkv, int d, int sink,
                          int R_w, int n_max, float k_scale, float v_scale, int32_t* err,
-                         void* stream);
+                         hipStream_t stream);
 int wmtp_cache_append_fp8(void* k, void* v, const void* k_new, const void* v_new,
                           const int32_t* n_new, int32_t* lens, int B, int Hkv, int d,
                           int64_t S_max, int n_max, float k_scale, float v_scale, int32_t* err,
-                          void* stream);
+                          hipStream_t stream);
 
 /*
  * The fp8 format's element conversions, as the appends and the attention
@@ -434,8 +444,8 @@ int wmtp_cache_append_fp8(void* k, void* v, const void* k_new, const void* v_new
  * dequantize writes the bf16 value of codes[i] (exact; NaN codes give NaN).
  * n must be a multiple of 8; x and out 16-byte, codes 8-byte aligned.
  */
-int wmtp_fp8_quantize(const void* x, int64_t n, float scale, void* codes, void* stream);
-int wmtp_fp8_dequantize(const void* codes, int64_t n, void* out, void* stream);
+int wmtp_fp8_quantize(const void* x, int64_t n, float scale, void* codes, hipStream_t stream);
+int wmtp_fp8_dequantize(const void* codes, int64_t n, void* out, hipStream_t stream);
 
 /*
  * Measurement helper, not part of the method: one streaming pass over `bytes`
@@ -449,7 +459,7 @@ int wmtp_fp8_dequantize(const void* codes, int64_t n, void* out, void* stream);
  * Returns WMTP_EINVAL for a bad size, pointer or alignment.
  */
 #define WMTP_PROBE_BLOCKS 512
-int wmtp_hbm_read_probe(const void* buf, int64_t bytes, uint32_t* sink, void* stream);
+int wmtp_hbm_read_probe(const void* buf, int64_t bytes, uint32_t* sink, hipStream_t stream);
 
 /* Human-readable name of a wmtp_status value (static string). */
 const char* wmtp_status_string(int status);
@@ -457,7 +467,7 @@ const char* wmtp_status_string(int status);
 /* ABI version of this header, (major << 16) | minor. */
 int wmtp_abi_version(void);
 
-#define WMTP_ABI_VERSION ((1 << 16) | 6)
+#define WMTP_ABI_VERSION ((2 << 16) | 0)
 
 #ifdef __cplusplus
 }

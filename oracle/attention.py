@@ -54,9 +54,10 @@ __all__ = [
     "selected_positions",
     "n_selected",
     "attend_sequence",
-    "attend_batch",
+    "value_spread",
     "extend_lengths",
     "attend_extend",
+    "extend_spread",
 ]
 
 # Keys processed per chunk when forming logits and the value sum.
@@ -157,29 +158,39 @@ def attend_sequence(q, K, V, S: int, scale: float, mask=None, chunk: int = _CHUN
     return o, lse
 
 
-def attend_batch(q, K, V, lens, scale: float, variant: str = "full",
-                 W: int | None = None, sink: int | None = None, batch_ids=None):
-    """Batched draft decode attention over a dense cache [B, S_max, Hkv, d].
+def value_spread(q, K, V, S: int, scale: float, mask=None, chunk: int = 4096):
+    """Weighted mean absolute deviation of the attended values about the output.
 
-    variant "full" attends [0, lens[b]); "windowed" applies window_mask.
-    batch_ids restricts the computation to the listed sequences (the rows of
-    the result follow that order).  Returns (o [nb, Hq, d], lse [nb, Hq]).
+        spread[h, c] = sum_p w_p |V[p, g(h), c] - o[h, c]|,   w_p = exp(z_p - lse_h)
+
+    over the same kept keys, normalised weights (they sum to 1) and output o
+    as attend_sequence.  This is not part of the method: it sizes the effect
+    of perturbing the weights.  If every weight moves by a relative amount of
+    at most r and the result is renormalised, o moves by at most
+    r / (1 - r) * spread (because sum_p w_p (V_p - o) = 0).  The GPU tests use
+    it to bound the effect of rounding the weights to bfloat16.
+    Returns spread [Hq, d] float64 (zero for an empty key set).
     """
-    lens = np.asarray(lens).astype(np.int64)
-    ids = range(len(lens)) if batch_ids is None else list(batch_ids)
-    outs, lses = [], []
-    for b in ids:
-        S = int(lens[b])
-        if variant == "full":
-            mask = None
-        elif variant == "windowed":
-            mask = window_mask(S, W, sink)
-        else:
-            raise ValueError(f"unknown variant {variant!r}")
-        o, lse = attend_sequence(q[b], K[b], V[b], S, scale, mask)
-        outs.append(o)
-        lses.append(lse)
-    return np.stack(outs), np.stack(lses)
+    qf = _as_f64(q)
+    Hq, d = qf.shape
+    Hkv = K.shape[1]
+    G = Hq // Hkv
+    S = int(S)
+    keep = np.arange(S) if mask is None else np.flatnonzero(np.asarray(mask)[:S])
+    spread = np.zeros((Hq, d), dtype=np.float64)
+    if keep.size == 0:
+        return spread
+    o, lse = attend_sequence(q, K, V, S, scale, mask)
+    for c0 in range(0, keep.size, chunk):
+        rows = keep[c0:c0 + chunk]
+        Kc = _as_f64(np.asarray(K[rows]))
+        Vc = _as_f64(np.asarray(V[rows]))
+        for g in range(Hkv):
+            hs = slice(g * G, (g + 1) * G)
+            w = np.exp(scale * (qf[hs] @ Kc[:, g, :].T) - lse[hs, None])        # [G, c]
+            dev = np.abs(Vc[None, :, g, :] - o[hs, None, :])                   # [G, c, d]
+            spread[hs] += np.einsum("hp,hpc->hc", w, dev)
+    return spread
 
 
 def extend_lengths(S: int, n: int, q_max: int):
@@ -212,3 +223,18 @@ def attend_extend(q_rows, K, V, S: int, n: int, scale: float, variant: str = "fu
         mask = None if variant == "full" else window_mask(L, W, sink)
         o[t], lse[t] = attend_sequence(q_rows[t], K, V, L, scale, mask)
     return o, lse
+
+
+def extend_spread(q_rows, K, V, S: int, n: int, scale: float, variant: str = "full",
+                  W: int | None = None, sink: int | None = None):
+    """value_spread of every new row of a draft-extend (rows as attend_extend;
+    padding rows give 0).  Returns [q_max, Hq, d]."""
+    q_rows = np.asarray(q_rows)
+    q_max, Hq, d = q_rows.shape
+    out = np.zeros((q_max, Hq, d))
+    for t, L in enumerate(extend_lengths(S, n, q_max)):
+        if L <= 0:
+            continue
+        mask = None if variant == "full" else window_mask(L, W, sink)
+        out[t] = value_spread(q_rows[t], K, V, L, scale, mask)
+    return out

@@ -120,24 +120,33 @@ class DequantizedRows:
         return dequantize(np.asarray(self.codes[rows]), self.scale)
 
 
-def attend_sequence_fp8(q, k_codes, v_codes, S, scale, k_scale, v_scale, variant="full", W=1, sink=0):
+def attend_sequence_fp8(q, k_codes, v_codes, S, scale, k_scale, v_scale, variant="full", W=1, sink=0,
+                        spread=False):
     """Single-token GQA decode attention of one sequence over an fp8 cache.
 
     q [Hq, d] (bf16 bits or floats); k_codes, v_codes [rows >= S, Hkv, d]
     uint8 (or row views, see DequantizedRows).  The key set is the variant's
     (oracle.attention.window_mask); the softmax and the value sum are
     oracle.attention.attend_sequence over the dequantized rows.  Returns
-    (o [Hq, d], lse [Hq]) in float64.
+    (o [Hq, d], lse [Hq]) in float64, and with spread=True also
+    oracle.attention.value_spread over the same rows.
     """
     mask = None if variant == "full" else A.window_mask(S, W, sink)
-    return A.attend_sequence(q, DequantizedRows(k_codes, k_scale), DequantizedRows(v_codes, v_scale), S,
-                             scale, mask)
+    K, V = DequantizedRows(k_codes, k_scale), DequantizedRows(v_codes, v_scale)
+    o, lse = A.attend_sequence(q, K, V, S, scale, mask)
+    if not spread:
+        return o, lse
+    return o, lse, A.value_spread(q, K, V, S, scale, mask)
 
 
-def attend_ring_fp8(q, ring_k, ring_v, S, scale, k_scale, v_scale, W, sink, R_w):
+def attend_ring_fp8(q, ring_k, ring_v, S, scale, k_scale, v_scale, W, sink, R_w, spread=False):
     """Windowed attention read through the compact ring's slot map
-    (oracle.ring.ring_slot) from an fp8 ring [sink + R_w, Hkv, d]."""
+    (oracle.ring.ring_slot) from an fp8 ring [sink + R_w, Hkv, d]
+    (spread as for attend_sequence_fp8)."""
     slots = R.ring_slots(A.selected_positions(S, W, sink), sink, R_w)
     K = dequantize(np.asarray(ring_k)[slots], k_scale)
     V = dequantize(np.asarray(ring_v)[slots], v_scale)
-    return A.attend_sequence(q, K, V, len(slots), scale, None)
+    o, lse = A.attend_sequence(q, K, V, len(slots), scale, None)
+    if not spread:
+        return o, lse
+    return o, lse, A.value_spread(q, K, V, len(slots), scale, None)

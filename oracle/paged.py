@@ -41,9 +41,13 @@ def kv_indices(table, lens, variant: str, W: int | None = None, sink: int | None
 
 
 def attend_paged(q, K_pool, V_pool, table_row, S: int, scale: float, variant: str,
-                 W: int | None = None, sink: int | None = None):
-    """Attention of one request over the pool rows its index list names."""
+                 W: int | None = None, sink: int | None = None, spread: bool = False):
+    """Attention of one request over the pool rows its index list names
+    (with spread=True also oracle.attention.value_spread over those rows)."""
     rows = np.asarray(table_row)[keep_positions(int(S), variant, W, sink)]
     K = np.asarray(K_pool[rows])
     V = np.asarray(V_pool[rows])
-    return attention.attend_sequence(q, K, V, rows.size, scale, None)
+    o, lse = attention.attend_sequence(q, K, V, rows.size, scale, None)
+    if not spread:
+        return o, lse
+    return o, lse, attention.value_spread(q, K, V, rows.size, scale, None)

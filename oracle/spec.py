@@ -4,11 +4,12 @@ and tree-width rings -- the oracle's model.
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
 Paper facts this follows (Windowed-MTP):
-  * Section 7, "Compatibility with tree speculation": windowing changes only
-    which KV the draft attends, not the shape of the candidate tree; the
-    candidates share the sink + window prefix and differ only over their
-    last d positions, so a chain reserves n_sink + W + d ring slots per
-    request and a tree of width k reserves n_sink + W + d k.
+  * Section 7, "Compatibility with tree speculation": the window decides
+    which rows the draft reads, and is independent of how the candidates
+    branch.  Sizing: all candidates read one common set of sink and window
+    rows and keep private only their latest d draft rows, so one chain
+    needs n_sink + W + d ring slots per request and each extra candidate
+    adds d more (n_sink + W + d k for k candidates).
   * Appendix A pseudocode, ring comment: the chain ring's modulus is
     n_sink + W + d.
   * Section 3 (per-step latency model): each draft step writes its token's
@@ -144,17 +145,22 @@ class SpecSequences:
     def sequence(self, b: int):
         return self.committed + self.spec[b]
 
-    def attend(self, q, b: int, scale: float, W: int, sink: int):
-        """Candidate b's windowed draft attention at length S + depth."""
+    def attend(self, q, b: int, scale: float, W: int, sink: int, spread: bool = False):
+        """Candidate b's windowed draft attention at length S + depth (with
+        spread=True also oracle.attention.value_spread over the same rows)."""
         seq = self.sequence(b)
         L = len(seq)
         keep = attention.selected_positions(L, W, sink)
         if keep.size == 0:
             Hq, d = np.asarray(q).shape
-            return np.zeros((Hq, d)), np.full(Hq, -np.inf)
+            empty = (np.zeros((Hq, d)), np.full(Hq, -np.inf))
+            return empty + (np.zeros((Hq, d)),) if spread else empty
         K = np.stack([seq[p][0] for p in keep])
         V = np.stack([seq[p][1] for p in keep])
-        return attention.attend_sequence(q, K, V, keep.size, scale, None)
+        o, lse = attention.attend_sequence(q, K, V, keep.size, scale, None)
+        if not spread:
+            return o, lse
+        return o, lse, attention.value_spread(q, K, V, keep.size, scale, None)
 
 
 class ChainRing(ring.RingSimulator):

@@ -67,7 +67,7 @@ constexpr int kMaxQueryRows = 4096;
 int attention_common(int variant, const void* q, const void* k, const void* v,
                      const int32_t* lens, const int32_t* n_q, int q_max, void* out, float* lse,
                      int B, int Hq, int Hkv, int d, int64_t S_max, int W, int sink, int R_w,
-                     float scale, void* ws, size_t ws_bytes, int32_t* err, void* stream,
+                     float scale, void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream,
                      const int32_t* table = nullptr, int64_t pool_rows = 0, bool fp8 = false,
                      float k_scale = 1.0f, float v_scale = 1.0f, const void* k2 = nullptr,
                      const void* v2 = nullptr, int dd = 0, bool step = false,
@@ -172,14 +172,14 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   L.pl = reinterpret_cast<float*>(base + plan.off_pl);
   L.pz = reinterpret_cast<float*>(base + plan.off_pz);
   L.po = reinterpret_cast<float*>(base + plan.off_po);
-  if (wmtp::launch_attention(L, static_cast<hipStream_t>(stream)) != hipSuccess)
+  if (wmtp::launch_attention(L, stream) != hipSuccess)
     return WMTP_ELAUNCH;
   return WMTP_OK;
 }
 
 int append_common(bool ring, void* k, void* v, const void* k_new, const void* v_new,
                   const int32_t* n_new, int32_t* lens, int B, int Hkv, int d, int64_t rows,
-                  int sink, int R_w, int n_max, int32_t* err, void* stream, bool fp8 = false,
+                  int sink, int R_w, int n_max, int32_t* err, hipStream_t stream, bool fp8 = false,
                   float k_scale = 1.0f, float v_scale = 1.0f, int32_t* lens_out = nullptr,
                   bool dry_run = false) {
   if (B < 0 || Hkv < 1 || d < 1 || n_max < 0) return WMTP_EINVAL;
@@ -216,14 +216,14 @@ int append_common(bool ring, void* k, void* v, const void* k_new, const void* v_
   L.R_w = ring ? R_w : 1;
   L.n_max = n_max;
   L.lens_out = lens_out;
-  if (wmtp::launch_append(L, static_cast<hipStream_t>(stream)) != hipSuccess) return WMTP_ELAUNCH;
+  if (wmtp::launch_append(L, stream) != hipSuccess) return WMTP_ELAUNCH;
   return WMTP_OK;
 }
 
 }  // namespace
 
-WMTP_EXPORT size_t wmtp_workspace_bytes(int variant, int B, int Hq, int Hkv, int d, int64_t S_max,
-                                        int W, int sink) {
+WMTP_EXPORT size_t wmtp_workspace_bytes(int B, int Hq, int Hkv, int d, int64_t S_max, int W,
+                                        int sink, int variant) {
   if (variant < WMTP_VARIANT_FULL || variant > WMTP_VARIANT_TREE) return 0;
   if (check_heads(B, Hq, Hkv, d) != WMTP_OK || B == 0) return 0;
   if (windowed_variant(variant) && check_window(W, sink) != WMTP_OK) return 0;
@@ -237,7 +237,7 @@ WMTP_EXPORT size_t wmtp_workspace_bytes(int variant, int B, int Hq, int Hkv, int
 WMTP_EXPORT int wmtp_draft_attn_full(const void* q, const void* k, const void* v,
                                      const int32_t* lens, void* out, float* lse, int B, int Hq,
                                      int Hkv, int d, int64_t S_max, float scale, void* ws,
-                                     size_t ws_bytes, int32_t* err, void* stream) {
+                                     size_t ws_bytes, int32_t* err, hipStream_t stream) {
   return attention_common(WMTP_VARIANT_FULL, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv, d,
                           S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream);
 }
@@ -246,7 +246,7 @@ WMTP_EXPORT int wmtp_draft_attn_windowed(const void* q, const void* k, const voi
                                          const int32_t* lens, void* out, float* lse, int B,
                                          int Hq, int Hkv, int d, int64_t S_max, int W, int sink,
                                          float scale, void* ws, size_t ws_bytes, int32_t* err,
-                                         void* stream) {
+                                         hipStream_t stream) {
   return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv,
                           d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream);
 }
@@ -254,7 +254,7 @@ WMTP_EXPORT int wmtp_draft_attn_windowed(const void* q, const void* k, const voi
 WMTP_EXPORT int wmtp_ring_attn(const void* q, const void* k_ring, const void* v_ring,
                                const int32_t* lens, void* out, float* lse, int B, int Hq, int Hkv,
                                int d, int W, int sink, int R_w, float scale, void* ws,
-                               size_t ws_bytes, int32_t* err, void* stream) {
+                               size_t ws_bytes, int32_t* err, hipStream_t stream) {
   if (check_window(W, sink) == WMTP_OK && (R_w < W || static_cast<int64_t>(sink) + R_w > INT_MAX))
     return WMTP_EINVAL;
   return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, nullptr, 1, out, lse, B, Hq,
@@ -266,7 +266,7 @@ WMTP_EXPORT int wmtp_draft_extend_full(const void* q, const void* k, const void*
                                        const int32_t* lens, const int32_t* n_q, void* out,
                                        float* lse, int B, int q_max, int Hq, int Hkv, int d,
                                        int64_t S_max, float scale, void* ws, size_t ws_bytes,
-                                       int32_t* err, void* stream) {
+                                       int32_t* err, hipStream_t stream) {
   return attention_common(WMTP_VARIANT_FULL, q, k, v, lens, n_q, q_max, out, lse, B, Hq, Hkv, d,
                           S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream);
 }
@@ -275,7 +275,7 @@ WMTP_EXPORT int wmtp_draft_extend_windowed(const void* q, const void* k, const v
                                            const int32_t* lens, const int32_t* n_q, void* out,
                                            float* lse, int B, int q_max, int Hq, int Hkv, int d,
                                            int64_t S_max, int W, int sink, float scale, void* ws,
-                                           size_t ws_bytes, int32_t* err, void* stream) {
+                                           size_t ws_bytes, int32_t* err, hipStream_t stream) {
   return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, n_q, q_max, out, lse, B, Hq, Hkv,
                           d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream);
 }
@@ -284,7 +284,7 @@ WMTP_EXPORT int wmtp_ring_extend(const void* q, const void* k_ring, const void* 
                                  const int32_t* lens, const int32_t* n_q, void* out, float* lse,
                                  int B, int q_max, int Hq, int Hkv, int d, int W, int sink,
                                  int R_w, float scale, void* ws, size_t ws_bytes, int32_t* err,
-                                 void* stream) {
+                                 hipStream_t stream) {
   if (check_window(W, sink) == WMTP_OK && static_cast<int64_t>(sink) + R_w > INT_MAX)
     return WMTP_EINVAL;
   return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, n_q, q_max, out, lse, B, Hq,
@@ -296,7 +296,7 @@ WMTP_EXPORT int wmtp_paged_attn_full(const void* q, const void* k_pool, const vo
                                       const int32_t* req_to_token, const int32_t* lens, void* out,
                                       float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
                                       int64_t table_stride, float scale, void* ws, size_t ws_bytes,
-                                      int32_t* err, void* stream) {
+                                      int32_t* err, hipStream_t stream) {
   return attention_common(WMTP_VARIANT_PAGED_FULL, q, k_pool, v_pool, lens, nullptr, 1, out, lse, B,
                           Hq, Hkv, d, table_stride, 1, 0, 1, scale, ws, ws_bytes, err, stream,
                           req_to_token, pool_rows);
@@ -307,7 +307,7 @@ WMTP_EXPORT int wmtp_paged_attn_windowed(const void* q, const void* k_pool, cons
                                           void* out, float* lse, int B, int Hq, int Hkv, int d,
                                           int64_t pool_rows, int64_t table_stride, int W, int sink,
                                           float scale, void* ws, size_t ws_bytes, int32_t* err,
-                                          void* stream) {
+                                          hipStream_t stream) {
   return attention_common(WMTP_VARIANT_PAGED_WINDOWED, q, k_pool, v_pool, lens, nullptr, 1, out,
                           lse, B, Hq, Hkv, d, table_stride, W, sink, W, scale, ws, ws_bytes, err,
                           stream, req_to_token, pool_rows);
@@ -327,7 +327,7 @@ WMTP_EXPORT int64_t wmtp_kv_indices_capacity(int variant, int B, int64_t table_s
 WMTP_EXPORT int wmtp_build_kv_indices(const int32_t* req_to_token, const int32_t* lens, int B,
                                       int64_t table_stride, int variant, int W, int sink,
                                       int32_t* kv_indptr, int32_t* kv_indices, int64_t capacity,
-                                      int32_t* err, void* stream) {
+                                      int32_t* err, hipStream_t stream) {
   if (B < 0 || B > 65535 || table_stride < 0 || table_stride > INT_MAX) return WMTP_EINVAL;
   if (variant != WMTP_VARIANT_PAGED_FULL && variant != WMTP_VARIANT_PAGED_WINDOWED)
     return WMTP_EINVAL;
@@ -346,7 +346,7 @@ WMTP_EXPORT int wmtp_build_kv_indices(const int32_t* req_to_token, const int32_t
                                       : table_stride;
   if (wmtp::launch_kv_indices(req_to_token, table_stride, lens, B, windowed, W, sink, n_keys_max,
                               kv_indptr, kv_indices, err,
-                              static_cast<hipStream_t>(stream)) != hipSuccess)
+                              stream) != hipSuccess)
     return WMTP_ELAUNCH;
   return WMTP_OK;
 }
@@ -354,14 +354,14 @@ WMTP_EXPORT int wmtp_build_kv_indices(const int32_t* req_to_token, const int32_t
 WMTP_EXPORT int wmtp_ring_append(void* k_ring, void* v_ring, const void* k_new,
                                  const void* v_new, const int32_t* n_new, int32_t* lens, int B,
                                  int Hkv, int d, int sink, int R_w, int n_max, int32_t* err,
-                                 void* stream) {
+                                 hipStream_t stream) {
   return append_common(true, k_ring, v_ring, k_new, v_new, n_new, lens, B, Hkv, d, 0, sink, R_w,
                        n_max, err, stream);
 }
 
 WMTP_EXPORT int wmtp_cache_append(void* k, void* v, const void* k_new, const void* v_new,
                                   const int32_t* n_new, int32_t* lens, int B, int Hkv, int d,
-                                  int64_t S_max, int n_max, int32_t* err, void* stream) {
+                                  int64_t S_max, int n_max, int32_t* err, hipStream_t stream) {
   return append_common(false, k, v, k_new, v_new, n_new, lens, B, Hkv, d, S_max, 0, 1, n_max, err,
                        stream);
 }
@@ -370,7 +370,7 @@ WMTP_EXPORT int wmtp_draft_attn_full_fp8(const void* q, const void* k, const voi
                                          const int32_t* lens, void* out, float* lse, int B, int Hq,
                                          int Hkv, int d, int64_t S_max, float scale, float k_scale,
                                          float v_scale, void* ws, size_t ws_bytes, int32_t* err,
-                                         void* stream) {
+                                         hipStream_t stream) {
   return attention_common(WMTP_VARIANT_FULL, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv, d,
                           S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream, nullptr, 0, true,
                           k_scale, v_scale);
@@ -380,7 +380,7 @@ WMTP_EXPORT int wmtp_draft_attn_windowed_fp8(const void* q, const void* k, const
                                              const int32_t* lens, void* out, float* lse, int B,
                                              int Hq, int Hkv, int d, int64_t S_max, int W, int sink,
                                              float scale, float k_scale, float v_scale, void* ws,
-                                             size_t ws_bytes, int32_t* err, void* stream) {
+                                             size_t ws_bytes, int32_t* err, hipStream_t stream) {
   return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv,
                           d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream, nullptr, 0, true,
                           k_scale, v_scale);
@@ -390,7 +390,7 @@ WMTP_EXPORT int wmtp_draft_extend_full_fp8(const void* q, const void* k, const v
                                            const int32_t* lens, const int32_t* n_q, void* out,
                                            float* lse, int B, int q_max, int Hq, int Hkv, int d,
                                            int64_t S_max, float scale, float k_scale, float v_scale,
-                                           void* ws, size_t ws_bytes, int32_t* err, void* stream) {
+                                           void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream) {
   return attention_common(WMTP_VARIANT_FULL, q, k, v, lens, n_q, q_max, out, lse, B, Hq, Hkv, d,
                           S_max, 1, 0, 1, scale, ws, ws_bytes, err, stream, nullptr, 0, true,
                           k_scale, v_scale);
@@ -401,7 +401,7 @@ WMTP_EXPORT int wmtp_draft_extend_windowed_fp8(const void* q, const void* k, con
                                                float* lse, int B, int q_max, int Hq, int Hkv,
                                                int d, int64_t S_max, int W, int sink, float scale,
                                                float k_scale, float v_scale, void* ws,
-                                               size_t ws_bytes, int32_t* err, void* stream) {
+                                               size_t ws_bytes, int32_t* err, hipStream_t stream) {
   return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, n_q, q_max, out, lse, B, Hq, Hkv,
                           d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream, nullptr, 0, true,
                           k_scale, v_scale);
@@ -411,7 +411,7 @@ WMTP_EXPORT int wmtp_ring_extend_fp8(const void* q, const void* k_ring, const vo
                                      const int32_t* lens, const int32_t* n_q, void* out,
                                      float* lse, int B, int q_max, int Hq, int Hkv, int d, int W,
                                      int sink, int R_w, float scale, float k_scale, float v_scale,
-                                     void* ws, size_t ws_bytes, int32_t* err, void* stream) {
+                                     void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream) {
   if (check_window(W, sink) == WMTP_OK && static_cast<int64_t>(sink) + R_w > INT_MAX)
     return WMTP_EINVAL;
   return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, n_q, q_max, out, lse, B, Hq,
@@ -424,7 +424,7 @@ WMTP_EXPORT int wmtp_paged_attn_full_fp8(const void* q, const void* k_pool, cons
                                           float* lse, int B, int Hq, int Hkv, int d, int64_t pool_rows,
                                           int64_t table_stride, float scale, float k_scale,
                                           float v_scale, void* ws, size_t ws_bytes, int32_t* err,
-                                          void* stream) {
+                                          hipStream_t stream) {
   return attention_common(WMTP_VARIANT_PAGED_FULL, q, k_pool, v_pool, lens, nullptr, 1, out, lse, B,
                           Hq, Hkv, d, table_stride, 1, 0, 1, scale, ws, ws_bytes, err, stream,
                           req_to_token, pool_rows, true, k_scale, v_scale);
@@ -435,7 +435,7 @@ WMTP_EXPORT int wmtp_paged_attn_windowed_fp8(const void* q, const void* k_pool, 
                                               void* out, float* lse, int B, int Hq, int Hkv, int d,
                                               int64_t pool_rows, int64_t table_stride, int W,
                                               int sink, float scale, float k_scale, float v_scale,
-                                              void* ws, size_t ws_bytes, int32_t* err, void* stream) {
+                                              void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream) {
   return attention_common(WMTP_VARIANT_PAGED_WINDOWED, q, k_pool, v_pool, lens, nullptr, 1, out,
                           lse, B, Hq, Hkv, d, table_stride, W, sink, W, scale, ws, ws_bytes, err,
                           stream, req_to_token, pool_rows, true, k_scale, v_scale);
@@ -445,7 +445,7 @@ WMTP_EXPORT int wmtp_ring_attn_fp8(const void* q, const void* k_ring, const void
                                    const int32_t* lens, void* out, float* lse, int B, int Hq,
                                    int Hkv, int d, int W, int sink, int R_w, float scale,
                                    float k_scale, float v_scale, void* ws, size_t ws_bytes,
-                                   int32_t* err, void* stream) {
+                                   int32_t* err, hipStream_t stream) {
   if (check_window(W, sink) == WMTP_OK && (R_w < W || static_cast<int64_t>(sink) + R_w > INT_MAX))
     return WMTP_EINVAL;
   return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens, nullptr, 1, out, lse, B, Hq,
@@ -456,7 +456,7 @@ WMTP_EXPORT int wmtp_ring_attn_fp8(const void* q, const void* k_ring, const void
 WMTP_EXPORT int wmtp_ring_append_fp8(void* k_ring, void* v_ring, const void* k_new,
                                      const void* v_new, const int32_t* n_new, int32_t* lens, int B,
                                      int Hkv, int d, int sink, int R_w, int n_max, float k_scale,
-                                     float v_scale, int32_t* err, void* stream) {
+                                     float v_scale, int32_t* err, hipStream_t stream) {
   return append_common(true, k_ring, v_ring, k_new, v_new, n_new, lens, B, Hkv, d, 0, sink, R_w,
                        n_max, err, stream, true, k_scale, v_scale);
 }
@@ -464,7 +464,7 @@ WMTP_EXPORT int wmtp_ring_append_fp8(void* k_ring, void* v_ring, const void* k_n
 WMTP_EXPORT int wmtp_cache_append_fp8(void* k, void* v, const void* k_new, const void* v_new,
                                       const int32_t* n_new, int32_t* lens, int B, int Hkv, int d,
                                       int64_t S_max, int n_max, float k_scale, float v_scale,
-                                      int32_t* err, void* stream) {
+                                      int32_t* err, hipStream_t stream) {
   return append_common(false, k, v, k_new, v_new, n_new, lens, B, Hkv, d, S_max, 0, 1, n_max, err,
                        stream, true, k_scale, v_scale);
 }
@@ -474,7 +474,7 @@ WMTP_EXPORT int wmtp_draft_step_full(const void* q, void* k, void* v, const void
                                      const int32_t* lens_in, int32_t* lens_out, void* out,
                                      float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
                                      int n_max, float scale, void* ws, size_t ws_bytes,
-                                     int32_t* err, void* stream) {
+                                     int32_t* err, hipStream_t stream) {
   // The full-context step is the append (lens_in -> lens_out) followed by the
   // full attention at lens_out: reading the new rows through the fused path
   // costs the O(S) kernel more than the separate append launch saves.
@@ -499,7 +499,7 @@ WMTP_EXPORT int wmtp_draft_step_windowed(const void* q, void* k, void* v, const 
                                          const int32_t* lens_in, int32_t* lens_out, void* out,
                                          float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
                                          int n_max, int W, int sink, float scale, void* ws,
-                                         size_t ws_bytes, int32_t* err, void* stream) {
+                                         size_t ws_bytes, int32_t* err, hipStream_t stream) {
   return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens_in, n_new, 1, out, lse, B, Hq, Hkv,
                           d, S_max, W, sink, W, scale, ws, ws_bytes, err, stream, nullptr, 0, false,
                           1.0f, 1.0f, k_new, v_new, n_max, true, lens_out);
@@ -509,7 +509,7 @@ WMTP_EXPORT int wmtp_ring_step(const void* q, void* k_ring, void* v_ring, const 
                                const void* v_new, const int32_t* n_new, const int32_t* lens_in,
                                int32_t* lens_out, void* out, float* lse, int B, int Hq, int Hkv,
                                int d, int W, int sink, int R_w, int n_max, float scale, void* ws,
-                               size_t ws_bytes, int32_t* err, void* stream) {
+                               size_t ws_bytes, int32_t* err, hipStream_t stream) {
   if (check_window(W, sink) == WMTP_OK && (R_w < W || static_cast<int64_t>(sink) + R_w > INT_MAX))
     return WMTP_EINVAL;
   return attention_common(WMTP_VARIANT_RING, q, k_ring, v_ring, lens_in, n_new, 1, out, lse, B, Hq,
@@ -522,7 +522,7 @@ WMTP_EXPORT int wmtp_tree_attn(const void* q, const void* k_ring, const void* v_
                                const void* k_branch, const void* v_branch, const int32_t* lens,
                                const int32_t* depth, void* out, float* lse, int B, int width, int Hq,
                                int Hkv, int d, int W, int sink, int R_w, int depth_max, float scale,
-                               void* ws, size_t ws_bytes, int32_t* err, void* stream) {
+                               void* ws, size_t ws_bytes, int32_t* err, hipStream_t stream) {
   return attention_common(WMTP_VARIANT_TREE, q, k_ring, v_ring, lens, depth, width, out, lse, B, Hq,
                           Hkv, d, static_cast<int64_t>(sink) + R_w, W, sink, R_w, scale, ws,
                           ws_bytes, err, stream, nullptr, 0, false, 1.0f, 1.0f, k_branch, v_branch,
@@ -532,7 +532,7 @@ WMTP_EXPORT int wmtp_tree_attn(const void* q, const void* k_ring, const void* v_
 WMTP_EXPORT int wmtp_tree_append(void* k_ring, void* v_ring, void* k_branch, void* v_branch,
                                  const void* k_new, const void* v_new, const int32_t* lens,
                                  int32_t* depth, int B, int width, int Hkv, int d, int W, int sink,
-                                 int R_w, int depth_max, int32_t* err, void* stream) {
+                                 int R_w, int depth_max, int32_t* err, hipStream_t stream) {
   if (B < 0 || width < 1 || Hkv < 1 || d < 1 || depth_max < 1 || sink < 0 || check_window(W, sink))
     return WMTP_EINVAL;
   if (d != 64 && d != 128 && d != 256) return WMTP_EUNSUPPORTED;
@@ -566,55 +566,55 @@ WMTP_EXPORT int wmtp_tree_append(void* k_ring, void* v_ring, void* k_branch, voi
   L.sink = sink;
   L.R_w = R_w;
   L.dd = depth_max;
-  if (wmtp::launch_tree_append(L, static_cast<hipStream_t>(stream)) != hipSuccess) return WMTP_ELAUNCH;
+  if (wmtp::launch_tree_append(L, stream) != hipSuccess) return WMTP_ELAUNCH;
   return WMTP_OK;
 }
 
-WMTP_EXPORT int wmtp_tree_reset(int32_t* depth, int B, void* stream) {
+WMTP_EXPORT int wmtp_tree_reset(int32_t* depth, int B, hipStream_t stream) {
   if (B < 0) return WMTP_EINVAL;
   if (B == 0) return WMTP_OK;
   if (depth == nullptr || !aligned(depth, 4)) return WMTP_EINVAL;
-  if (wmtp::launch_rollback(depth, nullptr, B, nullptr, static_cast<hipStream_t>(stream)) != hipSuccess)
+  if (wmtp::launch_rollback(depth, nullptr, B, nullptr, stream) != hipSuccess)
     return WMTP_ELAUNCH;
   return WMTP_OK;
 }
 
 WMTP_EXPORT int wmtp_ring_rollback(int32_t* lens, const int32_t* n_drop, int B, int32_t* err,
-                                   void* stream) {
+                                   hipStream_t stream) {
   if (B < 0) return WMTP_EINVAL;
   if (B == 0) return WMTP_OK;
   if (lens == nullptr || n_drop == nullptr || !aligned(lens, 4) || !aligned(n_drop, 4) ||
       (err != nullptr && !aligned(err, 4)))
     return WMTP_EINVAL;
-  if (wmtp::launch_rollback(lens, n_drop, B, err, static_cast<hipStream_t>(stream)) != hipSuccess)
+  if (wmtp::launch_rollback(lens, n_drop, B, err, stream) != hipSuccess)
     return WMTP_ELAUNCH;
   return WMTP_OK;
 }
 
-WMTP_EXPORT int wmtp_fp8_quantize(const void* x, int64_t n, float scale, void* codes, void* stream) {
+WMTP_EXPORT int wmtp_fp8_quantize(const void* x, int64_t n, float scale, void* codes, hipStream_t stream) {
   if (n < 0 || n % 8 != 0 || !valid_scale(scale)) return WMTP_EINVAL;
   if (n == 0) return WMTP_OK;
   if (x == nullptr || codes == nullptr || !aligned(x, 16) || !aligned(codes, 8)) return WMTP_EINVAL;
   if (wmtp::launch_fp8_quantize(static_cast<const uint16_t*>(x), n, scale,
                                 static_cast<uint8_t*>(codes),
-                                static_cast<hipStream_t>(stream)) != hipSuccess)
+                                stream) != hipSuccess)
     return WMTP_ELAUNCH;
   return WMTP_OK;
 }
 
-WMTP_EXPORT int wmtp_fp8_dequantize(const void* codes, int64_t n, void* out, void* stream) {
+WMTP_EXPORT int wmtp_fp8_dequantize(const void* codes, int64_t n, void* out, hipStream_t stream) {
   if (n < 0 || n % 8 != 0) return WMTP_EINVAL;
   if (n == 0) return WMTP_OK;
   if (codes == nullptr || out == nullptr || !aligned(codes, 8) || !aligned(out, 16)) return WMTP_EINVAL;
   if (wmtp::launch_fp8_dequantize(static_cast<const uint8_t*>(codes), n, static_cast<uint16_t*>(out),
-                                  static_cast<hipStream_t>(stream)) != hipSuccess)
+                                  stream) != hipSuccess)
     return WMTP_ELAUNCH;
   return WMTP_OK;
 }
 
 WMTP_EXPORT int wmtp_select_indices(const int32_t* lens, int B, int W, int sink, int R_w,
                                     int32_t* pos_out, int32_t* slot_out, int32_t* n_sel_out,
-                                    int32_t* err, void* stream) {
+                                    int32_t* err, hipStream_t stream) {
   if (B < 0 || check_window(W, sink) != WMTP_OK) return WMTP_EINVAL;
   if (slot_out != nullptr && R_w < W) return WMTP_EINVAL;
   if (B == 0) return WMTP_OK;
@@ -623,16 +623,16 @@ WMTP_EXPORT int wmtp_select_indices(const int32_t* lens, int B, int W, int sink,
       (slot_out != nullptr && !aligned(slot_out, 4)) || (err != nullptr && !aligned(err, 4)))
     return WMTP_EINVAL;
   if (wmtp::launch_select(lens, B, W, sink, slot_out != nullptr ? R_w : W, pos_out, slot_out,
-                          n_sel_out, err, static_cast<hipStream_t>(stream)) != hipSuccess)
+                          n_sel_out, err, stream) != hipSuccess)
     return WMTP_ELAUNCH;
   return WMTP_OK;
 }
 
-WMTP_EXPORT int wmtp_hbm_read_probe(const void* buf, int64_t bytes, uint32_t* sink, void* stream) {
+WMTP_EXPORT int wmtp_hbm_read_probe(const void* buf, int64_t bytes, uint32_t* sink, hipStream_t stream) {
   if (bytes < 0 || bytes % 16 != 0) return WMTP_EINVAL;
   if (bytes == 0) return WMTP_OK;
   if (buf == nullptr || sink == nullptr || !aligned(buf, 16) || !aligned(sink, 4)) return WMTP_EINVAL;
-  if (wmtp::launch_hbm_read(buf, bytes, sink, static_cast<hipStream_t>(stream)) != hipSuccess)
+  if (wmtp::launch_hbm_read(buf, bytes, sink, stream) != hipSuccess)
     return WMTP_ELAUNCH;
   return WMTP_OK;
 }

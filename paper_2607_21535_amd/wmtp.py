@@ -123,7 +123,7 @@ _F = ctypes.c_float
 _SZ = ctypes.c_size_t
 
 _SIGNATURES = {
-    "wmtp_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I64, _I, _I]),
+    "wmtp_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I64, _I, _I, _I]),
     "wmtp_draft_attn_full": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _F, _P, _SZ, _P, _P]),
     "wmtp_draft_attn_windowed": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _F, _P, _SZ, _P, _P]),
     "wmtp_ring_attn": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P, _SZ, _P, _P]),
@@ -180,7 +180,7 @@ class WmtpError(RuntimeError):
 
 # The version of include/wmtp.h these signatures follow, (major << 16) | minor:
 # a library of another major version, or an older minor one, is refused.
-ABI_VERSION = (1 << 16) | 6
+ABI_VERSION = (2 << 16) | 0
 
 
 def lib_path() -> str:
@@ -241,15 +241,18 @@ def _need(t, name, dtype, ndim=None, device=None):
         raise ValueError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
 
 
-def workspace_bytes(variant, B, Hq, Hkv, d, S_max=0, W=1, sink=0) -> int:
-    return int(load_library().wmtp_workspace_bytes(variant, B, Hq, Hkv, d, S_max, W, sink))
+def workspace_bytes(B, Hq, Hkv, d, S_max=0, W=1, sink=0, variant=VARIANT_FULL) -> int:
+    """wmtp_workspace_bytes: bytes of the workspace one attention call of
+    this variant and shape needs (zero-filled once before its first use)."""
+    return int(load_library().wmtp_workspace_bytes(B, Hq, Hkv, d, S_max, W, sink, variant))
 
 
 def _workspace(ws, nbytes, device):
+    """The caller's workspace (checked for size), or a new zero-filled one."""
     if ws is None:
         if nbytes == 0:
             return None
-        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+        return torch.zeros(nbytes, dtype=torch.uint8, device=device)
     if ws.numel() * ws.element_size() < nbytes:
         raise WmtpError(EWORKSPACE, "workspace")
     return ws
@@ -294,7 +297,7 @@ def draft_attn_full(q, k, v, lens, out=None, lse=None, scale=None, ws=None, err=
     dev, B, Hq, d, out = _attn_io(q, k, v, lens, out, lse)
     S_max, Hkv = k.shape[1], k.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    nb = workspace_bytes(VARIANT_FULL, B, Hq, Hkv, d, S_max)
+    nb = workspace_bytes(B, Hq, Hkv, d, S_max, variant=VARIANT_FULL)
     ws = _workspace(ws, nb, dev)
     st = load_library().wmtp_draft_attn_full(
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, S_max, scale,
@@ -308,7 +311,7 @@ def draft_attn_windowed(q, k, v, lens, W, sink, out=None, lse=None, scale=None, 
     dev, B, Hq, d, out = _attn_io(q, k, v, lens, out, lse)
     S_max, Hkv = k.shape[1], k.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    nb = workspace_bytes(VARIANT_WINDOWED, B, Hq, Hkv, d, S_max, W, sink)
+    nb = workspace_bytes(B, Hq, Hkv, d, S_max, W, sink, variant=VARIANT_WINDOWED)
     ws = _workspace(ws, nb, dev)
     st = load_library().wmtp_draft_attn_windowed(
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, S_max, W, sink,
@@ -324,7 +327,7 @@ def ring_attn(q, k_ring, v_ring, lens, W, sink, R_w, out=None, lse=None, scale=N
         raise ValueError(f"ring must hold sink + R_w = {sink + R_w} rows, has {k_ring.shape[1]}")
     Hkv = k_ring.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    nb = workspace_bytes(VARIANT_RING, B, Hq, Hkv, d, sink + R_w, W, sink)
+    nb = workspace_bytes(B, Hq, Hkv, d, sink + R_w, W, sink, variant=VARIANT_RING)
     ws = _workspace(ws, nb, dev)
     st = load_library().wmtp_ring_attn(
         _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, W, sink,
@@ -373,7 +376,7 @@ def draft_extend_full(q, k, v, lens, n_q=None, out=None, lse=None, scale=None, w
     dev, B, q_max, Hq, d, out = _extend_io(q, k, v, lens, n_q, out, lse)
     S_max, Hkv = k.shape[1], k.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_FULL, B * q_max, Hq, Hkv, d, S_max), dev)
+    ws = _workspace(ws, workspace_bytes(B * q_max, Hq, Hkv, d, S_max, variant=VARIANT_FULL), dev)
     st = load_library().wmtp_draft_extend_full(
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq, Hkv, d,
         S_max, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -387,7 +390,7 @@ def draft_extend_windowed(q, k, v, lens, W, sink, n_q=None, out=None, lse=None, 
     dev, B, q_max, Hq, d, out = _extend_io(q, k, v, lens, n_q, out, lse)
     S_max, Hkv = k.shape[1], k.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_WINDOWED, B * q_max, Hq, Hkv, d, S_max, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B * q_max, Hq, Hkv, d, S_max, W, sink, variant=VARIANT_WINDOWED), dev)
     st = load_library().wmtp_draft_extend_windowed(
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq, Hkv, d,
         S_max, W, sink, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -403,7 +406,7 @@ def ring_extend(q, k_ring, v_ring, lens, W, sink, R_w, n_q=None, out=None, lse=N
         raise ValueError(f"ring must hold sink + R_w = {sink + R_w} rows, has {k_ring.shape[1]}")
     Hkv = k_ring.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_RING, B * q_max, Hq, Hkv, d, sink + R_w, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B * q_max, Hq, Hkv, d, sink + R_w, W, sink, variant=VARIANT_RING), dev)
     st = load_library().wmtp_ring_extend(
         _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq,
         Hkv, d, W, sink, R_w, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -440,7 +443,7 @@ def paged_attn_full(q, k_pool, v_pool, req_to_token, lens, out=None, lse=None, s
     P, Hkv = k_pool.shape[0], k_pool.shape[1]
     C = req_to_token.shape[1]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_PAGED_FULL, B, Hq, Hkv, d, C), dev)
+    ws = _workspace(ws, workspace_bytes(B, Hq, Hkv, d, C, variant=VARIANT_PAGED_FULL), dev)
     st = load_library().wmtp_paged_attn_full(
         _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(req_to_token), _ptr(lens), _ptr(out), _ptr(lse), B, Hq,
         Hkv, d, P, C, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -455,7 +458,7 @@ def paged_attn_windowed(q, k_pool, v_pool, req_to_token, lens, W, sink, out=None
     P, Hkv = k_pool.shape[0], k_pool.shape[1]
     C = req_to_token.shape[1]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_PAGED_WINDOWED, B, Hq, Hkv, d, C, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B, Hq, Hkv, d, C, W, sink, variant=VARIANT_PAGED_WINDOWED), dev)
     st = load_library().wmtp_paged_attn_windowed(
         _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(req_to_token), _ptr(lens), _ptr(out), _ptr(lse), B, Hq,
         Hkv, d, P, C, W, sink, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -543,7 +546,7 @@ def draft_attn_full_fp8(q, k, v, lens, k_scale=1.0, v_scale=1.0, out=None, lse=N
     dev, B, Hq, d, out = _attn_io(q, k, v, lens, out, lse, fp8=True)
     S_max, Hkv = k.shape[1], k.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_FULL, B, Hq, Hkv, d, S_max), dev)
+    ws = _workspace(ws, workspace_bytes(B, Hq, Hkv, d, S_max, variant=VARIANT_FULL), dev)
     st = load_library().wmtp_draft_attn_full_fp8(
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, S_max, scale,
         *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -557,7 +560,7 @@ def draft_attn_windowed_fp8(q, k, v, lens, W, sink, k_scale=1.0, v_scale=1.0, ou
     dev, B, Hq, d, out = _attn_io(q, k, v, lens, out, lse, fp8=True)
     S_max, Hkv = k.shape[1], k.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_WINDOWED, B, Hq, Hkv, d, S_max, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B, Hq, Hkv, d, S_max, W, sink, variant=VARIANT_WINDOWED), dev)
     st = load_library().wmtp_draft_attn_windowed_fp8(
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, S_max, W, sink, scale,
         *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -573,7 +576,7 @@ def ring_attn_fp8(q, k_ring, v_ring, lens, W, sink, R_w, k_scale=1.0, v_scale=1.
         raise ValueError(f"ring must hold sink + R_w = {sink + R_w} rows, has {k_ring.shape[1]}")
     Hkv = k_ring.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_RING, B, Hq, Hkv, d, sink + R_w, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B, Hq, Hkv, d, sink + R_w, W, sink, variant=VARIANT_RING), dev)
     st = load_library().wmtp_ring_attn_fp8(
         _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, W, sink, R_w,
         scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -588,7 +591,7 @@ def paged_attn_full_fp8(q, k_pool, v_pool, req_to_token, lens, k_scale=1.0, v_sc
     P, Hkv = k_pool.shape[0], k_pool.shape[1]
     C = req_to_token.shape[1]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_PAGED_FULL, B, Hq, Hkv, d, C), dev)
+    ws = _workspace(ws, workspace_bytes(B, Hq, Hkv, d, C, variant=VARIANT_PAGED_FULL), dev)
     st = load_library().wmtp_paged_attn_full_fp8(
         _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(req_to_token), _ptr(lens), _ptr(out), _ptr(lse), B, Hq,
         Hkv, d, P, C, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -603,7 +606,7 @@ def paged_attn_windowed_fp8(q, k_pool, v_pool, req_to_token, lens, W, sink, k_sc
     P, Hkv = k_pool.shape[0], k_pool.shape[1]
     C = req_to_token.shape[1]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_PAGED_WINDOWED, B, Hq, Hkv, d, C, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B, Hq, Hkv, d, C, W, sink, variant=VARIANT_PAGED_WINDOWED), dev)
     st = load_library().wmtp_paged_attn_windowed_fp8(
         _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(req_to_token), _ptr(lens), _ptr(out), _ptr(lse), B, Hq,
         Hkv, d, P, C, W, sink, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -617,7 +620,7 @@ def draft_extend_full_fp8(q, k, v, lens, k_scale=1.0, v_scale=1.0, n_q=None, out
     dev, B, q_max, Hq, d, out = _extend_io(q, k, v, lens, n_q, out, lse, fp8=True)
     S_max, Hkv = k.shape[1], k.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_FULL, B * q_max, Hq, Hkv, d, S_max), dev)
+    ws = _workspace(ws, workspace_bytes(B * q_max, Hq, Hkv, d, S_max, variant=VARIANT_FULL), dev)
     st = load_library().wmtp_draft_extend_full_fp8(
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq, Hkv, d,
         S_max, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -631,7 +634,7 @@ def draft_extend_windowed_fp8(q, k, v, lens, W, sink, k_scale=1.0, v_scale=1.0, 
     dev, B, q_max, Hq, d, out = _extend_io(q, k, v, lens, n_q, out, lse, fp8=True)
     S_max, Hkv = k.shape[1], k.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_WINDOWED, B * q_max, Hq, Hkv, d, S_max, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B * q_max, Hq, Hkv, d, S_max, W, sink, variant=VARIANT_WINDOWED), dev)
     st = load_library().wmtp_draft_extend_windowed_fp8(
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq, Hkv, d,
         S_max, W, sink, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -647,7 +650,7 @@ def ring_extend_fp8(q, k_ring, v_ring, lens, W, sink, R_w, k_scale=1.0, v_scale=
         raise ValueError(f"ring must hold sink + R_w = {sink + R_w} rows, has {k_ring.shape[1]}")
     Hkv = k_ring.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_RING, B * q_max, Hq, Hkv, d, sink + R_w, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B * q_max, Hq, Hkv, d, sink + R_w, W, sink, variant=VARIANT_RING), dev)
     st = load_library().wmtp_ring_extend_fp8(
         _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq,
         Hkv, d, W, sink, R_w, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -791,7 +794,7 @@ def tree_attn(q, k_ring, v_ring, k_branch, v_branch, lens, depth, W, sink, R_w, 
         if tuple(lse.shape) != (B, width, Hq):
             raise ValueError("lse must be [B, width, Hq]")
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_TREE, B * width, Hq, Hkv, d, 0, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B * width, Hq, Hkv, d, 0, W, sink, variant=VARIANT_TREE), dev)
     st = load_library().wmtp_tree_attn(
         _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(k_branch), _ptr(v_branch), _ptr(lens), _ptr(depth), _ptr(out),
         _ptr(lse), B, width, Hq, Hkv, d, W, sink, R_w, depth_max, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -827,7 +830,7 @@ def draft_step_full(q, k, v, k_new, v_new, n_new, lens_in, lens_out, out=None, l
     dev, B, Hq, Hkv, d, n_max, out = _step_io(q, k, v, k_new, v_new, n_new, lens_in, lens_out, out, lse)
     S_max = k.shape[1]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_FULL, B, Hq, Hkv, d, S_max), dev)
+    ws = _workspace(ws, workspace_bytes(B, Hq, Hkv, d, S_max, variant=VARIANT_FULL), dev)
     st = load_library().wmtp_draft_step_full(
         _ptr(q), _ptr(k), _ptr(v), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(lens_in), _ptr(lens_out), _ptr(out),
         _ptr(lse), B, Hq, Hkv, d, S_max, n_max, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -841,7 +844,7 @@ def draft_step_windowed(q, k, v, k_new, v_new, n_new, lens_in, lens_out, W, sink
     dev, B, Hq, Hkv, d, n_max, out = _step_io(q, k, v, k_new, v_new, n_new, lens_in, lens_out, out, lse)
     S_max = k.shape[1]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_WINDOWED, B, Hq, Hkv, d, S_max, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B, Hq, Hkv, d, S_max, W, sink, variant=VARIANT_WINDOWED), dev)
     st = load_library().wmtp_draft_step_windowed(
         _ptr(q), _ptr(k), _ptr(v), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(lens_in), _ptr(lens_out), _ptr(out),
         _ptr(lse), B, Hq, Hkv, d, S_max, n_max, W, sink, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -856,7 +859,7 @@ def ring_step(q, k_ring, v_ring, k_new, v_new, n_new, lens_in, lens_out, W, sink
     if k_ring.shape[1] != sink + R_w:
         raise ValueError(f"ring must hold sink + R_w = {sink + R_w} rows, has {k_ring.shape[1]}")
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(VARIANT_RING, B, Hq, Hkv, d, sink + R_w, W, sink), dev)
+    ws = _workspace(ws, workspace_bytes(B, Hq, Hkv, d, sink + R_w, W, sink, variant=VARIANT_RING), dev)
     st = load_library().wmtp_ring_step(
         _ptr(q), _ptr(k_ring), _ptr(v_ring), _ptr(k_new), _ptr(v_new), _ptr(n_new), _ptr(lens_in), _ptr(lens_out),
         _ptr(out), _ptr(lse), B, Hq, Hkv, d, W, sink, R_w, n_max, scale, _ptr(ws), _wsize(ws), _ptr(err),

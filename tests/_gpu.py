@@ -1,15 +1,26 @@
 """Helpers shared by the GPU parity tests (not collected by pytest).
 
 Parity bar (floating point, all variants):
-  * max |o - o_ref| <= 1e-2 over every output element (the contract) on the
-    five workloads, where |o_ref| < 1; for the small edge cases (a handful
-    of keys, |o_ref| up to ~4) the elementwise bar is
-    max(1e-2, 2^-8 |o_ref| + 1e-4): bf16 output rounding alone moves an
-    element by up to 2^-8 of its magnitude, 1.6e-2 at |o| = 4;
+  * max |o - o_ref| <= 1e-2 over every output element (the contract).  Where
+    the oracle also supplies the value spread (oracle.attention.value_spread,
+    s = sum_p w_p |v_p - o_ref| per element), an element may instead be
+    within the rounding the kernels' arithmetic provably allows, if that is
+    larger (rows with a handful of keys and large values):
+        e   = r / (1 - r) * s + 2^-12 * (s + 2 |o_ref|)
+        bound = max(1e-2, 2^-8 (|o_ref| + e) + e),   r = 2^-8 + 2^-10.
+    Derivation: the weights enter the value product rounded to bfloat16 and
+    the output is normalised by the sum of the same rounded weights; a
+    relative perturbation of at most r per weight moves the normalised sum
+    by at most r / (1 - r) * s.  Round to nearest even to bfloat16 has unit
+    roundoff 2^-8 (8 significant bits); the remaining 2^-10 of r covers the
+    fp32 logits (d products summed in fp32, the scale folded in fp32), the
+    hardware exp2 and the fp32 rescaling factors.  2^-12 covers the fp32
+    sums of the weighted values and of the weights (a few hundred additions
+    deep: the tiles of a work item, the waves, the items of the merge), and
+    the final bfloat16 rounding adds 2^-8 of the value rounded;
   * per (b, h): ||o - o_ref||_2 <= 5e-3 * ||o_ref||_2.  Rounding the output
     to bfloat16 alone moves each element by at most 2^-8 of its magnitude
-    (half an ulp with 8 significant bits), i.e. <= 3.9e-3 normwise; the fp32
-    logits and sums add far less (< 1e-5 relative at 1M keys);
+    (half an ulp with 8 significant bits), i.e. <= 3.9e-3 normwise;
   * lse: |lse - lse_ref| <= 1e-4 * max(1, |lse_ref|), -inf exactly for empty
     sequences.
 Integer, index and byte results (selected positions, ring slots, cache
@@ -31,7 +42,9 @@ from paper_2607_21535_amd import wmtp as W
 ATOL = 1e-2
 NREL = 5e-3
 LSE_REL = 1e-4
-BF16_REL = 2.0 ** -8
+U_BF16 = 2.0 ** -8          # unit roundoff of round-to-nearest-even to bfloat16
+R_WEIGHT = 2.0 ** -8 + 2.0 ** -10  # relative perturbation budget of one weight
+R_SUM = 2.0 ** -12          # fp32 summation budget
 
 
 def device():
@@ -59,29 +72,38 @@ class HostRows:
         return I.bf16_bits(self.t.index_select(0, idx))
 
 
-def oracle_seq(q_bits, k_dev_seq, v_dev_seq, S, scale, variant, W_=None, sink=None):
-    """Oracle output for one sequence whose cache lives on the device."""
+def oracle_seq(q_bits, k_dev_seq, v_dev_seq, S, scale, variant, W_=None, sink=None, spread=False):
+    """Oracle output for one sequence whose cache lives on the device;
+    with spread=True also the value spread (for the elementwise bound)."""
     mask = None if variant == "full" else A.window_mask(S, W_, sink)
-    return A.attend_sequence(q_bits, HostRows(k_dev_seq), HostRows(v_dev_seq), S, scale, mask)
+    K, V = HostRows(k_dev_seq), HostRows(v_dev_seq)
+    o, lse = A.attend_sequence(q_bits, K, V, S, scale, mask)
+    if not spread:
+        return o, lse
+    return o, lse, A.value_spread(q_bits, K, V, S, scale, mask)
 
 
-def assert_attn_close(out, o_ref, lse=None, lse_ref=None, what="", strict=True, v_max=None):
-    """Output within the contract's max-abs tolerance (strict) or, for small
-    cases with large outputs, within the bf16 rounding of the output itself;
-    v_max (the largest |value| the call can combine) adds the error of the
-    weights entering the PV product rounded to bf16: each moves by at most
-    2^-9 relative, so the output moves by at most 2^-9 max_i |v_i - o|, and
-    that is at most 2^-8 v_max.  Rows with few keys and a wide spread of
-    values reach it.  Also checks the normwise error per row and the lse."""
+def elementwise_bound(o_ref, spread):
+    """Per-element bound: the 1e-2 contract, or the provable rounding of the
+    kernels' arithmetic when that is larger (see the module docstring)."""
+    o_abs = np.abs(o_ref)
+    s = np.asarray(spread, dtype=np.float64).reshape(o_abs.shape)
+    e = R_WEIGHT / (1.0 - R_WEIGHT) * s + R_SUM * (s + 2.0 * o_abs)
+    return np.maximum(ATOL, U_BF16 * (o_abs + e) + e)
+
+
+def assert_attn_close(out, o_ref, lse=None, lse_ref=None, what="", spread=None):
+    """Output within the contract's max-abs tolerance, or (spread given)
+    within elementwise_bound; also the normwise error per row and the lse."""
     o = out.detach().float().cpu().numpy().astype(np.float64)
     o_ref = np.asarray(o_ref, dtype=np.float64).reshape(o.shape)
     d = o.shape[-1]
     err = np.abs(o - o_ref)
     assert np.all(np.isfinite(o)), f"{what}: non-finite output"
-    bound = ATOL if strict else np.maximum(ATOL, BF16_REL * np.abs(o_ref) + 1e-4)
-    if v_max is not None:
-        bound = bound + 2.0 ** -8 * float(v_max)
-    assert np.all(err <= bound), f"{what}: max abs err {err.max():.3e} (|o_ref| max {np.abs(o_ref).max():.2f})"
+    bound = ATOL if spread is None else elementwise_bound(o_ref, spread)
+    bad = err > bound
+    assert not bad.any(), (f"{what}: max abs err {err.max():.3e} (|o_ref| max {np.abs(o_ref).max():.2f}); "
+                           f"worst excess {np.max(err - bound):.3e} at {np.argwhere(bad)[:4].tolist()}")
     num = np.linalg.norm((o - o_ref).reshape(-1, d), axis=1)
     den = np.linalg.norm(o_ref.reshape(-1, d), axis=1)
     bad = num > NREL * den

@@ -112,12 +112,12 @@ int main(void) {
   hip_ok(hipMemcpy(lens, lens_h, sizeof(lens_h), hipMemcpyHostToDevice), "lens");
   hip_ok(hipMemset(err, 0, sizeof(int32_t)), "err = 0");
 
-  size_t ws_bytes = wmtp_workspace_bytes(WMTP_VARIANT_FULL, B, HQ, HKV, D, S_MAX, W, SINK);
-  const size_t ws_win = wmtp_workspace_bytes(WMTP_VARIANT_WINDOWED, B, HQ, HKV, D, S_MAX, W, SINK);
-  const size_t ws_ring = wmtp_workspace_bytes(WMTP_VARIANT_RING, B, HQ, HKV, D, SINK + R_W, W, SINK);
-  const size_t ws_ext = wmtp_workspace_bytes(WMTP_VARIANT_WINDOWED, B * QMAX, HQ, HKV, D, S_MAX, W, SINK);
-  const size_t ws_pool = wmtp_workspace_bytes(WMTP_VARIANT_PAGED_WINDOWED, B, HQ, HKV, D, S_MAX, W, SINK);
-  const size_t ws_tree = wmtp_workspace_bytes(WMTP_VARIANT_TREE, B * WIDTH, HQ, HKV, D, 0, W, SINK);
+  size_t ws_bytes = wmtp_workspace_bytes(B, HQ, HKV, D, S_MAX, W, SINK, WMTP_VARIANT_FULL);
+  const size_t ws_win = wmtp_workspace_bytes(B, HQ, HKV, D, S_MAX, W, SINK, WMTP_VARIANT_WINDOWED);
+  const size_t ws_ring = wmtp_workspace_bytes(B, HQ, HKV, D, SINK + R_W, W, SINK, WMTP_VARIANT_RING);
+  const size_t ws_ext = wmtp_workspace_bytes(B * QMAX, HQ, HKV, D, S_MAX, W, SINK, WMTP_VARIANT_WINDOWED);
+  const size_t ws_pool = wmtp_workspace_bytes(B, HQ, HKV, D, S_MAX, W, SINK, WMTP_VARIANT_PAGED_WINDOWED);
+  const size_t ws_tree = wmtp_workspace_bytes(B * WIDTH, HQ, HKV, D, 0, W, SINK, WMTP_VARIANT_TREE);
   check(ws_bytes > 0 && ws_win > 0 && ws_ring > 0 && ws_ext > 0 && ws_pool > 0, "workspace sizes are positive");
   if (ws_win > ws_bytes) ws_bytes = ws_win;
   if (ws_ring > ws_bytes) ws_bytes = ws_ring;
@@ -125,6 +125,7 @@ int main(void) {
   if (ws_pool > ws_bytes) ws_bytes = ws_pool;
   if (ws_tree > ws_bytes) ws_bytes = ws_tree;
   void* ws = dev_alloc(ws_bytes);
+  hip_ok(hipMemset(ws, 0, ws_bytes), "workspace zero-filled once");
   const float scale = 1.0f / sqrtf((float)D);
 
   /* Full context: every key. */

@@ -55,31 +55,31 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.wmtp_abi_version() == (1 << 16) | 6
+    assert lib.wmtp_abi_version() == (2 << 16) | 0
     # the header, the library and the binding's signatures agree
     with open(os.path.join(ROOT, "include", "wmtp.h")) as f:
-        m = re.search(r"#define WMTP_ABI_VERSION \(\(1 << 16\) \| (\d+)\)", f.read())
-    assert m is not None and W.ABI_VERSION == (1 << 16) | int(m.group(1)) == lib.wmtp_abi_version()
+        m = re.search(r"#define WMTP_ABI_VERSION \(\(2 << 16\) \| (\d+)\)", f.read())
+    assert m is not None and W.ABI_VERSION == (2 << 16) | int(m.group(1)) == lib.wmtp_abi_version()
     for code in range(5):
         assert W.status_string(code).startswith("WMTP_")
     assert "unknown" in W.status_string(99)
 
 
 def test_workspace_bytes_shapes():
-    full = W.workspace_bytes(W.VARIANT_FULL, 1, 32, 2, 256, 1 << 20)
-    win = W.workspace_bytes(W.VARIANT_WINDOWED, 1, 32, 2, 256, 1 << 20, 2048, 4)
-    ring = W.workspace_bytes(W.VARIANT_RING, 1, 32, 2, 256, 0, 2048, 4)
+    full = W.workspace_bytes(1, 32, 2, 256, 1 << 20, variant=W.VARIANT_FULL)
+    win = W.workspace_bytes(1, 32, 2, 256, 1 << 20, 2048, 4, variant=W.VARIANT_WINDOWED)
+    ring = W.workspace_bytes(1, 32, 2, 256, 0, 2048, 4, variant=W.VARIANT_RING)
     assert full > win > 0
     assert win == ring  # windowed and ring share one split plan
     # windowed workspace does not grow with the cache length
-    assert W.workspace_bytes(W.VARIANT_WINDOWED, 1, 32, 2, 256, 1 << 17, 2048, 4) == win
-    assert W.workspace_bytes(W.VARIANT_FULL, 1, 32, 2, 256, 0) == 0
-    assert W.workspace_bytes(W.VARIANT_FULL, 0, 32, 2, 256, 1000) == 0
+    assert W.workspace_bytes(1, 32, 2, 256, 1 << 17, 2048, 4, variant=W.VARIANT_WINDOWED) == win
+    assert W.workspace_bytes(1, 32, 2, 256, 0, variant=W.VARIANT_FULL) == 0
+    assert W.workspace_bytes(0, 32, 2, 256, 1000, variant=W.VARIANT_FULL) == 0
     # invalid shapes size to 0
-    assert W.workspace_bytes(W.VARIANT_FULL, 1, 32, 3, 256, 1000) == 0
-    assert W.workspace_bytes(W.VARIANT_FULL, 1, 32, 2, 96, 1000) == 0
-    assert W.workspace_bytes(7, 1, 32, 2, 256, 1000) == 0
-    assert W.workspace_bytes(W.VARIANT_WINDOWED, 1, 32, 2, 256, 1000, 0, 4) == 0
+    assert W.workspace_bytes(1, 32, 3, 256, 1000, variant=W.VARIANT_FULL) == 0
+    assert W.workspace_bytes(1, 32, 2, 96, 1000, variant=W.VARIANT_FULL) == 0
+    assert W.workspace_bytes(1, 32, 2, 256, 1000, variant=7) == 0
+    assert W.workspace_bytes(1, 32, 2, 256, 1000, 0, 4, variant=W.VARIANT_WINDOWED) == 0
 
 
 def _full(lib, **kw):
@@ -131,7 +131,7 @@ def test_attention_argument_checks(lib, call):
 @fake_pointers
 def test_full_specific_checks(lib):
     assert _full(lib, S_max=-1) == W.EINVAL
-    assert W.workspace_bytes(W.VARIANT_FULL, 1, 16, 2, 128, 0) == 0
+    assert W.workspace_bytes(1, 16, 2, 128, 0, variant=W.VARIANT_FULL) == 0
 
 
 @fake_pointers
@@ -411,8 +411,8 @@ def test_tree_attn_specific_checks(lib):
     assert _tattn(lib, ws_bytes=1) == W.EWORKSPACE
     assert _tattn(lib, q=None) == W.EINVAL
     assert _tattn(lib, Hq=64, Hkv=2) == W.EUNSUPPORTED
-    assert W.workspace_bytes(W.VARIANT_TREE, 6, 16, 2, 128, 0, 8, 4) == \
-        W.workspace_bytes(W.VARIANT_RING, 6, 16, 2, 128, 12, 8, 4)
+    assert W.workspace_bytes(6, 16, 2, 128, 0, 8, 4, variant=W.VARIANT_TREE) == \
+        W.workspace_bytes(6, 16, 2, 128, 12, 8, 4, variant=W.VARIANT_RING)
 
 
 @fake_pointers

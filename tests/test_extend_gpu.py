@@ -39,13 +39,16 @@ def _ring_from_dense(k, lens, sink, R_w):
 
 
 def _oracle(q, k, v, lens, n_q, scale, variant, W_=None, sink=None):
+    """Oracle outputs, lse and value spreads of every sequence's new rows."""
     qb = I.bf16_bits(q)
-    outs, lses = [], []
+    outs, lses, spreads = [], [], []
     for b, (S, n) in enumerate(zip(lens, n_q)):
-        o, l = A.attend_extend(qb[b], G.HostRows(k[b]), G.HostRows(v[b]), S, n, scale, variant, W_, sink)
+        K, V = G.HostRows(k[b]), G.HostRows(v[b])
+        o, l = A.attend_extend(qb[b], K, V, S, n, scale, variant, W_, sink)
         outs.append(o)
         lses.append(l)
-    return np.stack(outs), np.stack(lses)
+        spreads.append(A.extend_spread(qb[b], K, V, S, n, scale, variant, W_, sink))
+    return np.stack(outs), np.stack(lses), np.stack(spreads)
 
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(64, 6, 2), (128, 16, 2), (256, 32, 2), (256, 8, 8)])
@@ -72,8 +75,8 @@ def test_extend_vs_oracle(dev, d, Hq, Hkv, q_max):
         else:
             out = W.draft_extend_windowed(q, k, v, lt, W_, sink, n_q=nt, lse=lse, err=err)
         torch.cuda.synchronize()
-        o_ref, l_ref = _oracle(q, k, v, lens, n_q, scale, variant, W_, sink)
-        G.assert_attn_close(out, o_ref, lse, l_ref, what=f"extend {variant}", strict=False)
+        o_ref, l_ref, spread = _oracle(q, k, v, lens, n_q, scale, variant, W_, sink)
+        G.assert_attn_close(out, o_ref, lse, l_ref, what=f"extend {variant}", spread=spread)
     assert err.item() == 0
     # a ring sized exactly W + q_max - 1 gives the windowed result bit for bit
     R_w = W_ + q_max - 1
@@ -102,8 +105,8 @@ def test_full_extend_many_rows(dev, d, Hq, Hkv, q_max):
     err = G.err_word(dev)
     out = W.draft_extend_full(q, k, v, lt, n_q=nt, lse=lse, err=err)
     torch.cuda.synchronize()
-    o_ref, l_ref = _oracle(q, k, v, lens, n_q, 1.0 / np.sqrt(d), "full")
-    G.assert_attn_close(out, o_ref, lse, l_ref, what="extend many rows", strict=False)
+    o_ref, l_ref, spread = _oracle(q, k, v, lens, n_q, 1.0 / np.sqrt(d), "full")
+    G.assert_attn_close(out, o_ref, lse, l_ref, what="extend many rows", spread=spread)
     assert err.item() == 0
 
 
@@ -153,7 +156,7 @@ def test_extend_s1m_draft_depth8(dev):
     ow = W.draft_extend_windowed(q, k, v, lt, wl.W, wl.sink, n_q=nt, lse=lse_w)
     of = W.draft_extend_full(q, k, v, lt, n_q=nt, lse=lse_f)
     torch.cuda.synchronize()
-    o_ref, l_ref = _oracle(q, k, v, [S], [q_max], wl.scale, "windowed", wl.W, wl.sink)
+    o_ref, l_ref, _ = _oracle(q, k, v, [S], [q_max], wl.scale, "windowed", wl.W, wl.sink)
     G.say(f"extend 1M windowed err {G.assert_attn_close(ow, o_ref, lse_w, l_ref, 'extend 1M windowed')}")
     qb = I.bf16_bits(q)
     for t in (0, 3, q_max - 1):

@@ -36,8 +36,8 @@ def test_graph_replay_matches_eager():
     lens = lens0.clone()
     outs_f = torch.empty((gamma, 1, Hq, d), dtype=torch.bfloat16, device=dev)
     outs_w = torch.empty_like(outs_f)
-    ws_f = torch.empty(W.workspace_bytes(W.VARIANT_FULL, 1, Hq, Hkv, d, S + gamma), dtype=torch.uint8, device=dev)
-    ws_w = torch.empty(W.workspace_bytes(W.VARIANT_WINDOWED, 1, Hq, Hkv, d, S + gamma, Wn, sink),
+    ws_f = torch.zeros(W.workspace_bytes(1, Hq, Hkv, d, S + gamma, variant=W.VARIANT_FULL), dtype=torch.uint8, device=dev)
+    ws_w = torch.zeros(W.workspace_bytes(1, Hq, Hkv, d, S + gamma, Wn, sink, variant=W.VARIANT_WINDOWED),
                        dtype=torch.uint8, device=dev)
 
     def loop():
@@ -125,8 +125,8 @@ def test_graph_extend_dense_and_ring():
     vr = torch.zeros_like(kr)
     lens, lens_r = G.lens_tensor(S0, dev), G.lens_tensor(S0, dev)
     outs = [torch.empty_like(q) for _ in range(3)]
-    ws = torch.empty(W.workspace_bytes(W.VARIANT_FULL, B * qm, Hq, Hkv, d, 500), dtype=torch.uint8, device=dev)
-    ws_w = torch.empty(W.workspace_bytes(W.VARIANT_WINDOWED, B * qm, Hq, Hkv, d, 500, Wn, sink),
+    ws = torch.zeros(W.workspace_bytes(B * qm, Hq, Hkv, d, 500, variant=W.VARIANT_FULL), dtype=torch.uint8, device=dev)
+    ws_w = torch.zeros(W.workspace_bytes(B * qm, Hq, Hkv, d, 500, Wn, sink, variant=W.VARIANT_WINDOWED),
                        dtype=torch.uint8, device=dev)
 
     def reset():
@@ -160,8 +160,8 @@ def test_graph_paged_index_build_and_attention():
     indptr = [torch.empty(B + 1, dtype=torch.int32, device=dev) for _ in range(2)]
     idx = [torch.empty(B * C, dtype=torch.int32, device=dev) for _ in range(2)]
     outs = [torch.empty_like(q) for _ in range(2)]
-    ws = torch.empty(W.workspace_bytes(W.VARIANT_PAGED_FULL, B, Hq, Hkv, d, C), dtype=torch.uint8, device=dev)
-    ws_w = torch.empty(W.workspace_bytes(W.VARIANT_PAGED_WINDOWED, B, Hq, Hkv, d, C, Wn, sink),
+    ws = torch.zeros(W.workspace_bytes(B, Hq, Hkv, d, C, variant=W.VARIANT_PAGED_FULL), dtype=torch.uint8, device=dev)
+    ws_w = torch.zeros(W.workspace_bytes(B, Hq, Hkv, d, C, Wn, sink, variant=W.VARIANT_PAGED_WINDOWED),
                        dtype=torch.uint8, device=dev)
 
     def body():
@@ -196,8 +196,8 @@ def test_graph_fp8_append_and_attention():
     ones = G.lens_tensor([1, 1], dev)
     lens, lens_r = G.lens_tensor(S0, dev), G.lens_tensor(S0, dev)
     outs = [torch.empty_like(q) for _ in range(3)]
-    ws = torch.empty(W.workspace_bytes(W.VARIANT_FULL, B, Hq, Hkv, d, S_max), dtype=torch.uint8, device=dev)
-    ws_w = torch.empty(W.workspace_bytes(W.VARIANT_WINDOWED, B, Hq, Hkv, d, S_max, Wn, sink),
+    ws = torch.zeros(W.workspace_bytes(B, Hq, Hkv, d, S_max, variant=W.VARIANT_FULL), dtype=torch.uint8, device=dev)
+    ws_w = torch.zeros(W.workspace_bytes(B, Hq, Hkv, d, S_max, Wn, sink, variant=W.VARIANT_WINDOWED),
                        dtype=torch.uint8, device=dev)
 
     def reset():
@@ -235,7 +235,7 @@ def test_graph_tree_speculation_round():
     depth = G.lens_tensor([0, 0], dev)
     drop = G.lens_tensor([2, 0], dev)
     outs = torch.empty_like(q)
-    ws = torch.empty(W.workspace_bytes(W.VARIANT_TREE, B * width, Hq, Hkv, d, 0, Wn, sink), dtype=torch.uint8,
+    ws = torch.zeros(W.workspace_bytes(B * width, Hq, Hkv, d, 0, Wn, sink, variant=W.VARIANT_TREE), dtype=torch.uint8,
                      device=dev)
     depth_seen = torch.empty((dd, B), dtype=torch.int32, device=dev)
 

@@ -274,18 +274,13 @@ def test_empty_sequence():
         assert np.all(o == 0) and np.all(np.isneginf(lse))
 
 
-def test_batch_wrapper_and_sink_bias_case():
+def test_sink_bias_case():
     wl = I.WORKLOADS["draft_loop_s1m"]
     case = I.decode_case(wl, "cpu", S=600, steps=1)
     kb = I.bf16_bits(case["k"])
     # The x4 bias rows are exact in bf16.
     raw = I.normal_bf16((600, 2, 256), I.stream_seed(wl.seed, I.STREAM_K, 0))
     assert np.array_equal(A.bf16_to_f64(kb[0, :4]), 4.0 * raw[:4].to(torch.float64).numpy())
-    q = I.bf16_bits(case["q"][0])
-    vb = I.bf16_bits(case["v"])
-    o, lse = A.attend_batch(q, kb, vb, case["lens"], wl.scale, "windowed", W=wl.W, sink=wl.sink)
-    o1, _ = A.attend_sequence(q[0], kb[0], vb[0], 600, wl.scale, None)
-    assert np.array_equal(o[0], o1)  # S = 600 <= W + sink: degenerate
 
 
 # ---------------------------------------------------------------- extend
@@ -337,3 +332,69 @@ def test_extend_rows_are_decode_steps():
         assert np.array_equal(o[t], od) and np.array_equal(lse[t], ld)
     assert A.extend_lengths(S, 1, 1) == [S]
     assert A.extend_lengths(10, 3, 5) == [8, 9, 10, 0, 0]
+
+
+# ---------------------------------------------------------- value spread
+# value_spread sizes the effect of perturbed weights in the GPU tolerances;
+# it is pinned by closed forms that do not restate its definition.
+def test_spread_of_binary_values_is_bernoulli():
+    # values in {0, 1}: for any weights, o = P(v = 1) and the mean absolute
+    # deviation of a Bernoulli variable about its mean is 2 o (1 - o)
+    rng = np.random.default_rng(5)
+    Hq, Hkv, d, S = 6, 2, 16, 90
+    q = rng.standard_normal((Hq, d))
+    K = rng.standard_normal((S, Hkv, d))
+    V = (rng.random((S, Hkv, d)) < np.linspace(0.05, 0.95, d)).astype(np.float64)
+    for mask in (None, A.window_mask(S, 20, 3)):
+        o, _ = A.attend_sequence(q, K, V, S, 0.4, mask)
+        s = A.value_spread(q, K, V, S, 0.4, mask)
+        np.testing.assert_allclose(s, 2 * o * (1 - o), atol=1e-13)
+
+
+def test_spread_of_two_keys_closed_form():
+    # two keys with logits z1, z2: w1 = 1 / (1 + e^(z2 - z1)), w2 = 1 - w1 and
+    # |v1 - o| = w2 |v1 - v2|, |v2 - o| = w1 |v1 - v2|, so spread = 2 w1 w2 |v1 - v2|
+    rng = np.random.default_rng(6)
+    Hq, Hkv, d = 4, 2, 8
+    q = rng.standard_normal((Hq, d))
+    K = rng.standard_normal((2, Hkv, d))
+    V = rng.standard_normal((2, Hkv, d)) * 3
+    s = A.value_spread(q, K, V, 2, 0.9)
+    for h in range(Hq):
+        g = h // (Hq // Hkv)
+        z1, z2 = 0.9 * float(q[h] @ K[0, g]), 0.9 * float(q[h] @ K[1, g])
+        w1 = 1.0 / (1.0 + np.exp(z2 - z1))
+        np.testing.assert_allclose(s[h], 2 * w1 * (1 - w1) * np.abs(V[0, g] - V[1, g]), rtol=1e-12, atol=1e-15)
+
+
+def test_spread_shift_scale_and_degenerate_cases():
+    rng = np.random.default_rng(7)
+    Hq, Hkv, d, S = 4, 1, 8, 40
+    q = rng.standard_normal((Hq, d))
+    K = rng.standard_normal((S, Hkv, d))
+    V = rng.standard_normal((S, Hkv, d))
+    s = A.value_spread(q, K, V, S, 0.5)
+    np.testing.assert_allclose(A.value_spread(q, K, V + 7.5, S, 0.5), s, atol=1e-12)   # deviation about o
+    np.testing.assert_allclose(A.value_spread(q, K, -3.0 * V, S, 0.5), 3.0 * s, rtol=1e-12)
+    const = np.broadcast_to(rng.standard_normal((1, Hkv, d)), (S, Hkv, d))
+    assert np.abs(A.value_spread(q, K, const, S, 0.5)).max() < 1e-13                  # no deviation
+    assert np.all(A.value_spread(q, K, V, 1, 0.5) == 0)                               # one key
+    assert np.all(A.value_spread(q, K, V, 0, 0.5) == 0)                               # no key
+    # a dominant key (logit +40 above every other) leaves almost no spread
+    Kd = np.zeros((S, Hkv, d))
+    Kd[11, 0, :] = 40.0 / 0.5 / np.abs(q[0]).sum() * np.sign(q[0])   # q[0] . k = 80: logit 40
+    qd = np.tile(q[:1], (Hq, 1))
+    assert np.abs(A.value_spread(qd, Kd, V, S, 0.5)).max() < 1e-12
+    # chunking does not change it
+    np.testing.assert_allclose(A.value_spread(q, K, V, S, 0.5, chunk=7), s, atol=1e-14)
+
+
+def test_extend_spread_rows_are_decode_steps():
+    S, n = 300, 5
+    q, K, V = _rand_case(1, S, Hq=4, Hkv=2, d=8)
+    qr = np.stack([I.bf16_bits(torch.randn(4, 8).to(torch.bfloat16)) for _ in range(n + 2)])
+    sp = A.extend_spread(qr, K, V, S, n, 0.3, "windowed", 32, 3)
+    for t in range(n):
+        L = S - n + t + 1
+        assert np.array_equal(sp[t], A.value_spread(qr[t], K, V, L, 0.3, A.window_mask(L, 32, 3)))
+    assert np.all(sp[n:] == 0)

@@ -260,3 +260,24 @@ def test_mutant_v_scale_on_keys(monkeypatch):
 
     monkeypatch.setattr(F, "attend_sequence_fp8", swapped)
     assert _some_pin_fails()
+
+
+def test_spread_option_over_binary_codes():
+    # codes of 0.0 and 1.0 (0x38) with v_scale 1: Bernoulli values, spread 2 o (1 - o)
+    rng = np.random.default_rng(9)
+    S, Hkv, d = 60, 2, 16
+    q = rng.standard_normal((4, d))
+    kc = F.encode(rng.standard_normal((S, Hkv, d)).astype(np.float32))
+    vc = np.where(rng.random((S, Hkv, d)) < 0.3, 0x38, 0x00).astype(np.uint8)
+    for variant in ("full", "windowed"):
+        o, lse, s = F.attend_sequence_fp8(q, kc, vc, S, 0.3, 0.5, 1.0, variant, 20, 2, spread=True)
+        o2, lse2 = F.attend_sequence_fp8(q, kc, vc, S, 0.3, 0.5, 1.0, variant, 20, 2)
+        assert np.array_equal(o, o2) and np.array_equal(lse, lse2)
+        np.testing.assert_allclose(s, 2 * o * (1 - o), atol=1e-13)
+    R_w = 24
+    slots = R.ring_slots(A.selected_positions(S, 20, 2), 2, R_w)
+    rk = np.zeros((2 + R_w, Hkv, d), np.uint8)
+    rv = np.zeros_like(rk)
+    rk[slots], rv[slots] = kc[A.selected_positions(S, 20, 2)], vc[A.selected_positions(S, 20, 2)]
+    o, _, s = F.attend_ring_fp8(q, rk, rv, S, 0.3, 0.5, 1.0, 20, 2, R_w, spread=True)
+    np.testing.assert_allclose(s, 2 * o * (1 - o), atol=1e-13)

@@ -3,7 +3,8 @@
 Each mutant below plants one mistake in the oracle (on the CPU, through
 monkeypatching) -- an off-by-one window start, a non-strict threshold, a
 dropped sink, a transposed GQA grouping, a missing scale, a dropped key, a
-naive ring modulus -- and the test asserts that at least one of the pin
+naive ring modulus, a value spread taken about zero, with unnormalised
+weights or over the wrong KV group -- and the test asserts that at least one of the pin
 checks (golden fixtures, the printed rule, torch SDPA, closed forms, the
 operational ring) then fails.
 """
@@ -20,6 +21,7 @@ from .conftest import read_golden
 _orig_mask = A.window_mask
 _orig_attend = A.attend_sequence
 _orig_slot = R.ring_slot
+_orig_spread = A.value_spread
 
 
 # ---------------------------------------------------------------- pin checks
@@ -81,7 +83,36 @@ def _pin_ring():
     return True
 
 
-PINS = [_pin_golden_selection, _pin_count_closed_form, _pin_sdpa, _pin_zero_keys, _pin_ring]
+def _pin_spread_bernoulli():
+    # binary values: the weighted mean absolute deviation is 2 o (1 - o)
+    rng = np.random.default_rng(3)
+    Hq, Hkv, d, S = 6, 2, 8, 50
+    q = rng.standard_normal((Hq, d))
+    K = rng.standard_normal((S, Hkv, d))
+    V = (rng.random((S, Hkv, d)) < 0.4).astype(np.float64)
+    V[:, 1] = 1.0 - V[:, 1]  # the two KV groups differ
+    for mask in (None, A.window_mask(S, 9, 2)):
+        o, _ = _orig_attend(q, K, V, S, 0.5, mask)
+        if not np.allclose(A.value_spread(q, K, V, S, 0.5, mask), 2 * o * (1 - o), rtol=0, atol=1e-12):
+            return False
+    return True
+
+
+def _pin_spread_two_keys():
+    rng = np.random.default_rng(4)
+    q = rng.standard_normal((2, 4))
+    K = rng.standard_normal((2, 1, 4))
+    V = rng.standard_normal((2, 1, 4))
+    s = A.value_spread(q, K, V, 2, 0.7)
+    for h in range(2):
+        w1 = 1.0 / (1.0 + np.exp(0.7 * float(q[h] @ (K[1, 0] - K[0, 0]))))
+        if not np.allclose(s[h], 2 * w1 * (1 - w1) * np.abs(V[0, 0] - V[1, 0]), rtol=1e-12, atol=1e-15):
+            return False
+    return True
+
+
+PINS = [_pin_golden_selection, _pin_count_closed_form, _pin_sdpa, _pin_zero_keys, _pin_ring,
+        _pin_spread_bernoulli, _pin_spread_two_keys]
 
 
 # ------------------------------------------------------------------- mutants
@@ -136,6 +167,39 @@ def _attend_drop_last_key(q, K, V, S, scale, mask=None, chunk=65536):
     return _orig_attend(q, K, V, S, scale, m, chunk)
 
 
+def _spread_with(q, K, V, S, scale, mask, weight, about_output=True, group=None):
+    """value_spread with one planted change: the weights (normalised or not),
+    the deviation about the output or the raw magnitude, the KV group."""
+    qf = np.asarray(q, dtype=np.float64)
+    Hq, d = qf.shape
+    Hkv = K.shape[1]
+    G = Hq // Hkv
+    keep = np.arange(S) if mask is None else np.flatnonzero(np.asarray(mask)[:S])
+    out = np.zeros((Hq, d))
+    if keep.size == 0:
+        return out
+    o, lse = _orig_attend(q, K, V, S, scale, mask)
+    for h in range(Hq):
+        g = h // G if group is None else group(h, Hkv)
+        z = scale * (np.asarray(K[keep], dtype=np.float64)[:, g, :] @ qf[h])
+        w = weight(z, lse[h])
+        Vk = np.asarray(V[keep], dtype=np.float64)[:, g, :]
+        out[h] = w @ (np.abs(Vk - o[h]) if about_output else np.abs(Vk))
+    return out
+
+
+def _spread_magnitude(q, K, V, S, scale, mask=None, chunk=4096):
+    return _spread_with(q, K, V, S, scale, mask, lambda z, lse: np.exp(z - lse), about_output=False)
+
+
+def _spread_unnormalised(q, K, V, S, scale, mask=None, chunk=4096):
+    return _spread_with(q, K, V, S, scale, mask, lambda z, lse: np.exp(z - z.max()))
+
+
+def _spread_grouping_mod(q, K, V, S, scale, mask=None, chunk=4096):
+    return _spread_with(q, K, V, S, scale, mask, lambda z, lse: np.exp(z - lse), group=lambda h, Hkv: h % Hkv)
+
+
 def _slot_naive_modulus(p, sink, R_w):
     return int(p) % (sink + R_w)
 
@@ -153,6 +217,9 @@ MUTANTS = [
     ("attend_sequence", _attend_grouping_mod),
     ("attend_sequence", _attend_no_scale),
     ("attend_sequence", _attend_drop_last_key),
+    ("value_spread", _spread_magnitude),
+    ("value_spread", _spread_unnormalised),
+    ("value_spread", _spread_grouping_mod),
     ("ring_slot", _slot_naive_modulus),
     ("ring_slot", _slot_absolute),
 ]

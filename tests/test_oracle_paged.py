@@ -62,3 +62,17 @@ def test_relabelling_the_pool_changes_nothing(variant):
     np.testing.assert_allclose(o1, o2, atol=1e-14)
     o3, _ = Pg.attend_paged(q, Kq, Vq, table, S, 0.3, variant, 16, 2)
     assert np.abs(o3 - o1).max() > 1e-3
+
+
+@pytest.mark.parametrize("variant", ["full", "windowed"])
+def test_spread_option_over_binary_pool(variant):
+    rng = np.random.default_rng(4)
+    P, S, Hkv, d = 200, 90, 2, 8
+    q = rng.standard_normal((4, d))
+    Kp = rng.standard_normal((P, Hkv, d))
+    Vp = (rng.random((P, Hkv, d)) < 0.6).astype(np.float64)
+    table = rng.permutation(P)[:S]
+    o, lse, s = Pg.attend_paged(q, Kp, Vp, table, S, 0.3, variant, 16, 2, spread=True)
+    o2, lse2 = Pg.attend_paged(q, Kp, Vp, table, S, 0.3, variant, 16, 2)
+    assert np.array_equal(o, o2) and np.array_equal(lse, lse2)
+    np.testing.assert_allclose(s, 2 * o * (1 - o), atol=1e-13)

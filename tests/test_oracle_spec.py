@@ -210,3 +210,21 @@ def test_mutant_private_run_indexed_from_zero_length(monkeypatch):
             return orig(p, S, b, sink, W, d, R_w)
         return sink + W + d + (b - 1) * d + (p % d)
     assert _pins_fail(monkeypatch, bad)
+
+
+def test_spread_option_over_binary_rows():
+    rng = np.random.default_rng(8)
+    Hkv, d = 2, 8
+    seqs = P.SpecSequences(3)
+    row = lambda: (rng.standard_normal((Hkv, d)), (rng.random((Hkv, d)) < 0.5).astype(np.float64))
+    seqs.verify([row() for _ in range(40)])
+    seqs.speculate([row() for _ in range(3)])
+    q = rng.standard_normal((4, d))
+    for b in range(3):
+        o, lse, s = seqs.attend(q, b, 0.3, 16, 2, spread=True)
+        o2, lse2 = seqs.attend(q, b, 0.3, 16, 2)
+        assert np.array_equal(o, o2) and np.array_equal(lse, lse2)
+        np.testing.assert_allclose(s, 2 * o * (1 - o), atol=1e-13)
+    empty = P.SpecSequences(1)
+    o, lse, s = empty.attend(q, 0, 0.3, 16, 2, spread=True)
+    assert np.all(s == 0) and np.all(np.isneginf(lse))

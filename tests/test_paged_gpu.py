@@ -97,9 +97,9 @@ def test_paged_attention_equals_dense(dev, d, Hq, Hkv):
         assert torch.equal(lse_p, lse_d), variant
         qb = I.bf16_bits(q)
         refs = [Pg.attend_paged(qb[b], G.HostRows(kp), G.HostRows(vp), table[b].cpu().numpy(), S,
-                                1.0 / np.sqrt(d), variant, Wn, sink) for b, S in enumerate(lens)]
+                                1.0 / np.sqrt(d), variant, Wn, sink, spread=True) for b, S in enumerate(lens)]
         G.assert_attn_close(op, np.stack([r[0] for r in refs]), lse_p, np.stack([r[1] for r in refs]),
-                            what=f"paged {variant}", strict=False)
+                            what=f"paged {variant}", spread=np.stack([r[2] for r in refs]))
     assert err.item() == 0
 
 
@@ -187,10 +187,10 @@ def test_paged_fp8_equals_dense_fp8(dev, d, Hq, Hkv):
         assert torch.equal(op, od), variant
         assert torch.equal(lse_p, lse_d), variant
         kv = F.DequantizedRows(_HostCodes(kp), ks), F.DequantizedRows(_HostCodes(vp), vs)
-        refs = [Pg.attend_paged(qb[b], kv[0], kv[1], table[b].cpu().numpy(), S, scale, variant, Wn, sink)
-                for b, S in enumerate(lens)]
+        refs = [Pg.attend_paged(qb[b], kv[0], kv[1], table[b].cpu().numpy(), S, scale, variant, Wn, sink,
+                                spread=True) for b, S in enumerate(lens)]
         G.assert_attn_close(op, np.stack([r[0] for r in refs]), lse_p, np.stack([r[1] for r in refs]),
-                            what=f"paged fp8 {variant}", strict=False)
+                            what=f"paged fp8 {variant}", spread=np.stack([r[2] for r in refs]))
         assert torch.count_nonzero(op[0]) == 0
     assert err.item() == 0
     # a table entry outside the pool is flagged

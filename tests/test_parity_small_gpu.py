@@ -67,10 +67,12 @@ def test_full_and_windowed_vs_oracle(dev, d, Hq, Hkv):
             else:
                 out = W.draft_attn_windowed(q, k, v, lt, W_, sink, lse=lse)
             torch.cuda.synchronize()
-            refs = [G.oracle_seq(qb[b], k[b], v[b], lens[b], scale, variant, W_, sink) for b in range(B)]
+            refs = [G.oracle_seq(qb[b], k[b], v[b], lens[b], scale, variant, W_, sink, spread=True)
+                    for b in range(B)]
             o_ref = np.stack([r[0] for r in refs])
             l_ref = np.stack([r[1] for r in refs])
-            G.assert_attn_close(out, o_ref, lse, l_ref, what=f"{variant} d={d} G={Hq // Hkv} W={W_}", strict=False)
+            G.assert_attn_close(out, o_ref, lse, l_ref, what=f"{variant} d={d} G={Hq // Hkv} W={W_}",
+                                spread=np.stack([r[2] for r in refs]))
             # empty sequence: exact zeros
             assert torch.count_nonzero(out[0]) == 0
         if W_ == 64:  # the window really drops keys past the threshold
@@ -116,9 +118,10 @@ def test_ring_equals_windowed_bitwise(dev, d, Hq, Hkv, W_, sink, slack):
     assert torch.equal(lse_r, lse_w)
     qb = I.bf16_bits(q)
     scale = 1.0 / np.sqrt(d)
-    refs = [G.oracle_seq(qb[b], k[b], v[b], lens[b], scale, "windowed", W_, sink) for b in range(B)]
+    refs = [G.oracle_seq(qb[b], k[b], v[b], lens[b], scale, "windowed", W_, sink, spread=True)
+            for b in range(B)]
     G.assert_attn_close(orr, np.stack([r[0] for r in refs]), lse_r, np.stack([r[1] for r in refs]),
-                        what="ring", strict=False)
+                        what="ring", spread=np.stack([r[2] for r in refs]))
 
 
 def test_select_indices_export_exact(dev):
@@ -231,9 +234,10 @@ def _vs_oracle(dev, d, Hq, Hkv, lens, variant, W_=None, sink=None, seed=7):
         out = W.draft_attn_windowed(q, k, v, lt, W_, sink, lse=lse)
     torch.cuda.synchronize()
     qb = I.bf16_bits(q)
-    refs = [G.oracle_seq(qb[b], k[b], v[b], lens[b], scale, variant, W_, sink) for b in range(B)]
+    refs = [G.oracle_seq(qb[b], k[b], v[b], lens[b], scale, variant, W_, sink, spread=True)
+            for b in range(B)]
     G.assert_attn_close(out, np.stack([r[0] for r in refs]), lse, np.stack([r[1] for r in refs]),
-                        what=f"{variant} d={d} lens={lens[:6]}", strict=False)
+                        what=f"{variant} d={d} lens={lens[:6]}", spread=np.stack([r[2] for r in refs]))
 
 
 @pytest.mark.parametrize("n_sel", [63 * 64, 64 * 64, 64 * 64 + 1, 65 * 64 + 17])

@@ -50,9 +50,9 @@ def test_ring_b8_1000_iterations(dev):
     out_d = torch.empty_like(out_r)
     lse_r = torch.empty((B, Hq), dtype=torch.float32, device=dev)
     lse_d = torch.empty_like(lse_r)
-    ws_r = torch.empty(W.workspace_bytes(W.VARIANT_RING, B, Hq, Hkv, d, sink + R_w, Wn, sink),
+    ws_r = torch.zeros(W.workspace_bytes(B, Hq, Hkv, d, sink + R_w, Wn, sink, variant=W.VARIANT_RING),
                        dtype=torch.uint8, device=dev)
-    ws_d = torch.empty(W.workspace_bytes(W.VARIANT_WINDOWED, B, Hq, Hkv, d, S_cap, Wn, sink),
+    ws_d = torch.zeros(W.workspace_bytes(B, Hq, Hkv, d, S_cap, Wn, sink, variant=W.VARIANT_WINDOWED),
                        dtype=torch.uint8, device=dev)
     replay = [R.ReplayCache(Hkv, d) for _ in range(B)]
     host_len = np.zeros(B, dtype=np.int64)

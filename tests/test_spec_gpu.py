@@ -48,7 +48,7 @@ class Rows:
 def _check(out, lse, refs, what):
     o_ref = np.stack([r[0] for r in refs])
     l_ref = np.stack([r[1] for r in refs])
-    G.assert_attn_close(out, o_ref, lse, l_ref, what=what, strict=False)
+    G.assert_attn_close(out, o_ref, lse, l_ref, what=what, spread=np.stack([r[2] for r in refs]))
 
 
 def _prefill(dev, rows, kr, vr, lens, seqs, S0, sink, R_w):
@@ -88,7 +88,7 @@ def test_chain_speculate_rollback(dev, d, Hq, Hkv):
             refs = []
             for b in range(B):
                 seqs[b].speculate([(kb[b, 0], vb[b, 0])])
-                refs.append(seqs[b].attend(qb[b], 0, scale, Wn, sink))
+                refs.append(seqs[b].attend(qb[b], 0, scale, Wn, sink, spread=True))
             _check(out, lse, refs, f"chain round {rnd} step {j}")
         acc = rng.integers(0, gamma + 1, size=B)
         W.ring_rollback(lens, G.lens_tensor(gamma - acc, dev), err=err)
@@ -102,7 +102,7 @@ def test_chain_speculate_rollback(dev, d, Hq, Hkv):
         for b in range(B):
             kept = seqs[b].spec[0][: acc[b]] + [(kb[b, 0], vb[b, 0])]
             seqs[b].verify(kept)
-            refs.append(seqs[b].attend(qb[b], 0, scale, Wn, sink))
+            refs.append(seqs[b].attend(qb[b], 0, scale, Wn, sink, spread=True))
         _check(out, lse, refs, f"chain round {rnd} after rollback")
         assert lens.cpu().numpy().tolist() == [s.S for s in seqs]
     assert err.item() == 0
@@ -143,10 +143,11 @@ def test_tree_candidates_and_verify(dev, d, Hq, Hkv, width, dd):
             refs = []
             for b in range(B):
                 seqs[b].speculate([(kb[b, c], vb[b, c]) for c in range(width)])
-                refs.append([seqs[b].attend(qb[b, c], c, scale, Wn, sink) for c in range(width)])
+                refs.append([seqs[b].attend(qb[b, c], c, scale, Wn, sink, spread=True) for c in range(width)])
             o_ref = np.stack([[r[0] for r in rr] for rr in refs])
             l_ref = np.stack([[r[1] for r in rr] for rr in refs])
-            G.assert_attn_close(out, o_ref, lse, l_ref, what=f"tree round {rnd} step {i}", strict=False)
+            spread = np.stack([[r[2] for r in rr] for rr in refs])
+            G.assert_attn_close(out, o_ref, lse, l_ref, what=f"tree round {rnd} step {i}", spread=spread)
         assert depth.cpu().numpy().tolist() == [n_steps] * B
         # verify: candidate cb[b] wins with acc[b] accepted rows, plus a bonus row
         cb = rng.integers(0, width, size=B)
@@ -173,13 +174,15 @@ def test_tree_candidates_and_verify(dev, d, Hq, Hkv, width, dd):
         qxb = I.bf16_bits(qx)
         o_ref = np.zeros((B, n_max, Hq, d))
         l_ref = np.full((B, n_max, Hq), -np.inf)
+        spread = np.zeros((B, n_max, Hq, d))
         for b in range(B):
             seqs[b].verify(accepted[b])
             K = np.stack([r[0] for r in seqs[b].committed])
             V = np.stack([r[1] for r in seqs[b].committed])
             o_ref[b], l_ref[b] = A.attend_extend(qxb[b], K, V, seqs[b].S, int(n_new[b]), scale, "windowed",
                                                  Wn, sink)
-        G.assert_attn_close(ox, o_ref, lse_x, l_ref, what=f"tree round {rnd} extend", strict=False)
+            spread[b] = A.extend_spread(qxb[b], K, V, seqs[b].S, int(n_new[b]), scale, "windowed", Wn, sink)
+        G.assert_attn_close(ox, o_ref, lse_x, l_ref, what=f"tree round {rnd} extend", spread=spread)
         assert lens.cpu().numpy().tolist() == [s.S for s in seqs]
     assert err.item() == 0
 

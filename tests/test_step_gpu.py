@@ -2,8 +2,9 @@
 
 * bit for bit against the unfused path (wmtp_cache_append / wmtp_ring_append
   followed by the attention call): outputs, lse, cache contents and lengths,
-  over several steps with ragged append counts (0, 1, 2 rows), lengths 0,
-  short, past the window, and a ring append longer than the ring;
+  over several steps with ragged append counts (0 to 6 rows), lengths 0,
+  short and past the window; and ring steps whose append is longer than the
+  ring (the fused kernel writes only the rows that stay resident);
 * the million-token windowed and full draft loop through the fused step
   against the oracle;
 * a dense cache that would grow past its capacity keeps the rows that fit and
@@ -85,6 +86,44 @@ def test_step_equals_append_then_attention(dev, variant, d, Hq, Hkv):
             of = W.ring_step(q, k_f, v_f, kn, vn, n_new, lin, lout, Wn, sink, R_w, lse=lse_f, err=err_f)
             W.ring_append(k_u, v_u, kn, vn, n_new, lens_u, sink, R_w, err=err_u)
             ou = W.ring_attn(q, k_u, v_u, lens_u, Wn, sink, R_w, lse=lse_u, err=err_u)
+        torch.cuda.synchronize()
+        assert torch.equal(lout, lens_u), step
+        assert torch.equal(of, ou), step
+        assert torch.equal(lse_f, lse_u), step
+        assert torch.equal(k_f, k_u) and torch.equal(v_f, v_u), step
+    assert err_f.item() == 0 and err_u.item() == 0
+
+
+@pytest.mark.parametrize("d,Hq,Hkv", [(128, 16, 2), (256, 32, 2)])
+def test_ring_step_append_longer_than_ring(dev, d, Hq, Hkv):
+    """n_new up to R_w + sink + 3 rows in one fused ring step, from lengths
+    0, below the sink, past the window and far past it: positions that a
+    later row of the same append overwrites must not be written."""
+    Wn, sink = 16, 4
+    R_w = Wn
+    lens0 = [0, 2, 30, 200]
+    B, n_max = len(lens0), R_w + sink + 3
+    k0 = I.normal_bf16((B, sink + R_w, Hkv, d), 11 * d, dev)
+    v0 = I.normal_bf16((B, sink + R_w, Hkv, d), 11 * d + 1, dev)
+    k_f, v_f = k0.clone(), v0.clone()
+    k_u, v_u = k0.clone(), v0.clone()
+    lens_a = G.lens_tensor(lens0, dev)
+    lens_b = torch.empty_like(lens_a)
+    lens_u = G.lens_tensor(lens0, dev)
+    err_f, err_u = G.err_word(dev), G.err_word(dev)
+    counts = [[n_max, R_w + 1, n_max, R_w], [1, n_max, 0, n_max], [R_w + 2, 3, n_max - 1, 5]]
+    for step, nn in enumerate(counts):
+        G.say(f"ring step longer than the ring d={d} step {step} n_new={nn}")
+        kn = I.normal_bf16((B, n_max, Hkv, d), 300 + 10 * step, dev)
+        vn = I.normal_bf16((B, n_max, Hkv, d), 301 + 10 * step, dev)
+        q = I.normal_bf16((B, Hq, d), 302 + 10 * step, dev)
+        n_new = G.lens_tensor(nn, dev)
+        lse_f = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        lse_u = torch.empty_like(lse_f)
+        lin, lout = (lens_a, lens_b) if step % 2 == 0 else (lens_b, lens_a)
+        of = W.ring_step(q, k_f, v_f, kn, vn, n_new, lin, lout, Wn, sink, R_w, lse=lse_f, err=err_f)
+        W.ring_append(k_u, v_u, kn, vn, n_new, lens_u, sink, R_w, err=err_u)
+        ou = W.ring_attn(q, k_u, v_u, lens_u, Wn, sink, R_w, lse=lse_u, err=err_u)
         torch.cuda.synchronize()
         assert torch.equal(lout, lens_u), step
         assert torch.equal(of, ou), step
