@@ -61,7 +61,8 @@ typedef enum {
   WMTP_EINVAL = 1,        /* bad argument (null pointer, misalignment, bad size) */
   WMTP_EUNSUPPORTED = 2,  /* head size or GQA group outside the built kernels */
   WMTP_EWORKSPACE = 3,    /* ws_bytes smaller than wmtp_workspace_bytes() */
-  WMTP_ELAUNCH = 4        /* the HIP runtime rejected a kernel launch */
+  WMTP_ELAUNCH = 4,       /* the HIP runtime rejected a kernel launch */
+  WMTP_ESCRATCH = 5       /* the allocation-free call needs more than its static scratch */
 } wmtp_status;
 
 /* Device error bits, OR-ed into *err by the kernels. */
@@ -130,6 +131,32 @@ int wmtp_draft_attn_windowed(const void* q, const void* k, const void* v, const 
                              void* out, float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
                              int W, int sink, float scale, void* ws, size_t ws_bytes,
                              int32_t* err, hipStream_t stream);
+
+/*
+ * Allocation-free windowed draft decode attention, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Computes exactly what
+ * wmtp_draft_attn_windowed computes, with the same kernels, bit for bit, but
+ * keeps the split partials in a static device array of
+ * WMTP_NOALLOC_SCRATCH_BYTES inside the library (one per GPU, part of the
+ * library's code object, held until the process ends) instead of a caller
+ * workspace; the caller still passes inputs and outputs.  The call allocates
+ * nothing and calls no allocating routine; its first call on a device
+ * resolves the array's device address once.
+ *   Returns WMTP_ESCRATCH (nothing enqueued) when the shape needs more
+ *   partials than the array holds (wmtp_workspace_bytes of the windowed
+ *   variant > WMTP_NOALLOC_SCRATCH_BYTES); other arguments and errors as for
+ *   wmtp_draft_attn_windowed.
+ *   Every call on one GPU uses that GPU's single array: calls that may
+ *   overlap in time on one GPU (different streams, concurrent host threads)
+ *   race on it and must be serialised by the caller.  Calls enqueued on one
+ *   stream are ordered and safe.
+ */
+#define WMTP_NOALLOC_SCRATCH_BYTES (16u << 20)
+int wmtp_draft_attn_windowed_noalloc(const void* q, const void* k, const void* v,
+                                     const int32_t* lens, void* out, float* lse, int B, int Hq,
+                                     int Hkv, int d, int64_t S_max, int W, int sink, float scale,
+                                     int32_t* err, hipStream_t stream);
 
 /*
  * Windowed draft decode attention over the compact ring store (Section 4 and
@@ -467,7 +494,7 @@ const char* wmtp_status_string(int status);
 /* ABI version of this header, (major << 16) | minor. */
 int wmtp_abi_version(void);
 
-#define WMTP_ABI_VERSION ((2 << 16) | 0)
+#define WMTP_ABI_VERSION ((2 << 16) | 1)
 
 #ifdef __cplusplus
 }

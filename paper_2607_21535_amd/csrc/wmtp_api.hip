@@ -6,9 +6,11 @@
 #include "launch.h"
 
 #include <algorithm>
+#include <atomic>
 #include <climits>
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #define WMTP_EXPORT extern "C" __attribute__((visibility("default")))
 
@@ -71,7 +73,7 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
                      const int32_t* table = nullptr, int64_t pool_rows = 0, bool fp8 = false,
                      float k_scale = 1.0f, float v_scale = 1.0f, const void* k2 = nullptr,
                      const void* v2 = nullptr, int dd = 0, bool step = false,
-                     int32_t* lens_out = nullptr, bool dry_run = false) {
+                     int32_t* lens_out = nullptr, bool dry_run = false, bool check_ws = true) {
   int st = check_heads(B, Hq, Hkv, d);
   if (st != WMTP_OK) return st;
   const bool tree = variant == WMTP_VARIANT_TREE;
@@ -120,8 +122,10 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   const SplitPlan plan =
       wmtp::plan_split(variant, rows_q, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
   if (!plan_fits(plan, Hkv)) return WMTP_EUNSUPPORTED;
-  if (ws_bytes < plan.bytes) return WMTP_EWORKSPACE;
-  if (plan.bytes > 0 && (ws == nullptr || !aligned(ws, 256))) return WMTP_EINVAL;
+  if (check_ws) {
+    if (ws_bytes < plan.bytes) return WMTP_EWORKSPACE;
+    if (plan.bytes > 0 && (ws == nullptr || !aligned(ws, 256))) return WMTP_EINVAL;
+  }
 
   AttnLaunch L{};
   L.variant = variant;
@@ -637,6 +641,71 @@ WMTP_EXPORT int wmtp_hbm_read_probe(const void* buf, int64_t bytes, uint32_t* si
   return WMTP_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Allocation-free windowed attention: the split partials live in a static
+// device array (one copy per GPU, loaded with the library's code object and
+// kept until the process ends) instead of a caller workspace.
+//
+// In host code `scratch` names a host-side stand-in, not device memory: its
+// device address is resolved once per device with hipGetSymbolAddress and
+// only that address is ever passed to a kernel.
+static __device__ __align__(256) unsigned char scratch[WMTP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kScratchDevices = 64;
+std::atomic<void*> g_scratch_ptr[kScratchDevices];
+std::mutex g_scratch_mu;
+
+// Device address of the current device's copy of `scratch`, resolved on the
+// first call on that device (no allocation: the array is part of the code
+// object).  Returns WMTP_ELAUNCH when the runtime cannot resolve it.
+int scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) {
+    (void)hipGetLastError();
+    return WMTP_ELAUNCH;
+  }
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (p == nullptr) {
+      void* addr = nullptr;
+      if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || addr == nullptr) {
+        (void)hipGetLastError();
+        return WMTP_ELAUNCH;
+      }
+      p = addr;
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return WMTP_OK;
+}
+
+}  // namespace
+
+WMTP_EXPORT int wmtp_draft_attn_windowed_noalloc(const void* q, const void* k, const void* v,
+                                                 const int32_t* lens, void* out, float* lse, int B,
+                                                 int Hq, int Hkv, int d, int64_t S_max, int W,
+                                                 int sink, float scale, int32_t* err,
+                                                 hipStream_t stream) {
+  // Every argument check of the workspace form first (nothing enqueued),
+  // then the partials of this shape against the static array.
+  int st = attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv,
+                            d, S_max, W, sink, W, scale, nullptr, 0, err, stream, nullptr, 0, false,
+                            1.0f, 1.0f, nullptr, nullptr, 0, false, nullptr, true, false);
+  if (st != WMTP_OK || B == 0) return st;
+  const size_t need = wmtp_workspace_bytes(B, Hq, Hkv, d, S_max, W, sink, WMTP_VARIANT_WINDOWED);
+  if (need > WMTP_NOALLOC_SCRATCH_BYTES) return WMTP_ESCRATCH;
+  void* ptr = nullptr;
+  st = scratch_address(&ptr);
+  if (st != WMTP_OK) return st;
+  return attention_common(WMTP_VARIANT_WINDOWED, q, k, v, lens, nullptr, 1, out, lse, B, Hq, Hkv,
+                          d, S_max, W, sink, W, scale, ptr, WMTP_NOALLOC_SCRATCH_BYTES, err, stream);
+}
+
 WMTP_EXPORT const char* wmtp_status_string(int status) {
   switch (status) {
     case WMTP_OK: return "WMTP_OK";
@@ -644,6 +713,9 @@ WMTP_EXPORT const char* wmtp_status_string(int status) {
     case WMTP_EUNSUPPORTED: return "WMTP_EUNSUPPORTED: shape without a built kernel";
     case WMTP_EWORKSPACE: return "WMTP_EWORKSPACE: workspace too small";
     case WMTP_ELAUNCH: return "WMTP_ELAUNCH: kernel launch failed";
+    case WMTP_ESCRATCH:
+      return "WMTP_ESCRATCH: the call needs more scratch than the static array holds "
+             "(WMTP_NOALLOC_SCRATCH_BYTES); use the workspace form of the call";
     default: return "unknown wmtp status";
   }
 }

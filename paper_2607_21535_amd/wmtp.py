@@ -33,6 +33,8 @@ __all__ = [
     "workspace_bytes",
     "draft_attn_full",
     "draft_attn_windowed",
+    "draft_attn_windowed_noalloc",
+    "NOALLOC_SCRATCH_BYTES",
     "ring_attn",
     "draft_extend_full",
     "draft_extend_windowed",
@@ -71,13 +73,15 @@ __all__ = [
 VARIANT_FULL, VARIANT_WINDOWED, VARIANT_RING = 0, 1, 2
 VARIANT_PAGED_FULL, VARIANT_PAGED_WINDOWED, VARIANT_TREE = 3, 4, 5
 DERR_LEN_RANGE, DERR_NNEW_RANGE, DERR_CAPACITY, DERR_SLOT_RANGE, DERR_DEPTH = 0x1, 0x2, 0x4, 0x8, 0x10
-OK, EINVAL, EUNSUPPORTED, EWORKSPACE, ELAUNCH = 0, 1, 2, 3, 4
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, ELAUNCH, ESCRATCH = 0, 1, 2, 3, 4, 5
+NOALLOC_SCRATCH_BYTES = 16 << 20  # WMTP_NOALLOC_SCRATCH_BYTES
 PROBE_BLOCKS = 512  # WMTP_PROBE_BLOCKS
 
 EXPORTED_SYMBOLS = (
     "wmtp_workspace_bytes",
     "wmtp_draft_attn_full",
     "wmtp_draft_attn_windowed",
+    "wmtp_draft_attn_windowed_noalloc",
     "wmtp_ring_attn",
     "wmtp_draft_extend_full",
     "wmtp_draft_extend_windowed",
@@ -126,6 +130,7 @@ _SIGNATURES = {
     "wmtp_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I64, _I, _I, _I]),
     "wmtp_draft_attn_full": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _F, _P, _SZ, _P, _P]),
     "wmtp_draft_attn_windowed": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _F, _P, _SZ, _P, _P]),
+    "wmtp_draft_attn_windowed_noalloc": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _F, _P, _P]),
     "wmtp_ring_attn": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P, _SZ, _P, _P]),
     "wmtp_draft_extend_full": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I64, _F, _P, _SZ, _P, _P]),
     "wmtp_draft_extend_windowed": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I64, _I, _I, _F, _P, _SZ, _P, _P]),
@@ -180,7 +185,7 @@ class WmtpError(RuntimeError):
 
 # The version of include/wmtp.h these signatures follow, (major << 16) | minor:
 # a library of another major version, or an older minor one, is refused.
-ABI_VERSION = (2 << 16) | 0
+ABI_VERSION = (2 << 16) | 1
 
 
 def lib_path() -> str:
@@ -317,6 +322,23 @@ def draft_attn_windowed(q, k, v, lens, W, sink, out=None, lse=None, scale=None, 
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, S_max, W, sink,
         scale, _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _ptr(err), _stream(dev))
     _check(st, "wmtp_draft_attn_windowed")
+    return out
+
+
+def draft_attn_windowed_noalloc(q, k, v, lens, W, sink, out, lse=None, scale=None, err=None):
+    """draft_attn_windowed with the library's static scratch instead of a
+    workspace (wmtp_draft_attn_windowed_noalloc): the call allocates nothing,
+    so `out` must be given.  Raises WmtpError (ESCRATCH) for shapes whose
+    partials exceed NOALLOC_SCRATCH_BYTES."""
+    if out is None:
+        raise ValueError("the allocation-free call needs a preallocated out")
+    dev, B, Hq, d, out = _attn_io(q, k, v, lens, out, lse)
+    S_max, Hkv = k.shape[1], k.shape[2]
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    st = load_library().wmtp_draft_attn_windowed_noalloc(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(out), _ptr(lse), B, Hq, Hkv, d, S_max, W, sink,
+        scale, _ptr(err), _stream(dev))
+    _check(st, "wmtp_draft_attn_windowed_noalloc")
     return out
 
 

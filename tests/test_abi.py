@@ -55,12 +55,12 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.wmtp_abi_version() == (2 << 16) | 0
+    assert lib.wmtp_abi_version() == (2 << 16) | 1
     # the header, the library and the binding's signatures agree
     with open(os.path.join(ROOT, "include", "wmtp.h")) as f:
         m = re.search(r"#define WMTP_ABI_VERSION \(\(2 << 16\) \| (\d+)\)", f.read())
     assert m is not None and W.ABI_VERSION == (2 << 16) | int(m.group(1)) == lib.wmtp_abi_version()
-    for code in range(5):
+    for code in range(6):
         assert W.status_string(code).startswith("WMTP_")
     assert "unknown" in W.status_string(99)
 
@@ -473,3 +473,36 @@ def test_read_probe_argument_checks(lib):
     assert probe(None, 32, P, None) == W.EINVAL
     assert probe(P, 32, None, None) == W.EINVAL
     assert probe(None, 0, None, None) == W.OK  # nothing to read: no launch
+
+
+# ----------------------------------------------------- allocation-free call
+def _noalloc(lib, B=1, Hq=32, Hkv=2, d=256, S_max=1 << 20, W_=2048, sink=4, q=P, out=P):
+    return lib.wmtp_draft_attn_windowed_noalloc(q, P, P, P, out, None, B, Hq, Hkv, d, S_max, W_, sink,
+                                                0.0625, None, None)
+
+
+@fake_pointers
+def test_noalloc_host_checks(lib):
+    # argument errors come first, as for the workspace form
+    assert _noalloc(lib, d=96) == W.EUNSUPPORTED
+    assert _noalloc(lib, Hkv=3) == W.EINVAL
+    assert _noalloc(lib, W_=0) == W.EINVAL
+    assert _noalloc(lib, q=None) == W.EINVAL
+    assert _noalloc(lib, out=P + 2) == W.EINVAL
+    assert _noalloc(lib, B=0) == W.OK
+    # a batch whose partials exceed the static array is rejected, nothing enqueued
+    for B in (4096, 1 << 16):
+        need = W.workspace_bytes(B, 32, 2, 256, 1 << 20, 2048, 4, variant=W.VARIANT_WINDOWED)
+        assert need > W.NOALLOC_SCRATCH_BYTES
+        assert _noalloc(lib, B=B) == W.ESCRATCH
+    assert "static" in W.status_string(W.ESCRATCH)
+
+
+def test_noalloc_limit_matches_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define WMTP_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    assert m is not None and int(m.group(1)) << int(m.group(2)) == W.NOALLOC_SCRATCH_BYTES
+    # the 1M workload's windowed call and a 32-sequence batch fit the array
+    for B in (1, 8, 32):
+        assert W.workspace_bytes(B, 32, 2, 256, 1 << 20, 2048, 4, variant=W.VARIANT_WINDOWED) <= \
+            W.NOALLOC_SCRATCH_BYTES
