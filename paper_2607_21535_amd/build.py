@@ -23,7 +23,7 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_NAME = "libwmtp.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
 
-SOURCES = ["wmtp_api.hip", "decode_attn.hip", "kv_append.hip", "kv_index.hip", "probe.hip"]
+SOURCES = ["wmtp_api.hip", "decode_attn.hip", "window_attn.hip", "kv_append.hip", "kv_index.hip", "probe.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [

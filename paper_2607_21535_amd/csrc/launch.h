@@ -38,22 +38,35 @@ struct AttnLaunch {
   // the cache and the merge writes lens_out = old length + rows appended.
   bool step;
   int32_t* lens_out;
-  // split plan (from plan_split)
+  // split plan (from plan_split; full-context variants)
   int target;     // work items per KV head to aim for
   int chunk_cap;  // largest work item, in keys
   int max_items;  // work items per KV head, upper bound over all lengths
+  // windowed plan (from plan_window; every windowed variant)
+  int win_keys;    // selected keys per work item
+  int win_items;   // work items per query row and KV head
+  int win_slices;  // value slices per work item (1, or d / kWinSlice)
+  int32_t* tickets;
   float* pm;
   float* pl;
   float* pz;
   float* po;
 };
 
+// Every workspace starts with the ticket counters of the one-launch kernels
+// (int32, zero between calls); the partial results of any call follow them,
+// so calls of different variants and shapes can share one workspace without
+// touching each other's counters.
+constexpr size_t kTicketBytes = size_t(1) << 20;
+constexpr int64_t kMaxTickets = static_cast<int64_t>(kTicketBytes / sizeof(int32_t));
+
 struct SplitPlan {
   int target;      // work items per KV head to aim for
   int chunk_cap;   // largest work item, in keys (multiple of kChunkQuantum)
   int max_items;   // most work items per KV head for any lengths
   size_t bytes;    // workspace bytes
-  size_t off_pl;   // byte offsets of the partial arrays inside the workspace
+  size_t off_pm;   // byte offsets of the partial arrays inside the workspace
+  size_t off_pl;
   size_t off_pz;
   size_t off_po;
 };
@@ -61,6 +74,33 @@ struct SplitPlan {
 // Split plan for a validated shape; B counts query rows (sequences x rows per
 // sequence); n_keys_max = most keys one query row attends.
 SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_max);
+
+// Windowed calls run in one launch (window_attn.hip): fixed work items of
+// `item_keys` selected keys per query row and KV head, the value columns cut
+// into `slices` slices of kWinSlice (or whole rows), and the merge done by
+// the workgroup that takes the last ticket of its (row, KV head, slice).
+constexpr int kWinSlice = 64;          // value columns per slice when sliced
+constexpr int kWinMaxItemKeys = 1024;  // largest item (a paged item's pool rows live in LDS)
+
+struct WinPlan {
+  int item_keys;  // selected keys per work item (multiple of kChunkQuantum)
+  int n_items;    // work items per query row and KV head (0: the shape needs
+                  // more than kMaxTickets counters)
+  int slices;     // value slices
+  size_t bytes;   // workspace bytes (tickets + partials)
+  size_t off_pm;  // byte offsets inside the workspace (tickets at 0)
+  size_t off_pl;
+  size_t off_pz;
+  size_t off_po;
+};
+
+// Plan of a windowed call: NV query rows, at most `keys` = sink + W selected
+// keys per row.  Depends only on the shape (not on lengths, cache capacity or
+// the cache's element type), so the dense, ring and paged forms of one shape
+// split identically and give bit-identical results.
+WinPlan plan_window(int NV, int Hq, int Hkv, int d, int keys);
+
+hipError_t launch_window(const AttnLaunch& a, hipStream_t stream);
 
 // Compute units of the current device (cached per device).
 int device_cus();

@@ -61,6 +61,14 @@ bool plan_fits(const SplitPlan& p, int Hkv) {
   return static_cast<int64_t>(p.max_items) * Hkv < INT_MAX;
 }
 
+// The windowed kernel's work items (and their workgroups, eight per group
+// of eight items per slice) must be countable in an int.
+bool win_plan_fits(const wmtp::WinPlan& p, int64_t NV, int Hkv) {
+  const int64_t items = NV * Hkv * p.n_items;
+  return p.n_items > 0 && NV * Hkv * p.slices <= wmtp::kMaxTickets &&
+         (items + 7) / 8 * 8 * p.slices < INT_MAX / 2;
+}
+
 // Largest number of query rows per sequence an extend call accepts.
 constexpr int kMaxQueryRows = 4096;
 
@@ -119,12 +127,22 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
     return WMTP_EINVAL;
 
   const int rows_q = B * q_max;
-  const SplitPlan plan =
-      wmtp::plan_split(variant, rows_q, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
-  if (!plan_fits(plan, Hkv)) return WMTP_EUNSUPPORTED;
+  const bool win = windowed_variant(variant);
+  SplitPlan plan{};
+  wmtp::WinPlan wp{};
+  size_t need = 0;
+  if (win) {
+    wp = wmtp::plan_window(rows_q, Hq, Hkv, d, W + sink);
+    if (!win_plan_fits(wp, rows_q, Hkv)) return WMTP_EUNSUPPORTED;
+    need = wp.bytes;
+  } else {
+    plan = wmtp::plan_split(variant, rows_q, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
+    if (!plan_fits(plan, Hkv)) return WMTP_EUNSUPPORTED;
+    need = plan.bytes;
+  }
   if (check_ws) {
-    if (ws_bytes < plan.bytes) return WMTP_EWORKSPACE;
-    if (plan.bytes > 0 && (ws == nullptr || !aligned(ws, 256))) return WMTP_EINVAL;
+    if (ws_bytes < need) return WMTP_EWORKSPACE;
+    if (need > 0 && (ws == nullptr || !aligned(ws, 256))) return WMTP_EINVAL;
   }
 
   AttnLaunch L{};
@@ -170,12 +188,16 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   L.target = plan.target;
   L.chunk_cap = plan.chunk_cap;
   L.max_items = plan.max_items;
+  L.win_keys = wp.item_keys;
+  L.win_items = wp.n_items;
+  L.win_slices = wp.slices;
   if (dry_run) return WMTP_OK;
   char* base = static_cast<char*>(ws);
-  L.pm = reinterpret_cast<float*>(base);
-  L.pl = reinterpret_cast<float*>(base + plan.off_pl);
-  L.pz = reinterpret_cast<float*>(base + plan.off_pz);
-  L.po = reinterpret_cast<float*>(base + plan.off_po);
+  L.tickets = reinterpret_cast<int32_t*>(base);
+  L.pm = reinterpret_cast<float*>(base + (win ? wp.off_pm : plan.off_pm));
+  L.pl = reinterpret_cast<float*>(base + (win ? wp.off_pl : plan.off_pl));
+  L.pz = reinterpret_cast<float*>(base + (win ? wp.off_pz : plan.off_pz));
+  L.po = reinterpret_cast<float*>(base + (win ? wp.off_po : plan.off_po));
   if (wmtp::launch_attention(L, stream) != hipSuccess)
     return WMTP_ELAUNCH;
   return WMTP_OK;
@@ -232,6 +254,11 @@ WMTP_EXPORT size_t wmtp_workspace_bytes(int B, int Hq, int Hkv, int d, int64_t S
   if (check_heads(B, Hq, Hkv, d) != WMTP_OK || B == 0) return 0;
   if (windowed_variant(variant) && check_window(W, sink) != WMTP_OK) return 0;
   if (!windowed_variant(variant) && S_max < 0) return 0;
+  if (windowed_variant(variant)) {
+    const wmtp::WinPlan wp = wmtp::plan_window(B, Hq, Hkv, d, W + sink);
+    if (!win_plan_fits(wp, B, Hkv)) return 0;
+    return wp.bytes;
+  }
   const SplitPlan plan =
       wmtp::plan_split(variant, B, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
   if (!plan_fits(plan, Hkv)) return 0;
