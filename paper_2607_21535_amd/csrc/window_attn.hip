@@ -96,8 +96,15 @@ __device__ __forceinline__ u32x4 coherent_load16(__amdgpu_buffer_rsrc_t r, int b
   return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kCohSc1);
 }
 
+// Waves per workgroup: four, one per SIMD.  (Eight, one 16-key tile each
+// for a 128-key item, measured no faster: the item's tiles share the CU's
+// four SIMDs either way.)
+constexpr int win_waves(int) { return 4; }
+
 template <int D, int DS, KeyMap M, bool F8>
-__global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
+__global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a) {
+  constexpr int NW = win_waves(DS);
+  constexpr int NT = NW * kWave;
   using KT = std::conditional_t<F8, uint8_t, uint16_t>;  // one cached K/V element
   constexpr int NSL = D / DS;  // value slices
   constexpr int VEC = DS / 16;  // slice values of one key per lane in the PV operand
@@ -150,17 +157,27 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
   const int j0 = c * a.item_keys;
   const int j1 = min(j0 + a.item_keys, n_sel);
 
-  RowMap<M> map(S, a.W, a.sink, a.R_w);
+  // Rows of the cache (dense, ring or pool positions) come from the plain
+  // map; a tail map reads the positions at and past S_c -- the fused step's
+  // new rows, or a speculation candidate's own rows -- from the second
+  // buffer, at virtual indices j >= j_c (one compare per load).
+  constexpr KeyMap MB = M == KeyMap::WindowStep ? KeyMap::Window : (has_tail(M) ? KeyMap::Ring : M);
+  RowMap<MB> map(S, a.W, a.sink, a.R_w);
+  [[maybe_unused]] int S_c = S;
+  [[maybe_unused]] int j_c = INT_MAX;
+  [[maybe_unused]] int tbase = 0;  // first row of the candidate's run in the second buffer
   if constexpr (has_tail(M)) {
     int s_commit;
     (void)tail_len<M>(a.lens, a.n_q, a.dd, a.len_cap, b, a.err, false, s_commit);
-    map.S_c = s_commit;
+    S_c = s_commit;
+    bool tail = true;
     if constexpr (M == KeyMap::Tree) {
       const int cand = v - b * a.qps;
-      map.bbase = cand == 0 ? -1 : static_cast<int>(a.rows) + (cand - 1) * a.dd;
-    } else {
-      map.bbase = static_cast<int>(a.rows);
+      tail = cand != 0;  // candidate 0 lives in the ring, as a chain writes it
+      tbase = (cand - 1) * a.dd;
     }
+    // The first virtual index whose position is >= S_c (positions grow with j).
+    if (tail) j_c = S_c < a.sink ? S_c : max(a.sink, S_c - map.shift);
   }
   const int64_t rs = static_cast<int64_t>(a.Hkv) * D;  // elements between rows
   const int64_t seq_rows = is_paged(M) ? 0 : static_cast<int64_t>(b) * a.rows;
@@ -168,18 +185,10 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
   const KT* kbase = static_cast<const KT*>(a.k) + seq_off;
   const KT* vbase = static_cast<const KT*>(a.v) + seq_off;
   [[maybe_unused]] const int64_t off2 = (static_cast<int64_t>(b) * a.rows2 * a.Hkv + g) * D;
-  auto key_row = [&](int r) -> const KT* {
-    if constexpr (has_tail(M)) {
-      if (r >= a.rows) return static_cast<const KT*>(a.k2) + off2 + static_cast<int64_t>(r - a.rows) * rs;
-    }
-    return kbase + static_cast<int64_t>(r) * rs;
-  };
-  auto value_row = [&](int r) -> const KT* {
-    if constexpr (has_tail(M)) {
-      if (r >= a.rows) return static_cast<const KT*>(a.v2) + off2 + static_cast<int64_t>(r - a.rows) * rs;
-    }
-    return vbase + static_cast<int64_t>(r) * rs;
-  };
+  [[maybe_unused]] const KT* kbase2 = has_tail(M) ? static_cast<const KT*>(a.k2) + off2 : nullptr;
+  [[maybe_unused]] const KT* vbase2 = has_tail(M) ? static_cast<const KT*>(a.v2) + off2 : nullptr;
+  // Second-buffer row of virtual index j >= j_c.
+  [[maybe_unused]] auto tail_row = [&](int j) { return (j < a.sink ? j : j + map.shift) - S_c + tbase; };
 
   // Fused draft step: the first item of a row also writes its slice of its KV
   // head's new rows into the cache (ring: the resident ones).  No workgroup
@@ -193,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
   [[maybe_unused]] int64_t cpy_dst = -1;
   auto copy_unit = [&](int u, int64_t& dst) -> bool {  // false: nothing to write for unit u
     const int i = u / kCopyUnits;
-    const int p = map.S_c + i;
+    const int p = S_c + i;
     int slot = p;
     if constexpr (is_ring(M)) {
       if (p >= a.sink && p < S - a.R_w) return false;  // overwritten later in the same append
@@ -204,7 +213,7 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
   };
   auto copy_src = [&](int u) { return off2 + static_cast<int64_t>(u / kCopyUnits) * rs + s * DS + (u % kCopyUnits) * 8; };
   if constexpr (is_step(M)) {
-    if (c == 0 && tid < (S - map.S_c) * kCopyUnits) {
+    if (c == 0 && tid < (S - S_c) * kCopyUnits) {
       int64_t dst;
       if (copy_unit(tid, dst)) {
         cpy_dst = dst;
@@ -217,15 +226,15 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
   constexpr int kKUnits = F8 ? D / 16 : D / 8;  // 16-byte units per key row (one KV head)
   constexpr int kKPitch = kKUnits + 2;          // LDS row pitch in units (conflict-free operand reads)
   constexpr int kKLoads = kTileKeys * kKUnits / kWave;  // load instructions per tile
-  constexpr int kStageBytes = kWaves * kTileKeys * kKPitch * 16;
-  constexpr int kComboBytes = 2 * VEC * kWave * 16;  // the wave-combine regions
+  constexpr int kStageBytes = NW * kTileKeys * kKPitch * 16;
+  constexpr int kComboBytes = (NW / 2) * VEC * kWave * 16;  // the wave-combine regions
   constexpr int kRec = kHdr + kMaxGroup * DS;         // floats of one partial record
   constexpr int kLdsBytes = kStageBytes > kComboBytes ? kStageBytes : kComboBytes;
   static_assert(kRec * 4 <= kLdsBytes, "the partial record is staged in the K tiles' LDS");
   __shared__ __align__(16) unsigned char s_lds[kLdsBytes];
-  __shared__ float s_m[kWaves][16];
-  __shared__ float s_l[kWaves][16];
-  __shared__ float s_z[kWaves][16];
+  __shared__ float s_m[NW][16];
+  __shared__ float s_l[NW][16];
+  __shared__ float s_z[NW][16];
   __shared__ int s_last;
   u32x4* s_k = reinterpret_cast<u32x4*>(s_lds) + wave * kTileKeys * kKPitch;
 
@@ -236,7 +245,7 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
     slots = s_slot;
     const int32_t* trow = a.table + static_cast<int64_t>(b) * a.table_stride;
     bool bad = false;
-    for (int j = j0 + tid; j < j1; j += kThreads) {
+    for (int j = j0 + tid; j < j1; j += NT) {
       int slot = trow[map.row(j)];
       if (slot < 0 || static_cast<int64_t>(slot) >= a.rows) {
         bad = true;
@@ -254,6 +263,18 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
       return map.row(j);
     }
   };
+  auto key_ptr = [&](int j) -> const KT* {
+    if constexpr (has_tail(M)) {
+      if (j >= j_c) return kbase2 + static_cast<int64_t>(tail_row(j)) * rs;
+    }
+    return kbase + static_cast<int64_t>(row_of(j)) * rs;
+  };
+  auto value_ptr = [&](int j) -> const KT* {
+    if constexpr (has_tail(M)) {
+      if (j >= j_c) return vbase2 + static_cast<int64_t>(tail_row(j)) * rs;
+    }
+    return vbase + static_cast<int64_t>(row_of(j)) * rs;
+  };
 
   struct Tile {
     u32x4 kx[kKLoads];
@@ -270,14 +291,12 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
     for (int i = 0; i < kKLoads; ++i) {
       const int f = i * kWave + lane;
       const int j = jt + f / kKUnits;
-      const int r = row_of(j < j1 ? j : j0);
-      T.kx[i] = stream_load<u32x4>(key_row(r) + (f % kKUnits) * (16 / static_cast<int>(sizeof(KT))));
+      T.kx[i] = stream_load<u32x4>(key_ptr(j < j1 ? j : j0) + (f % kKUnits) * (16 / static_cast<int>(sizeof(KT))));
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = jt + 4 * grp + i;
-      const int r = row_of(j < j1 ? j : j0);
-      const KT* p = value_row(r) + s * DS + SEG * col;
+      const KT* p = value_ptr(j < j1 ? j : j0) + s * DS + SEG * col;
       if constexpr (F8) {
         if constexpr (VEC == 16) {
           const u32x4 x = stream_load<u32x4>(p);
@@ -339,19 +358,19 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
 
   // Two register buffers per wave (the next tile's loads in flight while the
   // current one is computed); the four waves take interleaved tiles.
-  const int my_tiles = n_tiles > wave ? (n_tiles - wave + kWaves - 1) / kWaves : 0;
+  const int my_tiles = n_tiles > wave ? (n_tiles - wave + NW - 1) / NW : 0;
   if (n_tiles > 0) {
     Tile T0, T1;
     load_tile(T0, wave);
     int i = 0;
     for (; i + 2 <= my_tiles; i += 2) {
-      const int t = wave + i * kWaves;
-      load_tile(T1, t + kWaves);
+      const int t = wave + i * NW;
+      load_tile(T1, t + NW);
       compute_tile(T0, t);
-      load_tile(T0, t + 2 * kWaves);
-      compute_tile(T1, t + kWaves);
+      load_tile(T0, t + 2 * NW);
+      compute_tile(T1, t + NW);
     }
-    if (i < my_tiles) compute_tile(T0, wave + i * kWaves);
+    if (i < my_tiles) compute_tile(T0, wave + i * NW);
 
     // ---- combine the four waves: (m, l, z) per head, O pairwise ----
     float l_run = st.l, z_run = st.z;
@@ -368,33 +387,34 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
     __syncthreads();
     float Mx = neg_inf();
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) Mx = fmaxf(Mx, s_m[w][col]);
+    for (int w = 0; w < NW; ++w) Mx = fmaxf(Mx, s_m[w][col]);
     float Lx = 0.f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) Lx += s_l[w][col] * __builtin_amdgcn_exp2f(s_m[w][col] - Mx);
+    for (int w = 0; w < NW; ++w) Lx += s_l[w][col] * __builtin_amdgcn_exp2f(s_m[w][col] - Mx);
     float Zx = 0.f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) Zx += s_z[w][col] * __builtin_amdgcn_exp2f(s_m[w][col] - Mx);
+    for (int w = 0; w < NW; ++w) Zx += s_z[w][col] * __builtin_amdgcn_exp2f(s_m[w][col] - Mx);
     const float f = __builtin_amdgcn_exp2f(m_run - Mx);  // 0 for a wave with no tile
 #pragma unroll
     for (int e = 0; e < VEC; ++e) st.acc[e] *= f;
-    // O of the four waves as (w0 + w1) + (w2 + w3), through two LDS regions.
+    // O of the NW waves summed pairwise in a fixed tree ((w0 + w1) + (w2 +
+    // w3)) + ..., through NW / 2 LDS regions; wave 0 ends with the total.
     floatx4* s_x = reinterpret_cast<floatx4*>(s_lds);
-    if (wave & 1) {
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) s_x[((wave >> 1) * VEC + e) * kWave + lane] = st.acc[e];
-    }
-    __syncthreads();
-    if (!(wave & 1)) {
+    for (int h = 1; h < NW; h <<= 1) {
+      if (wave % (2 * h) == h) {
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) st.acc[e] += s_x[((wave >> 1) * VEC + e) * kWave + lane];
-    }
-    __syncthreads();
-    if (wave == 2) {
+        for (int e = 0; e < VEC; ++e) s_x[((wave / (2 * h)) * VEC + e) * kWave + lane] = st.acc[e];
+      }
+      __syncthreads();
+      if (2 * h < NW) {
+        if (wave % (2 * h) == 0) {
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) s_x[e * kWave + lane] = st.acc[e];
+          for (int e = 0; e < VEC; ++e) st.acc[e] += s_x[((wave / (2 * h)) * VEC + e) * kWave + lane];
+        }
+        __syncthreads();
+      }
     }
-    __syncthreads();
     // The partial record of (row, KV head, slice, item): header m, l, z per
     // head, then o [16 heads, DS] (acc[e][jj] of lane (grp, col) is head col
     // at slice column (e / SEG) * 16 * SEG + SEG * (4 grp + jj) + e % SEG),
@@ -421,7 +441,7 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
     }
     __syncthreads();
     const __amdgpu_buffer_rsrc_t rr = record_rsrc(a.rec + ((static_cast<int64_t>(vg) * NSL + s) * a.n_items + c) * kRec);
-    for (int i = tid; i < kRec / 4; i += kThreads)
+    for (int i = tid; i < kRec / 4; i += NT)
       coherent_store16(rr, i * 16, reinterpret_cast<const u32x4*>(s_rec)[i]);
     __builtin_amdgcn_s_waitcnt(0);  // the stores are complete at the point of coherence
   }
@@ -434,7 +454,7 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
         *reinterpret_cast<u32x4*>(kw + cpy_dst) = cpy_k;
         *reinterpret_cast<u32x4*>(vw + cpy_dst) = cpy_v;
       }
-      for (int u = tid + kThreads; u < (S - map.S_c) * kCopyUnits; u += kThreads) {  // long appends
+      for (int u = tid + NT; u < (S - S_c) * kCopyUnits; u += NT) {  // long appends
         int64_t dst;
         if (!copy_unit(u, dst)) continue;
         *reinterpret_cast<u32x4*>(kw + dst) =
@@ -464,7 +484,7 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
   // batch's headers go to LDS and its columns to registers, all loads of a
   // batch in flight together.
   constexpr int Q4 = DS / 4;
-  constexpr int CPT = (kMaxGroup * Q4 + kThreads - 1) / kThreads;  // columns per thread
+  constexpr int CPT = (kMaxGroup * Q4 + NT - 1) / NT;  // columns per thread
   constexpr int NB = 32 / CPT;                                       // items per batch
   static_assert(NB * kHdr * 4 <= kLdsBytes, "a batch's headers are staged in the K tiles' LDS");
   float* s_hdr = reinterpret_cast<float*>(s_lds);
@@ -487,21 +507,21 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
     for (int cc = 0; cc < NB; ++cc)
 #pragma unroll
       for (int x = 0; x < CPT; ++x) {
-        const int colx = tid + x * kThreads;
+        const int colx = tid + x * NT;
         const int hl = colx / Q4, q4 = colx % Q4;
         ov[cc][x] = floatx4{0.f, 0.f, 0.f, 0.f};
         if (cc < nb && hl < G)
           ov[cc][x] = __builtin_bit_cast(floatx4, coherent_load16(rg, ((c0 + cc) * kRec + kHdr + hl * DS + 4 * q4) * 4));
       }
     // m, l, z of the batch's items (12 of the header's 16 chunks each)
-    for (int i = tid; i < nb * 12; i += kThreads) {
+    for (int i = tid; i < nb * 12; i += NT) {
       const int cc = i / 12, ch = i % 12;
       reinterpret_cast<u32x4*>(s_hdr)[cc * (kHdr / 4) + ch] = coherent_load16(rg, (c0 + cc) * kRec * 4 + ch * 16);
     }
     __syncthreads();
 #pragma unroll
     for (int x = 0; x < CPT; ++x) {
-      const int colx = tid + x * kThreads;
+      const int colx = tid + x * NT;
       const int hl = min(colx / Q4, kMaxGroup - 1);
       float mb = Mrun[x];
       for (int cc = 0; cc < nb; ++cc) mb = fmaxf(mb, s_hdr[cc * kHdr + hl]);
@@ -524,7 +544,7 @@ __global__ __launch_bounds__(kThreads) void window_kernel(WinArgs a) {
   }
 #pragma unroll
   for (int x = 0; x < CPT; ++x) {
-    const int colx = tid + x * kThreads;
+    const int colx = tid + x * NT;
     const int hl = colx / Q4, q4 = colx % Q4;
     if (hl >= G) continue;
     float r[4];
@@ -560,7 +580,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   a.rec = L.pm; a.tickets = L.tickets;
   const int64_t groups = (NI + 7) / 8;
   const dim3 grid(static_cast<unsigned>(groups * (D / DS) * 8));
-  hipLaunchKernelGGL((window_kernel<D, DS, M, F8>), grid, dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((window_kernel<D, DS, M, F8>), grid, dim3(win_waves(DS) * kWave), 0, st, a);
   return hipGetLastError();
 }
 
