@@ -209,15 +209,41 @@ def warm_clocks(ms=50.0):
 
 
 def timed(fn, steps, warmup):
+    """Median GPU time of one fn() in seconds: HIP events around each of
+    `steps` back-to-back calls (after `warmup`), on the stream the library
+    enqueues on.  Also returns the wall-clock mean over the same calls."""
     warm_clocks()
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     t0 = time.perf_counter()
-    for _ in range(steps):
+    for a, b in ev:
+        a.record()
         fn()
+        b.record()
     torch.cuda.synchronize()
-    return (time.perf_counter() - t0) / steps
+    wall = (time.perf_counter() - t0) / steps
+    return float(np.median([a.elapsed_time(b) for a, b in ev])) * 1e-3, wall
+
+
+FLUSH_BYTES = 1 << 30  # written between cold-cache repetitions: 4x the 256 MB Infinity Cache
+
+
+def cold_timed(fn, steps, flush):
+    """Median GPU time (seconds) of fn() with the caches cold: before each of
+    `steps` repetitions the flush buffer (FLUSH_BYTES) is written, then fn()
+    is bracketed by HIP events."""
+    fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        flush.fill_(1)
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) for a, b in ev])) * 1e-3
 
 
 def graph_of(fn):
@@ -268,7 +294,7 @@ def sweep_flatness(loop, lengths, steps, warmup):
             loop.lens.fill_(S)
             g = graph_of(body)
             loop.lens.fill_(S)
-            res[name] = timed(g.replay, steps, warmup) * 1e6 / wl.gamma
+            res[name] = timed(g.replay, steps, warmup)[0] * 1e6 / wl.gamma
         rows.append({"S": S, "windowed_us_per_step": round(res["windowed"], 2),
                      "full_us_per_step": round(res["full"], 2)})
         log(f"sweep S={S}: windowed {res['windowed']:.2f} us/step, full {res['full']:.2f} us/step")
@@ -344,6 +370,85 @@ def cache_figures(loop):
         res[f"{name}_attention_call_hot_us"] = round(queued_call_us(fn, spin), 2)
         res[f"{name}_attention_call_cold_us"] = round(queued_call_us(fn, cold), 2)
     log("attention call (hot / cold): " + ", ".join(f"{k}={v}" for k, v in res.items()))
+    del flush
+    torch.cuda.empty_cache()
+    return res
+
+
+def config_block(wl_name, dev, steps):
+    """Figures of another configuration at its own shape (the 8K decode call,
+    the 128K draft loop), each the median of `steps` repetitions: the
+    full-context attention call hot (the smaller of two medians: HIP events
+    around each call inside the running eager draft loop, as for the 1M call,
+    and the call queued behind a clock spin so that its launch is hidden --
+    an 8K call is shorter than the host's launches) and cold (1 GiB written before each repetition) with its
+    achieved HBM rate, the full draft step (append + attention, eager), and
+    the windowed draft step: the gamma-step loop (append + attention per
+    step) captured in a graph, repeated back to back in one graph (hot) or
+    replayed after 1 GiB is written (cold), per step."""
+    wl = I.WORKLOADS[wl_name]
+    loop = DraftLoop(wl, dev, extra_steps=24 * steps + 64)
+    flush = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    spin = lambda: torch.cuda._sleep(400_000)
+    q, out = loop.q[0], loop.out[0]
+    full_call = lambda: W.draft_attn_full(q, loop.k, loop.v, loop.lens, out=out, ws=loop.ws_full, scale=wl.scale)
+    win_call = lambda: W.draft_attn_windowed(q, loop.k, loop.v, loop.lens, wl.W, wl.sink, out=out,
+                                             ws=loop.ws_win, scale=wl.scale)
+    alg = full_call_bytes(wl)
+    hot_loop = float(np.median(attention_call_times(loop, steps, 2))) * 1e3  # inside the running draft loop
+    hot_queued = queued_call_us(full_call, spin, reps=steps)  # launch hidden behind a spin
+    hot = min(hot_loop, hot_queued)  # short calls are launch-bound inside the eager loop
+    cold = cold_timed(full_call, steps, flush) * 1e6
+    win_hot = queued_call_us(win_call, spin, reps=steps)
+    win_cold = cold_timed(win_call, steps, flush) * 1e6
+
+    # the gamma-step loop (append + windowed attention per step): repeated
+    # back to back inside one graph (hot), or one loop after 1 GiB is written
+    reps_per_graph = max(1, 20 // wl.gamma)
+    step_hot = graph_us(loop.step_windowed, calls=reps_per_graph) / wl.gamma
+    gw = graph_of(loop.step_windowed)
+    step_cold = cold_timed(gw.replay, steps, flush) * 1e6 / wl.gamma
+    full_step = timed(loop.step_full, steps, 2)[0] * 1e6 / wl.gamma
+    gb = lambda us: alg / (us * 1e-6) / 1e9
+    res = {"config": {"B": wl.B, "Hq": wl.Hq, "Hkv": wl.Hkv, "d": wl.d, "S": wl.S, "W": wl.W, "sink": wl.sink,
+                      "gamma": wl.gamma},
+           "reps": steps,
+           "full_attention_call_hot_us": round(hot, 2), "full_attention_call_cold_us": round(cold, 2),
+           "full_attention_call_hot_in_loop_us": round(hot_loop, 2),
+           "full_attention_call_hot_queued_us": round(hot_queued, 2),
+           "full_hbm_gbps_hot": round(gb(hot), 1), "full_hbm_gbps_cold": round(gb(cold), 1),
+           "full_frac_of_peak_hot": round(gb(hot) / HBM_PEAK_GBPS, 4),
+           "full_frac_of_peak_cold": round(gb(cold) / HBM_PEAK_GBPS, 4),
+           "algorithmic_bytes_full": alg,
+           "full_us_per_step": round(full_step, 2),
+           "windowed_attention_call_hot_us": round(win_hot, 2), "windowed_attention_call_cold_us": round(win_cold, 2),
+           "windowed_us_per_step_hot": round(step_hot, 2), "windowed_us_per_step_cold": round(step_cold, 2)}
+    log(f"{wl.name}: full call {hot:.1f} us hot ({gb(hot):.0f} GB/s), {cold:.1f} us cold ({gb(cold):.0f} GB/s); "
+        f"windowed step {step_hot:.2f} us hot, {step_cold:.2f} us cold")
+    del loop, flush
+    torch.cuda.empty_cache()
+    return res
+
+
+def windowed_step_cold(loop, steps):
+    """The 1M windowed draft step with 1 GiB written before each repetition,
+    median: the captured gamma-step loop (per step: the first step starts
+    cold) and a single captured step (append + windowed attention)."""
+    wl = loop.wl
+    flush = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=loop.dev)
+
+    def one_step():
+        W.cache_append(loop.k, loop.v, loop.kn[0], loop.vn[0], loop.ones, loop.lens)
+        W.draft_attn_windowed(loop.q[0], loop.k, loop.v, loop.lens, wl.W, wl.sink, out=loop.out[0],
+                              ws=loop.ws_win, scale=wl.scale)
+
+    loop.lens.copy_(loop.lens0)
+    gw = graph_of(loop.step_windowed)
+    g1 = graph_of(one_step)
+    loop.lens.copy_(loop.lens0)
+    res = {"windowed_us_per_step_cold": round(cold_timed(gw.replay, steps, flush) * 1e6 / wl.gamma, 2),
+           "windowed_single_step_cold_us": round(cold_timed(g1.replay, steps, flush) * 1e6, 2)}
+    loop.lens.copy_(loop.lens0)
     del flush
     torch.cuda.empty_cache()
     return res
@@ -453,12 +558,16 @@ def extend_figures(loop):
     rows = wl.gamma + 1
     qx = I.normal_bf16((1, rows, wl.Hq, wl.d), I.stream_seed(wl.seed, I.STREAM_Q, 99), dev)
     nq = torch.full((1,), rows, dtype=torch.int32, device=dev)
+    ws_w = torch.zeros(W.workspace_bytes(rows, wl.Hq, wl.Hkv, wl.d, loop.S_max, wl.W, wl.sink,
+                                         variant=W.VARIANT_WINDOWED), dtype=torch.uint8, device=dev)
+    ws_f = torch.zeros(W.workspace_bytes(rows, wl.Hq, wl.Hkv, wl.d, loop.S_max, variant=W.VARIANT_FULL),
+                       dtype=torch.uint8, device=dev)
     ext = {
         "rows": rows,
         "windowed_us": round(graph_us(lambda: W.draft_extend_windowed(qx, loop.k, loop.v, loop.lens, wl.W, wl.sink,
-                                                                      n_q=nq, scale=wl.scale)), 2),
+                                                                      n_q=nq, scale=wl.scale, ws=ws_w)), 2),
         "full_us": round(event_us(lambda: W.draft_extend_full(qx, loop.k, loop.v, loop.lens, n_q=nq,
-                                                              scale=wl.scale), reps=5, warm=2), 1),
+                                                              scale=wl.scale, ws=ws_f), reps=5, warm=2), 1),
     }
     ext["full_hbm_gbps"] = round(wl.S * wl.Hkv * wl.d * 4 / ext["full_us"] / 1e3, 1)
     log(f"extend ({rows} rows): windowed {ext['windowed_us']} us, full {ext['full_us']} us")
@@ -483,15 +592,19 @@ def paged_figures(loop):
     idx = torch.empty(C, dtype=torch.int32, device=dev)
     q = loop.q[0]
     kv_bytes = S * wl.Hkv * wl.d * 4
+    ws_pf = torch.zeros(W.workspace_bytes(1, wl.Hq, wl.Hkv, wl.d, C, variant=W.VARIANT_PAGED_FULL),
+                        dtype=torch.uint8, device=dev)
+    ws_pw = torch.zeros(W.workspace_bytes(1, wl.Hq, wl.Hkv, wl.d, C, wl.W, wl.sink, variant=W.VARIANT_PAGED_WINDOWED),
+                        dtype=torch.uint8, device=dev)
     paged = {
         "kv_index_build_full_us": round(graph_us(lambda: W.build_kv_indices(
             table, loop.lens, W.VARIANT_PAGED_FULL, indptr=indptr, indices=idx)), 2),
         "kv_index_build_windowed_us": round(graph_us(lambda: W.build_kv_indices(
             table, loop.lens, W.VARIANT_PAGED_WINDOWED, wl.W, wl.sink, indptr=indptr, indices=idx)), 2),
-        "full_us": round(event_us(lambda: W.paged_attn_full(q, kp, vp, table, loop.lens, scale=wl.scale),
-                                  reps=10, warm=3), 1),
+        "full_us": round(event_us(lambda: W.paged_attn_full(q, kp, vp, table, loop.lens, scale=wl.scale,
+                                                             ws=ws_pf), reps=10, warm=3), 1),
         "windowed_us": round(graph_us(lambda: W.paged_attn_windowed(q, kp, vp, table, loop.lens, wl.W, wl.sink,
-                                                                    scale=wl.scale)), 2),
+                                                                    scale=wl.scale, ws=ws_pw)), 2),
         "pool": "1M rows at a random permutation of pool slots",
     }
     paged["full_hbm_gbps"] = round(kv_bytes / paged["full_us"] / 1e3, 1)
@@ -532,9 +645,14 @@ def fp8_figures(loop):
     rows = wl.gamma + 1
     qx = I.normal_bf16((1, rows, wl.Hq, wl.d), I.stream_seed(wl.seed, I.STREAM_Q, 99), dev)
     nq = torch.full((1,), rows, dtype=torch.int32, device=dev)
+    ws_xw = torch.zeros(W.workspace_bytes(rows, wl.Hq, wl.Hkv, wl.d, loop.S_max, wl.W, wl.sink,
+                                          variant=W.VARIANT_WINDOWED), dtype=torch.uint8, device=dev)
+    ws_xf = torch.zeros(W.workspace_bytes(rows, wl.Hq, wl.Hkv, wl.d, loop.S_max, variant=W.VARIANT_FULL),
+                        dtype=torch.uint8, device=dev)
     ext_w = graph_us(lambda: W.draft_extend_windowed_fp8(qx, k8, v8, loop.lens, wl.W, wl.sink, n_q=nq,
-                                                         scale=wl.scale))
-    ext_f = event_us(lambda: W.draft_extend_full_fp8(qx, k8, v8, loop.lens, n_q=nq, scale=wl.scale), reps=3, warm=1)
+                                                         scale=wl.scale, ws=ws_xw))
+    ext_f = event_us(lambda: W.draft_extend_full_fp8(qx, k8, v8, loop.lens, n_q=nq, scale=wl.scale, ws=ws_xf),
+                     reps=3, warm=1)
     res.update({"extend_rows": rows, "extend_windowed_us": round(ext_w, 2), "extend_full_us": round(ext_f, 1)})
     log(f"fp8 extend ({rows} rows): windowed {ext_w:.2f} us, full {ext_f:.1f} us (per-row items)")
     del kr8, vr8
@@ -547,9 +665,14 @@ def fp8_figures(loop):
     kp8[table[0].long()] = k8[0]
     vp8[table[0].long()] = v8[0]
     del k8, v8
-    pfull = event_us(lambda: W.paged_attn_full_fp8(q, kp8, vp8, table, loop.lens, scale=wl.scale), reps=10, warm=3)
+    ws_pf = torch.zeros(W.workspace_bytes(1, wl.Hq, wl.Hkv, wl.d, C, variant=W.VARIANT_PAGED_FULL),
+                        dtype=torch.uint8, device=dev)
+    ws_pw = torch.zeros(W.workspace_bytes(1, wl.Hq, wl.Hkv, wl.d, C, wl.W, wl.sink, variant=W.VARIANT_PAGED_WINDOWED),
+                        dtype=torch.uint8, device=dev)
+    pfull = event_us(lambda: W.paged_attn_full_fp8(q, kp8, vp8, table, loop.lens, scale=wl.scale, ws=ws_pf),
+                     reps=10, warm=3)
     pwin = graph_us(lambda: W.paged_attn_windowed_fp8(q, kp8, vp8, table, loop.lens, wl.W, wl.sink,
-                                                      scale=wl.scale))
+                                                      scale=wl.scale, ws=ws_pw))
     res.update({"paged_full_us": round(pfull, 1), "paged_full_hbm_gbps": round(alg / pfull / 1e3, 1),
                 "paged_windowed_us": round(pwin, 2)})
     log(f"fp8 paged pool: full {pfull:.1f} us, windowed {pwin:.2f} us")
@@ -801,15 +924,15 @@ def main(argv=None):
         return 0
     log("timing full (eager): wall clock per draft step, then HIP events per attention call")
     loop.lens.copy_(loop.lens0)
-    wall_full = timed(loop.step_full, args.steps, args.warmup)
-    us_full_step = wall_full * 1e6 / g
+    med_full, wall_full = timed(loop.step_full, args.steps, args.warmup)
+    us_full_step = med_full * 1e6 / g
     loop.lens.copy_(loop.lens0)
     call_ms = attention_call_times(loop, args.steps, 1)
     call_us = float(call_ms.mean() * 1e3)
     # the fused form of the same step, timed in the same state of the GPU
     for pr in loop.lp:
         pr.copy_(loop.lens0)
-    fused_full_us = timed(loop.step_full_fused, args.steps, args.warmup) * 1e6 / g
+    fused_full_us = timed(loop.step_full_fused, args.steps, args.warmup)[0] * 1e6 / g
     alg_bytes = full_call_bytes(wl)  # at the starting length (S grows by < 0.02% over the loop)
     achieved = alg_bytes / (call_us * 1e-6) / 1e9
     log(f"full: {us_full_step:.1f} us/draft step (wall), attention call {call_us:.1f} us (events), "
@@ -822,11 +945,11 @@ def main(argv=None):
         loop.lens.copy_(loop.lens0)
         gw = graph_of(loop.step_windowed)
         loop.lens.copy_(loop.lens0)
-        win_step = timed(gw.replay, args.steps, args.warmup)
+        win_step = timed(gw.replay, args.steps, args.warmup)[0]
         win_us = win_step * 1e6 / g
         gr = graph_of(loop.step_ring)
         loop.lens_r.copy_(loop.lens0)
-        ring_step = timed(gr.replay, args.steps, args.warmup)
+        ring_step = timed(gr.replay, args.steps, args.warmup)[0]
         ring_us = ring_step * 1e6 / g
         log(f"windowed: {win_us:.2f} us/draft step, ring: {ring_us:.2f} us/draft step (graph replay)")
         for pr in loop.lp + loop.lp_r:
@@ -835,20 +958,28 @@ def main(argv=None):
         grf = graph_of(loop.step_ring_fused)
         for pr in loop.lp + loop.lp_r:
             pr.copy_(loop.lens0)
-        fused = {"windowed_us_per_step": round(timed(gwf.replay, args.steps, args.warmup) * 1e6 / g, 2),
-                 "ring_us_per_step": round(timed(grf.replay, args.steps, args.warmup) * 1e6 / g, 2),
+        fused = {"windowed_us_per_step": round(timed(gwf.replay, args.steps, args.warmup)[0] * 1e6 / g, 2),
+                 "ring_us_per_step": round(timed(grf.replay, args.steps, args.warmup)[0] * 1e6 / g, 2),
                  "full_us_per_step": round(fused_full_us, 2)}
         log("fused append + attention steps: " + ", ".join(f"{k}={v}" for k, v in fused.items()))
         lengths = [S for S in (131072, 262144, 524288, 1048576) if S <= wl.S]
         if not args.no_sweep and len(lengths) > 1:
             sweep = sweep_flatness(loop, lengths, args.steps, args.warmup)
         caches = cache_figures(loop)
+        caches.update(windowed_step_cold(loop, args.steps))
+        log(f"windowed step, cold caches: {caches['windowed_us_per_step_cold']} us per step of the loop, "
+            f"{caches['windowed_single_step_cold_us']} us for one step alone")
     extra = None if (args.only_full or args.no_extras) else extras(loop)
 
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(loop)
         log(f"cpu oracle: {cpu['value']:.0f} us/step on {cpu['cores']} threads")
+
+    blocks = {}
+    if not args.only_full and args.workload == "draft_loop_s1m":
+        for name in ("draft_loop_s128k", "decode_s8k"):
+            blocks[name] = config_block(name, dev, max(20, args.steps))
 
     traffic = profiled_traffic(wl.name)
     ceiling = read_ceiling_gbps(loop)
@@ -870,6 +1001,8 @@ def main(argv=None):
                    "gamma": g, "W": wl.W, "sink": wl.sink, "ring_slots": wl.sink + loop.R_w,
                    "step": f"one draft step: append 1 K/V row + full-context attention ({g} per draft-loop "
                            "iteration, timed back to back)"},
+        "value_statistic": f"median over {args.steps} draft-loop iterations (HIP events), per draft step",
+        "full_us_per_step_wall_mean": round(wall_full * 1e6 / g, 2),
         "full_us_per_step": round(us_full_step, 2),
         "full_attention_call_us": round(call_us, 2),
         "full_hbm_gbps": round(achieved, 1),
@@ -897,6 +1030,7 @@ def main(argv=None):
             "frac_of_read_probe": None if ceiling is None else round(achieved / ceiling, 4),
         },
         "cpu_baseline": cpu,
+        "configs": blocks or None,
         "extras": extra,
         "paper_context": "B200: native draft-decode attention 1608 us per 6 forwards (268 us each), "
                          "windowed+ring 348 us (58 us each); per-decode-step gain +28..44% at 1M",

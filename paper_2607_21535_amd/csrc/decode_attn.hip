@@ -1075,14 +1075,27 @@ hipError_t launch_d(const AttnLaunch& L, hipStream_t st) {
   if (L.kv_fp8) {
     switch (L.variant) {
       case WMTP_VARIANT_FULL: return launch_typed<D, KeyMap::Full, true>(L, st);
+      case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::Window, true>(L, st);
+      case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::Ring, true>(L, st);
       case WMTP_VARIANT_PAGED_FULL: return launch_typed<D, KeyMap::PagedFull, true>(L, st);
+      case WMTP_VARIANT_PAGED_WINDOWED: return launch_typed<D, KeyMap::PagedWindow, true>(L, st);
+      default: return hipErrorInvalidValue;  // no fp8 tree kernels
+    }
+  }
+  if (L.step) {
+    switch (L.variant) {
+      case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::WindowStep, false>(L, st);
+      case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::RingStep, false>(L, st);
       default: return hipErrorInvalidValue;
     }
   }
   switch (L.variant) {
     case WMTP_VARIANT_FULL: return launch_typed<D, KeyMap::Full, false>(L, st);
+    case WMTP_VARIANT_WINDOWED: return launch_typed<D, KeyMap::Window, false>(L, st);
+    case WMTP_VARIANT_RING: return launch_typed<D, KeyMap::Ring, false>(L, st);
     case WMTP_VARIANT_PAGED_FULL: return launch_typed<D, KeyMap::PagedFull, false>(L, st);
-    default: return hipErrorInvalidValue;
+    case WMTP_VARIANT_PAGED_WINDOWED: return launch_typed<D, KeyMap::PagedWindow, false>(L, st);
+    default: return launch_typed<D, KeyMap::Tree, false>(L, st);
   }
 }
 
@@ -1157,8 +1170,8 @@ SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_
 }
 
 hipError_t launch_attention(const AttnLaunch& L, hipStream_t st) {
-  // Every windowed variant runs the one-launch windowed kernel.
-  if (L.variant != WMTP_VARIANT_FULL && L.variant != WMTP_VARIANT_PAGED_FULL) return launch_window(L, st);
+  // Windowed calls with few query rows run the one-launch windowed kernel.
+  if (L.win_items > 0) return launch_window(L, st);
   switch (L.d) {
     case 64: return launch_d<64>(L, st);
     case 128: return launch_d<128>(L, st);

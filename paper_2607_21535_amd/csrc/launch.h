@@ -80,6 +80,7 @@ SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_
 // into `slices` slices of kWinSlice (or whole rows), and the merge done by
 // the workgroup that takes the last ticket of its (row, KV head, slice).
 constexpr int kWinSlice = 64;          // value columns per slice when sliced
+constexpr int kWinOneLaunchRows = 4;   // query rows x KV heads up to which the one-launch kernel runs
 constexpr int kWinMaxItemKeys = 1024;  // largest item (a paged item's pool rows live in LDS)
 
 struct WinPlan {
@@ -99,6 +100,12 @@ struct WinPlan {
 // the cache's element type), so the dense, ring and paged forms of one shape
 // split identically and give bit-identical results.
 WinPlan plan_window(int NV, int Hq, int Hkv, int d, int keys);
+
+// Whether a windowed call of NV query rows runs the one-launch kernel (few
+// rows: latency-bound single decodes) or the split-K kernel plus the merge
+// kernel (many rows: the merge is spread over one workgroup per row and
+// head).  Depends only on the shape, like the plans.
+bool use_window_kernel(int NV, int Hkv);
 
 hipError_t launch_window(const AttnLaunch& a, hipStream_t stream);
 

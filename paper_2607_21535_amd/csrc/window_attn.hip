@@ -695,6 +695,22 @@ WinPlan plan_window(int NV, int Hq, int Hkv, int d, int keys) {
   return p;
 }
 
+bool use_window_kernel(int NV, int Hkv) {
+  // Measured on MI355X at d = 256, Hq = 32, W = 2048: one sequence (2 rows of
+  // KV heads) 13.1 us per draft step against 14.9 us with split + merge; 8
+  // extend rows, 4 tree candidates or 8 sequences are faster with the
+  // split + merge kernels, whose merge runs on a workgroup per row and head.
+  // WMTP_WIN_ONE_LAUNCH_ROWS overrides the threshold (0: never), read at
+  // every call so that tests can run both paths in one process.
+  int64_t max_rows = kWinOneLaunchRows;
+  if (const char* e = std::getenv("WMTP_WIN_ONE_LAUNCH_ROWS"); e != nullptr && *e != '\0') {
+    char* end = nullptr;
+    const long long x = std::strtoll(e, &end, 10);
+    if (end != e && x >= 0) max_rows = x;
+  }
+  return static_cast<int64_t>(NV) * Hkv <= max_rows;
+}
+
 hipError_t launch_window(const AttnLaunch& L, hipStream_t st) {
   switch (L.d) {
     case 64: return launch_d<64>(L, st);

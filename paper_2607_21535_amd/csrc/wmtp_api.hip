@@ -127,7 +127,7 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
     return WMTP_EINVAL;
 
   const int rows_q = B * q_max;
-  const bool win = windowed_variant(variant);
+  const bool win = windowed_variant(variant) && wmtp::use_window_kernel(rows_q, Hkv);
   SplitPlan plan{};
   wmtp::WinPlan wp{};
   size_t need = 0;
@@ -254,7 +254,7 @@ WMTP_EXPORT size_t wmtp_workspace_bytes(int B, int Hq, int Hkv, int d, int64_t S
   if (check_heads(B, Hq, Hkv, d) != WMTP_OK || B == 0) return 0;
   if (windowed_variant(variant) && check_window(W, sink) != WMTP_OK) return 0;
   if (!windowed_variant(variant) && S_max < 0) return 0;
-  if (windowed_variant(variant)) {
+  if (windowed_variant(variant) && wmtp::use_window_kernel(B, Hkv)) {
     const wmtp::WinPlan wp = wmtp::plan_window(B, Hq, Hkv, d, W + sink);
     if (!win_plan_fits(wp, B, Hkv)) return 0;
     return wp.bytes;

@@ -128,3 +128,30 @@ def lens_tensor(lens, dev):
 
 def err_word(dev):
     return torch.zeros(1, dtype=torch.int32, device=dev)
+
+
+WINDOW_PATH_ENV = "WMTP_WIN_ONE_LAUNCH_ROWS"
+WINDOW_PATHS = ("one_launch", "split")
+
+
+class window_path:
+    """Context manager: windowed calls take the one-launch kernel
+    ("one_launch") or the split-K + merge kernels ("split") whatever their
+    row count (the library reads the threshold at every call)."""
+
+    def __init__(self, path):
+        self.value = {"one_launch": str(1 << 30), "split": "0"}[path]
+
+    def __enter__(self):
+        import os
+        self.old = os.environ.get(WINDOW_PATH_ENV)
+        os.environ[WINDOW_PATH_ENV] = self.value
+        return self
+
+    def __exit__(self, *exc):
+        import os
+        if self.old is None:
+            os.environ.pop(WINDOW_PATH_ENV, None)
+        else:
+            os.environ[WINDOW_PATH_ENV] = self.old
+        return False

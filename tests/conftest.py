@@ -31,3 +31,19 @@ def read_golden(name):
 @pytest.fixture
 def golden():
     return read_golden
+
+
+@pytest.fixture(params=["one_launch", "split"])
+def wpath(request):
+    """Runs the test once with windowed calls on the one-launch windowed
+    kernel and once on the split-K + merge kernels (the library reads
+    WMTP_WIN_ONE_LAUNCH_ROWS, the row threshold between them, at every call;
+    0: never the one-launch kernel)."""
+    key = "WMTP_WIN_ONE_LAUNCH_ROWS"
+    old = os.environ.get(key)
+    os.environ[key] = str(1 << 30) if request.param == "one_launch" else "0"
+    yield request.param
+    if old is None:
+        os.environ.pop(key, None)
+    else:
+        os.environ[key] = old

@@ -53,7 +53,7 @@ def _oracle(q, k, v, lens, n_q, scale, variant, W_=None, sink=None):
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(64, 6, 2), (128, 16, 2), (256, 32, 2), (256, 8, 8)])
 @pytest.mark.parametrize("q_max", [1, 3, 8])
-def test_extend_vs_oracle(dev, d, Hq, Hkv, q_max):
+def test_extend_vs_oracle(dev, d, Hq, Hkv, q_max, wpath):
     W_, sink = 64, 4
     rng = np.random.default_rng(d + q_max)
     lens = [1, q_max, 50, sink + W_, sink + W_ + 2, 700, 4099]
@@ -110,7 +110,7 @@ def test_full_extend_many_rows(dev, d, Hq, Hkv, q_max):
     assert err.item() == 0
 
 
-def test_one_row_extend_is_the_decode_step(dev):
+def test_one_row_extend_is_the_decode_step(dev, wpath):
     Hq, Hkv, d = 32, 2, 256
     lens = [5000, 70000, 1, 3000]
     q = I.normal_bf16((4, 1, Hq, d), 41, dev)
@@ -129,7 +129,7 @@ def test_ring_extend_rejects_small_ring(dev):
         W.ring_extend(q, kr, kr, G.lens_tensor([10], dev), 64, 4, 70)  # needs R_w >= 71
 
 
-def test_extend_flags_bad_row_counts(dev):
+def test_extend_flags_bad_row_counts(dev, wpath):
     q = I.normal_bf16((2, 4, 16, 128), 1, dev)
     k = I.normal_bf16((2, 100, 2, 128), 2, dev)
     err = G.err_word(dev)

@@ -144,7 +144,7 @@ SHAPES = [(64, 1, 1), (64, 6, 2), (128, 16, 2), (128, 4, 4), (256, 32, 2), (256,
 
 @pytest.mark.parametrize("d,Hq,Hkv", SHAPES)
 @pytest.mark.parametrize("ks,vs", [(1.0, 1.0), (0.75, 1.5)])
-def test_fp8_attention_vs_oracle(dev, d, Hq, Hkv, ks, vs):
+def test_fp8_attention_vs_oracle(dev, d, Hq, Hkv, ks, vs, wpath):
     seed = 31 * d + Hq + 7 * Hkv
     for W_, sink in ((64, 4), (100, 7)):
         lens = [0, 1, 3, sink + W_, sink + W_ + 1, 17, 1000, 5003]
@@ -183,7 +183,7 @@ def _ring_from_dense(x, lens, sink, R_w):
 
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(64, 6, 2), (128, 16, 2), (256, 32, 2)])
-def test_fp8_ring_equals_windowed_bitwise(dev, d, Hq, Hkv):
+def test_fp8_ring_equals_windowed_bitwise(dev, d, Hq, Hkv, wpath):
     W_, sink, R_w = 64, 4, 71
     lens = [0, 1, 3, sink + W_, sink + W_ + 1, sink + R_w + 1, 777, 5003]
     B, S_max = len(lens), max(lens) + 2
@@ -241,7 +241,7 @@ def _check_exact(out, exp_per_kv, what):
 
 
 @pytest.mark.parametrize("S", [3, 2053, 1048576 + 7])
-def test_fp8_windowed_reads_the_right_rows(dev, S):
+def test_fp8_windowed_reads_the_right_rows(dev, S, wpath):
     G.say(f"fp8 index encoding windowed S={S}")
     sink, Wn = 4, 2048
     k8 = torch.zeros((1, S, Hkv_e, d_e), dtype=torch.uint8, device=dev)
@@ -260,7 +260,7 @@ def test_fp8_windowed_reads_the_right_rows(dev, S):
 
 
 @pytest.mark.parametrize("S", [2060, 1048576 + 3])
-def test_fp8_ring_reads_the_right_slots(dev, S):
+def test_fp8_ring_reads_the_right_slots(dev, S, wpath):
     G.say(f"fp8 index encoding ring S={S}")
     sink, Wn, R_w = 4, 2048, 2056
     kr = torch.zeros((1, sink + R_w, Hkv_e, d_e), dtype=torch.uint8, device=dev)
@@ -321,7 +321,7 @@ def test_fp8_draft_loop_1m(dev):
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(64, 6, 2), (128, 16, 2), (256, 32, 2)])
 @pytest.mark.parametrize("q_max", [3, 8, 12])
-def test_fp8_extend_vs_oracle(dev, d, Hq, Hkv, q_max):
+def test_fp8_extend_vs_oracle(dev, d, Hq, Hkv, q_max, wpath):
     W_, sink, ks, vs = 64, 4, 0.75, 1.5
     rng = np.random.default_rng(3 * d + q_max)
     lens = [1, q_max, 50, sink + W_, sink + W_ + 2, 700, 4099]

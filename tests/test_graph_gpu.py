@@ -19,7 +19,7 @@ from . import _gpu as G
 pytestmark = pytest.mark.gpu
 
 
-def test_graph_replay_matches_eager():
+def test_graph_replay_matches_eager(wpath):
     dev = G.device()
     Hq, Hkv, d, S, gamma, Wn, sink = 32, 2, 256, 70000, 3, 2048, 4
     q = I.normal_bf16((gamma, 1, Hq, d), 1, dev)
@@ -109,7 +109,7 @@ def _graph_matches_eager(reset, body, outputs, state=lambda: [], reps=3):
         _ = (ref[0].float().sum() + 1).item()  # unrelated eager work between replays
 
 
-def test_graph_extend_dense_and_ring():
+def test_graph_extend_dense_and_ring(wpath):
     dev = G.device()
     B, Hq, Hkv, d, Wn, sink, qm = 3, 16, 2, 128, 64, 4, 5
     R_w = Wn + qm
@@ -219,7 +219,7 @@ def test_graph_fp8_append_and_attention():
     _graph_matches_eager(reset, body, lambda: outs, lambda: [k, v, kr, lens, lens_r])
 
 
-def test_graph_tree_speculation_round():
+def test_graph_tree_speculation_round(wpath):
     dev = G.device()
     B, width, dd, Hq, Hkv, d, Wn, sink = 2, 3, 4, 16, 2, 128, 64, 4
     R_w = Wn + dd

@@ -70,7 +70,7 @@ def _check_exact(out, exp_per_kv, what):
 
 
 @pytest.mark.parametrize("S", [1, 3, 2052, 2053, 5000, 131075, 1048576 + 7])
-def test_windowed_reads_the_right_rows(dev, S):
+def test_windowed_reads_the_right_rows(dev, S, wpath):
     G.say(f"index encoding windowed S={S}")
     sink, Wn = 4, 2048
     S_max = S
@@ -92,7 +92,7 @@ def test_windowed_reads_the_right_rows(dev, S):
 
 @pytest.mark.parametrize("S", [5, 2052, 2060, 4100, 1048576 + 3])
 @pytest.mark.parametrize("R_w", [2048, 2056])
-def test_ring_reads_the_right_slots(dev, S, R_w):
+def test_ring_reads_the_right_slots(dev, S, R_w, wpath):
     G.say(f"index encoding ring S={S} R_w={R_w}")
     sink, Wn = 4, 2048
     kr = torch.zeros((1, sink + R_w, Hkv, d), dtype=torch.bfloat16, device=dev)

@@ -70,7 +70,7 @@ def test_index_builder_exact(dev, variant):
 
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(128, 16, 2), (256, 32, 2), (64, 6, 2)])
-def test_paged_attention_equals_dense(dev, d, Hq, Hkv):
+def test_paged_attention_equals_dense(dev, d, Hq, Hkv, wpath):
     lens = [0, 1, 3, 68, 69, 1000, 5003, 12000]
     B, C = len(lens), max(lens) + 5
     P = B * C + 777
@@ -103,7 +103,7 @@ def test_paged_attention_equals_dense(dev, d, Hq, Hkv):
     assert err.item() == 0
 
 
-def test_slot_outside_pool_is_flagged(dev):
+def test_slot_outside_pool_is_flagged(dev, wpath):
     Hq, Hkv, d, P = 16, 2, 128, 1000
     q = I.normal_bf16((1, Hq, d), 1, dev)
     kp = I.normal_bf16((P, Hkv, d), 2, dev)
@@ -158,7 +158,7 @@ class _HostCodes:
 
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(128, 16, 2), (256, 32, 2), (64, 6, 2)])
-def test_paged_fp8_equals_dense_fp8(dev, d, Hq, Hkv):
+def test_paged_fp8_equals_dense_fp8(dev, d, Hq, Hkv, wpath):
     lens = [0, 1, 3, 68, 69, 1000, 5003, 12000]
     B, C = len(lens), max(lens) + 5
     P = B * C + 333

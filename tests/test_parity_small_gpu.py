@@ -49,7 +49,7 @@ def _lens_for(W_, sink):
 
 
 @pytest.mark.parametrize("d,Hq,Hkv", SHAPES)
-def test_full_and_windowed_vs_oracle(dev, d, Hq, Hkv):
+def test_full_and_windowed_vs_oracle(dev, d, Hq, Hkv, wpath):
     seed = 100 * d + 10 * Hq + Hkv
     for W_, sink in WINDOWS:
         lens = _lens_for(W_, sink)
@@ -99,7 +99,7 @@ def _ring_from_dense(k, lens, sink, R_w):
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(64, 6, 2), (128, 16, 2), (256, 32, 2)])
 @pytest.mark.parametrize("W_,sink,slack", [(64, 4, 0), (64, 4, 7), (1, 0, 0), (100, 7, 3)])
-def test_ring_equals_windowed_bitwise(dev, d, Hq, Hkv, W_, sink, slack):
+def test_ring_equals_windowed_bitwise(dev, d, Hq, Hkv, W_, sink, slack, wpath):
     R_w = W_ + slack
     lens = [0, 1, 3, sink + W_, sink + W_ + 1, sink + R_w + 1, 777, 5003]
     B = len(lens)
@@ -140,7 +140,7 @@ def test_select_indices_export_exact(dev):
             assert np.all(slot[b, exp.size:] == -1)
 
 
-def test_length_out_of_range_is_clamped_and_flagged(dev):
+def test_length_out_of_range_is_clamped_and_flagged(dev, wpath):
     d, Hq, Hkv, S_max = 128, 16, 2, 300
     q, k, v = _make(dev, 3, Hq, Hkv, d, S_max, 5)
     err = G.err_word(dev)
@@ -157,7 +157,7 @@ def test_length_out_of_range_is_clamped_and_flagged(dev):
     assert err.item() == 0
 
 
-def test_determinism(dev):
+def test_determinism(dev, wpath):
     d, Hq, Hkv = 256, 32, 2
     lens = [70000, 12345, 1]
     q, k, v = _make(dev, 3, Hq, Hkv, d, max(lens), 9)

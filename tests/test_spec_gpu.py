@@ -62,7 +62,7 @@ def _prefill(dev, rows, kr, vr, lens, seqs, S0, sink, R_w):
 
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(128, 16, 2), (256, 32, 2)])
-def test_chain_speculate_rollback(dev, d, Hq, Hkv):
+def test_chain_speculate_rollback(dev, d, Hq, Hkv, wpath):
     B, Wn, sink, gamma = 4, 64, 4, 5
     R_w = Wn + gamma
     scale = 1.0 / np.sqrt(d)
@@ -117,7 +117,7 @@ def _tree_state(dev, B, width, dd, Hkv, d, sink, R_w):
 
 
 @pytest.mark.parametrize("d,Hq,Hkv,width,dd", [(128, 16, 2, 3, 4), (256, 32, 2, 4, 3), (64, 6, 2, 2, 7)])
-def test_tree_candidates_and_verify(dev, d, Hq, Hkv, width, dd):
+def test_tree_candidates_and_verify(dev, d, Hq, Hkv, width, dd, wpath):
     B, Wn, sink = 3, 64, 4
     R_w = Wn + dd
     scale = 1.0 / np.sqrt(d)
@@ -187,7 +187,7 @@ def test_tree_candidates_and_verify(dev, d, Hq, Hkv, width, dd):
     assert err.item() == 0
 
 
-def test_width_one_tree_equals_chain_bitwise(dev):
+def test_width_one_tree_equals_chain_bitwise(dev, wpath):
     B, Hq, Hkv, d, Wn, sink, dd = 2, 16, 2, 128, 64, 4, 6
     R_w = Wn + dd
     rows = Rows(dev, Hkv, d)
@@ -213,7 +213,7 @@ def test_width_one_tree_equals_chain_bitwise(dev):
         assert torch.equal(kr, kc) and torch.equal(vr, vc)
 
 
-def test_append_past_largest_depth_is_flagged(dev):
+def test_append_past_largest_depth_is_flagged(dev, wpath):
     B, Hkv, d, Wn, sink, dd, width = 2, 2, 64, 8, 2, 2, 3
     R_w = Wn + dd
     rows = Rows(dev, Hkv, d)

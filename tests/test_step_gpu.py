@@ -49,7 +49,7 @@ class Spliced:
 
 @pytest.mark.parametrize("variant", ["full", "windowed", "ring"])
 @pytest.mark.parametrize("d,Hq,Hkv", [(128, 16, 2), (256, 32, 2), (64, 6, 2)])
-def test_step_equals_append_then_attention(dev, variant, d, Hq, Hkv):
+def test_step_equals_append_then_attention(dev, variant, d, Hq, Hkv, wpath):
     Wn, sink = 64, 4
     R_w = Wn + 3
     lens0 = [0, 3, 70, 5000]
@@ -95,7 +95,7 @@ def test_step_equals_append_then_attention(dev, variant, d, Hq, Hkv):
 
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(128, 16, 2), (256, 32, 2)])
-def test_ring_step_append_longer_than_ring(dev, d, Hq, Hkv):
+def test_ring_step_append_longer_than_ring(dev, d, Hq, Hkv, wpath):
     """n_new up to R_w + sink + 3 rows in one fused ring step, from lengths
     0, below the sink, past the window and far past it: positions that a
     later row of the same append overwrites must not be written."""

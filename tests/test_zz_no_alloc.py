@@ -53,7 +53,7 @@ def _run(dev, case, seed):
     G.say(f"noalloc B={B} Hq={Hq} d={d} lens={lens}: equal to the workspace call; oracle err {e}")
 
 
-def test_noalloc_two_calls_then_smaller(dev):
+def test_noalloc_two_calls_then_smaller(dev, wpath):
     G.say("noalloc: two calls in a row, the second smaller")
     _run(dev, CASES[0], 900)
     _run(dev, CASES[1], 910)
