@@ -54,7 +54,9 @@ from paper_2607_21535_amd import wmtp as W  # noqa: E402
 METRIC = "draft-attention µs/step + achieved HBM GB/s at 1M ctx, windowed vs full"
 HBM_PEAK_GBPS = 8000.0
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "split_full_draft_loop_s1m_traffic.txt")
-KERNEL_SOURCES = ["paper_2607_21535_amd/csrc/decode_attn.hip", "paper_2607_21535_amd/csrc/index_map.h",
+# Sources of the full-context split and merge kernels (the traffic figure's kernels).
+KERNEL_SOURCES = ["paper_2607_21535_amd/csrc/decode_attn.hip", "paper_2607_21535_amd/csrc/attn_device.h",
+                  "paper_2607_21535_amd/csrc/index_map.h", "paper_2607_21535_amd/csrc/fp8.h",
                   "paper_2607_21535_amd/csrc/common.h"]
 
 
@@ -246,6 +248,12 @@ def cold_timed(fn, steps, flush):
     return float(np.median([a.elapsed_time(b) for a, b in ev])) * 1e-3
 
 
+def loops_per_graph(gamma, min_steps=20):
+    """Whole gamma-step loops captured in one graph for the windowed timings:
+    at least `min_steps` draft steps per replay."""
+    return max(1, -(-min_steps // gamma))
+
+
 def graph_of(fn):
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
@@ -284,17 +292,19 @@ def attention_call_times(loop, steps, warmup):
 
 def sweep_flatness(loop, lengths, steps, warmup):
     """Per-draft-step time (append + attention) vs length: at each starting
-    length, the captured gamma-step loop replayed back to back (as the
-    windowed and ring figures at 1M are timed)."""
+    length, the captured gamma-step loop (repeated to at least 20 steps)
+    replayed back to back (as the windowed and ring figures at 1M are timed)."""
     wl = loop.wl
+    r = loops_per_graph(wl.gamma)
     rows = []
     for S in lengths:
         res = {}
         for name, body in (("windowed", loop.step_windowed), ("full", loop.step_full)):
+            reps = r if name == "windowed" else 1
             loop.lens.fill_(S)
-            g = graph_of(body)
+            g = graph_of(lambda: [body() for _ in range(reps)])
             loop.lens.fill_(S)
-            res[name] = timed(g.replay, steps, warmup)[0] * 1e6 / wl.gamma
+            res[name] = timed(g.replay, steps, warmup)[0] * 1e6 / (wl.gamma * reps)
         rows.append({"S": S, "windowed_us_per_step": round(res["windowed"], 2),
                      "full_us_per_step": round(res["full"], 2)})
         log(f"sweep S={S}: windowed {res['windowed']:.2f} us/step, full {res['full']:.2f} us/step")
@@ -910,7 +920,7 @@ def main(argv=None):
     if wl.S_lo or wl.R_w:  # the batch and ring workloads: their own timed call
         print(json.dumps(bench_batch(wl, dev, args) if wl.S_lo else bench_ring(wl, dev, args)), flush=True)
         return 0
-    extra = args.warmup * 3 + args.steps * 3 + 64
+    extra = (args.warmup + args.steps) * 24 + 64
     loop = DraftLoop(wl, dev, extra_steps=extra)
     if args.calib_copy:
         calib_copy(dev)
@@ -942,24 +952,28 @@ def main(argv=None):
     win_us = ring_us = None
     sweep = caches = fused = None
     if not args.only_full:
+        # graphs of at least 20 draft steps (whole gamma-step loops), replayed
+        # back to back: short loops would otherwise time the host's launches
+        r = loops_per_graph(g)
+        per = r * g
         loop.lens.copy_(loop.lens0)
-        gw = graph_of(loop.step_windowed)
+        gw = graph_of(lambda: [loop.step_windowed() for _ in range(r)])
         loop.lens.copy_(loop.lens0)
         win_step = timed(gw.replay, args.steps, args.warmup)[0]
-        win_us = win_step * 1e6 / g
-        gr = graph_of(loop.step_ring)
+        win_us = win_step * 1e6 / per
+        gr = graph_of(lambda: [loop.step_ring() for _ in range(r)])
         loop.lens_r.copy_(loop.lens0)
         ring_step = timed(gr.replay, args.steps, args.warmup)[0]
-        ring_us = ring_step * 1e6 / g
+        ring_us = ring_step * 1e6 / per
         log(f"windowed: {win_us:.2f} us/draft step, ring: {ring_us:.2f} us/draft step (graph replay)")
         for pr in loop.lp + loop.lp_r:
             pr.copy_(loop.lens0)
-        gwf = graph_of(loop.step_windowed_fused)
-        grf = graph_of(loop.step_ring_fused)
+        gwf = graph_of(lambda: [loop.step_windowed_fused() for _ in range(r)])
+        grf = graph_of(lambda: [loop.step_ring_fused() for _ in range(r)])
         for pr in loop.lp + loop.lp_r:
             pr.copy_(loop.lens0)
-        fused = {"windowed_us_per_step": round(timed(gwf.replay, args.steps, args.warmup)[0] * 1e6 / g, 2),
-                 "ring_us_per_step": round(timed(grf.replay, args.steps, args.warmup)[0] * 1e6 / g, 2),
+        fused = {"windowed_us_per_step": round(timed(gwf.replay, args.steps, args.warmup)[0] * 1e6 / per, 2),
+                 "ring_us_per_step": round(timed(grf.replay, args.steps, args.warmup)[0] * 1e6 / per, 2),
                  "full_us_per_step": round(fused_full_us, 2)}
         log("fused append + attention steps: " + ", ".join(f"{k}={v}" for k, v in fused.items()))
         lengths = [S for S in (131072, 262144, 524288, 1048576) if S <= wl.S]

@@ -149,10 +149,18 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
       qf[kk] = __builtin_bit_cast(bf16x8, w);
     }
   }
-  int b_unused;
   const bool report = tid == 0 && c == 0 && s == 0 && g == 0;
-  const int S = __builtin_amdgcn_readfirstlane(
-      visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, report, b_unused, a.dd));
+  // The row's length; tail maps also give the committed / old length S_c
+  // (one read of each length array: a second read would be ordered behind
+  // the first one's error report).
+  int S, S_c_len = 0;
+  if constexpr (has_tail(M)) {
+    S = tail_len<M>(a.lens, a.n_q, a.dd, a.len_cap, b, a.err, report && v == b * a.qps, S_c_len);
+  } else {
+    int b_unused;
+    S = visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, report, b_unused, a.dd);
+  }
+  S = __builtin_amdgcn_readfirstlane(S);
   const int n_sel = selected_count<M>(S, a.W, a.sink);
   const int j0 = c * a.item_keys;
   const int j1 = min(j0 + a.item_keys, n_sel);
@@ -167,9 +175,7 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
   [[maybe_unused]] int j_c = INT_MAX;
   [[maybe_unused]] int tbase = 0;  // first row of the candidate's run in the second buffer
   if constexpr (has_tail(M)) {
-    int s_commit;
-    (void)tail_len<M>(a.lens, a.n_q, a.dd, a.len_cap, b, a.err, false, s_commit);
-    S_c = s_commit;
+    S_c = __builtin_amdgcn_readfirstlane(S_c_len);
     bool tail = true;
     if constexpr (M == KeyMap::Tree) {
       const int cand = v - b * a.qps;
@@ -263,14 +269,17 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
       return map.row(j);
     }
   };
-  auto key_ptr = [&](int j) -> const KT* {
-    if constexpr (has_tail(M)) {
+  // `tail` (std::true_type / false_type): whether this item reaches the
+  // tail keys; only the item holding a row's last keys does, so the others
+  // load without the per-key choice.
+  auto key_ptr = [&](int j, auto tail) -> const KT* {
+    if constexpr (decltype(tail)::value) {
       if (j >= j_c) return kbase2 + static_cast<int64_t>(tail_row(j)) * rs;
     }
     return kbase + static_cast<int64_t>(row_of(j)) * rs;
   };
-  auto value_ptr = [&](int j) -> const KT* {
-    if constexpr (has_tail(M)) {
+  auto value_ptr = [&](int j, auto tail) -> const KT* {
+    if constexpr (decltype(tail)::value) {
       if (j >= j_c) return vbase2 + static_cast<int64_t>(tail_row(j)) * rs;
     }
     return vbase + static_cast<int64_t>(row_of(j)) * rs;
@@ -285,18 +294,18 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
   // Keys past j1 read a valid row (j0) and are masked out of the softmax; a
   // tile index past the end re-reads the last tile, so every path issues the
   // same loads and the waits cover exactly the tile being computed.
-  auto load_tile = [&](Tile& T, int t) {
+  auto load_tile = [&](Tile& T, int t, auto tail) {
     const int jt = j0 + min(t, n_tiles - 1) * kTileKeys;
 #pragma unroll
     for (int i = 0; i < kKLoads; ++i) {
       const int f = i * kWave + lane;
       const int j = jt + f / kKUnits;
-      T.kx[i] = stream_load<u32x4>(key_ptr(j < j1 ? j : j0) + (f % kKUnits) * (16 / static_cast<int>(sizeof(KT))));
+      T.kx[i] = stream_load<u32x4>(key_ptr(j < j1 ? j : j0, tail) + (f % kKUnits) * (16 / static_cast<int>(sizeof(KT))));
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = jt + 4 * grp + i;
-      const KT* p = value_ptr(j < j1 ? j : j0) + s * DS + SEG * col;
+      const KT* p = value_ptr(j < j1 ? j : j0, tail) + s * DS + SEG * col;
       if constexpr (F8) {
         if constexpr (VEC == 16) {
           const u32x4 x = stream_load<u32x4>(p);
@@ -359,18 +368,29 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
   // Two register buffers per wave (the next tile's loads in flight while the
   // current one is computed); the four waves take interleaved tiles.
   const int my_tiles = n_tiles > wave ? (n_tiles - wave + NW - 1) / NW : 0;
-  if (n_tiles > 0) {
+  auto run_tiles = [&](auto tail) {
     Tile T0, T1;
-    load_tile(T0, wave);
+    load_tile(T0, wave, tail);
     int i = 0;
     for (; i + 2 <= my_tiles; i += 2) {
       const int t = wave + i * NW;
-      load_tile(T1, t + NW);
+      load_tile(T1, t + NW, tail);
       compute_tile(T0, t);
-      load_tile(T0, t + 2 * NW);
+      load_tile(T0, t + 2 * NW, tail);
       compute_tile(T1, t + NW);
     }
     if (i < my_tiles) compute_tile(T0, wave + i * NW);
+  };
+  if (n_tiles > 0) {
+    if constexpr (has_tail(M)) {
+      if (j1 > j_c) {
+        run_tiles(std::true_type{});
+      } else {
+        run_tiles(std::false_type{});
+      }
+    } else {
+      run_tiles(std::false_type{});
+    }
 
     // ---- combine the four waves: (m, l, z) per head, O pairwise ----
     float l_run = st.l, z_run = st.z;
