@@ -86,8 +86,17 @@ struct WinArgs {
 constexpr int kCohSc1 = 16;  // cache policy bit of the raw buffer builtins: sc1 (device scope)
 constexpr int kHdr = 64;     // header floats of a partial record: m[16], l[16], z[16], 16 unused
 
+// The base is uniform; it is passed through readfirstlane so that the
+// descriptor is built in scalar registers (a descriptor the compiler
+// believes divergent costs a loop around every load that uses it).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t record_rsrc(float* base) {
-  return __builtin_amdgcn_make_buffer_rsrc(base, 0, 0x7fffffff, 0x00020000);
+  // (the builtin returns int: each half goes back through uint32_t, or a
+  // low half with bit 31 set would sign-extend into the high one)
+  const uint64_t p = reinterpret_cast<uint64_t>(base);
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(p >> 32)));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(p & 0xffffffffu)));
+  const uint64_t u = (static_cast<uint64_t>(hi) << 32) | lo;
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<float*>(u), 0, 0x7fffffff, 0x00020000);
 }
 __device__ __forceinline__ void coherent_store16(__amdgpu_buffer_rsrc_t r, int byte_off, u32x4 x) {
   __builtin_amdgcn_raw_buffer_store_b128(x, r, byte_off, 0, kCohSc1);
@@ -201,8 +210,8 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
   // of this launch reads those slots: the appended positions are read from
   // the new-row buffer, and on a ring (R_w >= W) a slot they overwrite held a
   // position outside every window of this call.  A thread's first unit is
-  // loaded here, beside the tile loads, and stored after the tiles (the
-  // store would otherwise wait for its load ahead of them).
+  // loaded here, beside the tile loads, and stored once the workgroup has
+  // its ticket (the merger: after the merge).
   [[maybe_unused]] constexpr int kCopyUnits = DS / 8;  // 16-byte units of the slice
   [[maybe_unused]] u32x4 cpy_k = {}, cpy_v = {};
   [[maybe_unused]] int64_t cpy_dst = -1;
@@ -466,24 +475,29 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
     __builtin_amdgcn_s_waitcnt(0);  // the stores are complete at the point of coherence
   }
 
-  if constexpr (is_step(M)) {
-    if (c == 0) {
-      uint16_t* kw = const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(kbase));
-      uint16_t* vw = const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(vbase));
-      if (cpy_dst >= 0) {
-        *reinterpret_cast<u32x4*>(kw + cpy_dst) = cpy_k;
-        *reinterpret_cast<u32x4*>(vw + cpy_dst) = cpy_v;
-      }
-      for (int u = tid + NT; u < (S - S_c) * kCopyUnits; u += NT) {  // long appends
-        int64_t dst;
-        if (!copy_unit(u, dst)) continue;
-        *reinterpret_cast<u32x4*>(kw + dst) =
-            *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k2) + copy_src(u));
-        *reinterpret_cast<u32x4*>(vw + dst) =
-            *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v2) + copy_src(u));
+  // The fused step's copy of the new rows, stored after the ticket: a
+  // store ahead of the merge's loads would hold them up (memory operations
+  // of a wave complete in order).
+  auto store_copy = [&]() {
+    if constexpr (is_step(M)) {
+      if (c == 0) {
+        uint16_t* kw = const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(kbase));
+        uint16_t* vw = const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(vbase));
+        if (cpy_dst >= 0) {
+          *reinterpret_cast<u32x4*>(kw + cpy_dst) = cpy_k;
+          *reinterpret_cast<u32x4*>(vw + cpy_dst) = cpy_v;
+        }
+        for (int u = tid + NT; u < (S - S_c) * kCopyUnits; u += NT) {  // long appends
+          int64_t dst;
+          if (!copy_unit(u, dst)) continue;
+          *reinterpret_cast<u32x4*>(kw + dst) =
+              *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k2) + copy_src(u));
+          *reinterpret_cast<u32x4*>(vw + dst) =
+              *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v2) + copy_src(u));
+        }
       }
     }
-  }
+  };
 
   // ---- ticket: the last workgroup of (row, KV head, slice) merges ----
   int32_t* ticket = a.tickets + (static_cast<int64_t>(vg) * NSL + s);
@@ -495,19 +509,22 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
     s_last = last;
   }
   __syncthreads();
-  if (!s_last) return;
+  if (!s_last) {
+    store_copy();
+    return;
+  }
 
   // Combine the items that hold keys, in item order, in batches of NB:
   // M = running max of m, and O, L, Z the sums of o, l, z weighted by
   // 2^(m - M) (a batch rescales the sums of the earlier ones when M grows).
-  // Thread t owns float4 columns t, t + 256, ... of [G heads x DS / 4]; a
-  // batch's headers go to LDS and its columns to registers, all loads of a
-  // batch in flight together.
+  // Thread t owns float4 columns t, t + 256, ... of [G heads x DS / 4] and
+  // loads, for a batch's items, those columns and its heads' m, l, z into
+  // registers, all loads in flight together; an item past the batch holds
+  // m = -inf and zeros, which add nothing, so the combine needs no branch
+  // per item.
   constexpr int Q4 = DS / 4;
   constexpr int CPT = (kMaxGroup * Q4 + NT - 1) / NT;  // columns per thread
   constexpr int NB = 32 / CPT;                                       // items per batch
-  static_assert(NB * kHdr * 4 <= kLdsBytes, "a batch's headers are staged in the K tiles' LDS");
-  float* s_hdr = reinterpret_cast<float*>(s_lds);
   const int n_c = ceil_div_i(n_sel, a.item_keys);
   float* gbase = a.rec + (static_cast<int64_t>(vg) * NSL + s) * a.n_items * kRec;
   const __amdgpu_buffer_rsrc_t rg = record_rsrc(gbase);
@@ -523,44 +540,54 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
   for (int c0 = 0; c0 < n_c; c0 += NB) {
     const int nb = min(NB, n_c - c0);
     floatx4 ov[NB][CPT];
+    float hm[NB][CPT], hs[NB][CPT], hz[NB][CPT];
 #pragma unroll
-    for (int cc = 0; cc < NB; ++cc)
+    for (int cc = 0; cc < NB; ++cc) {
+      // The item's record offset is one uniform (scalar) operand of the
+      // loads; a thread's offsets within a record are fixed (columns of
+      // padding heads load those of head G - 1 and are not written).
+      const int so = (c0 + cc) * kRec * 4;
 #pragma unroll
       for (int x = 0; x < CPT; ++x) {
         const int colx = tid + x * NT;
-        const int hl = colx / Q4, q4 = colx % Q4;
+        const int hl = min(colx / Q4, G - 1), q4 = colx % Q4;
         ov[cc][x] = floatx4{0.f, 0.f, 0.f, 0.f};
-        if (cc < nb && hl < G)
-          ov[cc][x] = __builtin_bit_cast(floatx4, coherent_load16(rg, ((c0 + cc) * kRec + kHdr + hl * DS + 4 * q4) * 4));
+        hm[cc][x] = neg_inf();
+        hs[cc][x] = 0.f;
+        hz[cc][x] = 0.f;
+        if (cc < nb) {
+          ov[cc][x] = __builtin_bit_cast(
+              floatx4, __builtin_amdgcn_raw_buffer_load_b128(rg, (kHdr + hl * DS + 4 * q4) * 4, so, kCohSc1));
+          hm[cc][x] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rg, hl * 4, so, kCohSc1));
+          hs[cc][x] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rg, (16 + hl) * 4, so, kCohSc1));
+          hz[cc][x] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rg, (32 + hl) * 4, so, kCohSc1));
+        }
       }
-    // m, l, z of the batch's items (12 of the header's 16 chunks each)
-    for (int i = tid; i < nb * 12; i += NT) {
-      const int cc = i / 12, ch = i % 12;
-      reinterpret_cast<u32x4*>(s_hdr)[cc * (kHdr / 4) + ch] = coherent_load16(rg, (c0 + cc) * kRec * 4 + ch * 16);
     }
-    __syncthreads();
 #pragma unroll
     for (int x = 0; x < CPT; ++x) {
-      const int colx = tid + x * NT;
-      const int hl = min(colx / Q4, kMaxGroup - 1);
       float mb = Mrun[x];
-      for (int cc = 0; cc < nb; ++cc) mb = fmaxf(mb, s_hdr[cc * kHdr + hl]);
-      const float f = __builtin_amdgcn_exp2f(Mrun[x] - mb);  // 0 before the first batch
+#pragma unroll
+      for (int cc = 0; cc < NB; ++cc) mb = fmaxf(mb, hm[cc][x]);
+      const float f = mb == neg_inf() ? 0.f : __builtin_amdgcn_exp2f(Mrun[x] - mb);  // 0 before the first batch
       O[x] *= f;
       L[x] *= f;
       Z[x] *= f;
 #pragma unroll
-      for (int cc = 0; cc < NB; ++cc) {
-        if (cc < nb) {
-          const float w = __builtin_amdgcn_exp2f(s_hdr[cc * kHdr + hl] - mb);
-          O[x] += w * ov[cc][x];
-          L[x] += w * s_hdr[cc * kHdr + 16 + hl];
-          Z[x] += w * s_hdr[cc * kHdr + 32 + hl];
+      for (int c8 = 0; c8 < NB; c8 += 8) {
+        if (c8 < nb) {
+#pragma unroll
+          for (int i = 0; i < 8 && c8 + i < NB; ++i) {
+            const int cc = c8 + i;
+            const float w = cc < nb ? __builtin_amdgcn_exp2f(hm[cc][x] - mb) : 0.f;
+            O[x] += w * ov[cc][x];
+            L[x] += w * hs[cc][x];
+            Z[x] += w * hz[cc][x];
+          }
         }
       }
       Mrun[x] = mb;
     }
-    __syncthreads();  // the next batch's headers reuse the LDS
   }
 #pragma unroll
   for (int x = 0; x < CPT; ++x) {
@@ -576,6 +603,7 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
     if (a.lse != nullptr && s == 0 && q4 == 0)
       a.lse[static_cast<int64_t>(v) * a.Hq + h] = n_c > 0 ? (Mrun[x] + log2f(Z[x])) * kLn2 : neg_inf();
   }
+  store_copy();
   if constexpr (is_step(M)) {
     if (g == 0 && s == 0 && tid == 0) a.lens_out[v] = S;  // this launch reads only the old lengths
   }
