@@ -262,29 +262,52 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // slice of the appended rows into the cache (ring: the resident ones).  No
   // workgroup of this launch reads those slots: the appended positions are
   // read from the new-row buffer, and on a ring (R_w >= W) a slot they
-  // overwrite held a position outside every window of this call.
+  // overwrite held a position outside every window of this call.  A thread's
+  // first unit is loaded here, beside the tile loads, and stored when the
+  // workgroup is done (a store ahead of the tile loads would hold them up:
+  // memory operations of a wave complete in order).
+  [[maybe_unused]] constexpr int kCopyUnits = D / 8;  // 16-byte units per head row
+  [[maybe_unused]] u32x4 cpy_k = {}, cpy_v = {};
+  [[maybe_unused]] int64_t cpy_dst = -1;
+  auto copy_unit = [&](int u, int64_t& src, int64_t& dst) -> bool {  // false: nothing to write for unit u
+    const int i = u / kCopyUnits;
+    const int off = (u % kCopyUnits) * 8;
+    const int p = map.S_c + i;
+    int slot = p;
+    if constexpr (is_ring(M)) {
+      if (p >= a.sink && p < S - a.R_w) return false;  // overwritten later in the same append
+      slot = p < a.sink ? p : a.sink + (p - a.sink) % a.R_w;
+    }
+    src = off2 + static_cast<int64_t>(i) * rs + off;
+    dst = static_cast<int64_t>(slot) * rs + off;
+    return true;
+  };
   if constexpr (is_step(M)) {
-    if (c == 0) {
-      constexpr int kUnits = D / 8;  // 16-byte units per head row
-      const int n_app = S - map.S_c;
-      uint16_t* kw = const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(kbase));
-      uint16_t* vw = const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(vbase));
-      for (int u = static_cast<int>(threadIdx.x); u < n_app * kUnits; u += kThreads) {
-        const int i = u / kUnits;
-        const int off = (u % kUnits) * 8;
-        const int p = map.S_c + i;
-        int slot = p;
-        if constexpr (is_ring(M)) {
-          if (p >= a.sink && p < S - a.R_w) continue;  // overwritten later in the same append
-          slot = p < a.sink ? p : a.sink + (p - a.sink) % a.R_w;
-        }
-        const int64_t src = off2 + static_cast<int64_t>(i) * rs + off;
-        const int64_t dst = static_cast<int64_t>(slot) * rs + off;
-        *reinterpret_cast<u32x4*>(kw + dst) = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k2) + src);
-        *reinterpret_cast<u32x4*>(vw + dst) = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v2) + src);
-      }
+    int64_t src, dst;
+    if (c == 0 && static_cast<int>(threadIdx.x) < (S - map.S_c) * kCopyUnits && copy_unit(threadIdx.x, src, dst)) {
+      cpy_dst = dst;
+      cpy_k = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k2) + src);
+      cpy_v = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v2) + src);
     }
   }
+  auto store_copy = [&]() {
+    if constexpr (is_step(M)) {
+      if (c == 0) {
+        uint16_t* kw = const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(kbase));
+        uint16_t* vw = const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(vbase));
+        if (cpy_dst >= 0) {
+          *reinterpret_cast<u32x4*>(kw + cpy_dst) = cpy_k;
+          *reinterpret_cast<u32x4*>(vw + cpy_dst) = cpy_v;
+        }
+        for (int u = static_cast<int>(threadIdx.x) + kThreads; u < (S - map.S_c) * kCopyUnits; u += kThreads) {
+          int64_t src, dst;  // long appends
+          if (!copy_unit(u, src, dst)) continue;
+          *reinterpret_cast<u32x4*>(kw + dst) = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k2) + src);
+          *reinterpret_cast<u32x4*>(vw + dst) = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v2) + src);
+        }
+      }
+    }
+  };
 
   // Paged: the pool rows of this item's keys, looked up once into LDS.
   [[maybe_unused]] int* slots = nullptr;
@@ -493,7 +516,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     for (int e = 0; e < VEC; ++e) s_x[e * kWave + lane] = st.acc[e];
   }
   __syncthreads();
-  if (wave != 0) return;
+  if (wave != 0) {
+    store_copy();
+    return;
+  }
 #pragma unroll
   for (int e = 0; e < VEC; ++e) st.acc[e] += s_x[e * kWave + lane];
 
@@ -519,6 +545,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
               floatx4{st.acc[e][jj], st.acc[e + 1][jj], st.acc[e + 2][jj], st.acc[e + 3][jj]};
         }
   }
+  store_copy();
 }
 
 // ---------------------------------------------------------------------------
