@@ -101,9 +101,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t record_rsrc(float* base) {
 __device__ __forceinline__ void coherent_store16(__amdgpu_buffer_rsrc_t r, int byte_off, u32x4 x) {
   __builtin_amdgcn_raw_buffer_store_b128(x, r, byte_off, 0, kCohSc1);
 }
-__device__ __forceinline__ u32x4 coherent_load16(__amdgpu_buffer_rsrc_t r, int byte_off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kCohSc1);
-}
 
 // Waves per workgroup: four, one per SIMD.  (Eight, one 16-key tile each
 // for a 128-key item, measured no faster: the item's tiles share the CU's
