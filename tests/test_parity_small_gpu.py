@@ -240,6 +240,17 @@ def _vs_oracle(dev, d, Hq, Hkv, lens, variant, W_=None, sink=None, seed=7):
                         what=f"{variant} d={d} lens={lens[:6]}", spread=np.stack([r[2] for r in refs]))
 
 
+@pytest.mark.parametrize("d,Hq,Hkv", [(128, 16, 2), (256, 32, 2)])
+def test_windowed_merge_in_several_batches(dev, d, Hq, Hkv, wpath):
+    """A 65536-key window: at most 1024 keys per work item, so a row has at
+    least 65 items and the one-launch kernel's merger combines them in
+    several batches of registers (rows past, at and below the threshold)."""
+    W_, sink = 65536, 4
+    lens = [W_ + sink + 3001, W_ + sink, 40007, 5]
+    G.say(f"windowed merge batches d={d} W={W_} lens={lens}")
+    _vs_oracle(dev, d, Hq, Hkv, lens, "windowed", W_, sink)
+
+
 @pytest.mark.parametrize("n_sel", [63 * 64, 64 * 64, 64 * 64 + 1, 65 * 64 + 17])
 def test_merge_around_one_item_per_slot_wide(dev, n_sel):
     """One long row (the 1024-thread merge, 64 item slots): with 64-key items
