@@ -514,11 +514,11 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
   // Combine the items that hold keys, in item order, in batches of NB:
   // M = running max of m, and O, L, Z the sums of o, l, z weighted by
   // 2^(m - M) (a batch rescales the sums of the earlier ones when M grows).
-  // Thread t owns float4 columns t, t + 256, ... of [G heads x DS / 4] and
+  // Thread t owns float4 columns t, t + NT, ... of [G heads x DS / 4] and
   // loads, for a batch's items, those columns and its heads' m, l, z into
-  // registers, all loads in flight together; an item past the batch holds
-  // m = -inf and zeros, which add nothing, so the combine needs no branch
-  // per item.
+  // registers, all loads in flight together; a slot past the batch's last
+  // item holds m = -inf and zeros and gets weight 0, so the combine takes
+  // runs of eight items with no branch inside a run.
   constexpr int Q4 = DS / 4;
   constexpr int CPT = (kMaxGroup * Q4 + NT - 1) / NT;  // columns per thread
   constexpr int NB = 32 / CPT;                                       // items per batch
