@@ -171,6 +171,28 @@ def test_fp8_attention_vs_oracle(dev, d, Hq, Hkv, ks, vs, wpath):
             assert torch.count_nonzero(out[0]) == 0
 
 
+def test_fp8_windowed_merge_in_several_batches(dev, wpath):
+    """A 65536-key window over an fp8 cache: at least 65 items per row, so the
+    one-launch kernel's merger combines them in several batches."""
+    d, Hq, Hkv, W_, sink, ks, vs = 256, 32, 2, 65536, 4, 0.5, 0.25
+    lens = [W_ + sink + 3001, W_ + sink, 40007, 5]
+    B, S_max = len(lens), max(lens) + 3
+    G.say(f"fp8 windowed merge batches W={W_} lens={lens}")
+    q = I.normal_bf16((B, Hq, d), 71, dev)
+    k8 = I.normal_fp8((B, S_max, Hkv, d), 72, dev)
+    v8 = I.normal_fp8((B, S_max, Hkv, d), 73, dev)
+    lt = G.lens_tensor(lens, dev)
+    scale = 1.0 / np.sqrt(d)
+    lse = torch.empty(B, Hq, dtype=torch.float32, device=dev)
+    out = W.draft_attn_windowed_fp8(q, k8, v8, lt, W_, sink, ks, vs, lse=lse)
+    torch.cuda.synchronize()
+    qb = I.bf16_bits(q)
+    refs = [F.attend_sequence_fp8(qb[b], HostCodes(k8[b]), HostCodes(v8[b]), lens[b], scale, ks, vs,
+                                  "windowed", W_, sink, spread=True) for b in range(B)]
+    G.assert_attn_close(out, np.stack([r[0] for r in refs]), lse, np.stack([r[1] for r in refs]),
+                        what="fp8 windowed, several merge batches", spread=np.stack([r[2] for r in refs]))
+
+
 def _ring_from_dense(x, lens, sink, R_w):
     B, _, Hkv, d = x.shape
     ring = torch.zeros((B, sink + R_w, Hkv, d), dtype=x.dtype, device=x.device)
