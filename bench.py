@@ -570,7 +570,7 @@ def extend_figures(loop):
     nq = torch.full((1,), rows, dtype=torch.int32, device=dev)
     ws_w = torch.zeros(W.workspace_bytes(rows, wl.Hq, wl.Hkv, wl.d, loop.S_max, wl.W, wl.sink,
                                          variant=W.VARIANT_WINDOWED), dtype=torch.uint8, device=dev)
-    ws_f = torch.zeros(W.workspace_bytes(rows, wl.Hq, wl.Hkv, wl.d, loop.S_max, variant=W.VARIANT_FULL),
+    ws_f = torch.zeros(W.extend_workspace_bytes(1, rows, wl.Hq, wl.Hkv, wl.d, loop.S_max),
                        dtype=torch.uint8, device=dev)
     ext = {
         "rows": rows,
@@ -657,7 +657,7 @@ def fp8_figures(loop):
     nq = torch.full((1,), rows, dtype=torch.int32, device=dev)
     ws_xw = torch.zeros(W.workspace_bytes(rows, wl.Hq, wl.Hkv, wl.d, loop.S_max, wl.W, wl.sink,
                                           variant=W.VARIANT_WINDOWED), dtype=torch.uint8, device=dev)
-    ws_xf = torch.zeros(W.workspace_bytes(rows, wl.Hq, wl.Hkv, wl.d, loop.S_max, variant=W.VARIANT_FULL),
+    ws_xf = torch.zeros(W.extend_workspace_bytes(1, rows, wl.Hq, wl.Hkv, wl.d, loop.S_max),
                         dtype=torch.uint8, device=dev)
     ext_w = graph_us(lambda: W.draft_extend_windowed_fp8(qx, k8, v8, loop.lens, wl.W, wl.sink, n_q=nq,
                                                          scale=wl.scale, ws=ws_xw))

@@ -110,7 +110,7 @@ size_t wmtp_workspace_bytes(int B, int Hq, int Hkv, int d, int64_t S_max, int W,
  *   out    [B, Hq, d] bf16           attention output
  *   lse    [B, Hq] fp32 or NULL      natural-log log-sum-exp of the logits
  *   scale  logit scale (usually 1/sqrt(d)); must be finite
- *   ws, ws_bytes  workspace, see wmtp_workspace_bytes(WMTP_VARIANT_FULL, ...)
+ *   ws, ws_bytes  workspace, see wmtp_workspace_bytes(..., WMTP_VARIANT_FULL)
  *   err    device int32 error word or NULL
  */
 int wmtp_draft_attn_full(const void* q, const void* k, const void* v, const int32_t* lens,
@@ -125,7 +125,7 @@ int wmtp_draft_attn_full(const void* q, const void* k, const void* v, const int3
  * wmtp_draft_attn_full, plus
  *   W     recent-window length, >= 1 (the current token is always attended)
  *   sink  number of attention-sink keys, >= 0
- * Workspace: wmtp_workspace_bytes(WMTP_VARIANT_WINDOWED, ...).
+ * Workspace: wmtp_workspace_bytes(..., WMTP_VARIANT_WINDOWED).
  */
 int wmtp_draft_attn_windowed(const void* q, const void* k, const void* v, const int32_t* lens,
                              void* out, float* lse, int B, int Hq, int Hkv, int d, int64_t S_max,
@@ -171,7 +171,7 @@ int wmtp_draft_attn_windowed_noalloc(const void* q, const void* k, const void* v
  * never overwrite the live window.  The kept keys and their order are those
  * of wmtp_draft_attn_windowed, so the two calls give bit-identical outputs
  * for the same logical content.
- * Workspace: wmtp_workspace_bytes(WMTP_VARIANT_RING, ...).
+ * Workspace: wmtp_workspace_bytes(..., WMTP_VARIANT_RING).
  */
 int wmtp_ring_attn(const void* q, const void* k_ring, const void* v_ring, const int32_t* lens,
                    void* out, float* lse, int B, int Hq, int Hkv, int d, int W, int sink, int R_w,
@@ -191,9 +191,18 @@ int wmtp_ring_attn(const void* q, const void* k_ring, const void* v_ring, const 
  * lse = -inf.  A draft decode step is the case q_max = 1.  The ring variant
  * needs R_w >= W + q_max - 1 so that the earliest row's window is resident
  * (the paper's chain sizing R_w = W + gamma + 1 covers q_max = gamma + 1).
- * Workspace: wmtp_workspace_bytes(variant, B * q_max, ...).  Other arguments
- * and conventions as for the single-row calls.
+ * Workspace: at least wmtp_workspace_bytes(B * q_max, ..., variant).  Other
+ * arguments and conventions as for the single-row calls.
+ * The full-context form reads each sequence's keys once for all its rows,
+ * cut into work items over the keys.  With only wmtp_workspace_bytes(B *
+ * q_max, ...) bytes its items are sized from the keys of all rows, so a
+ * sequence with n new rows spreads over about 1/n of the device's CUs; with
+ * wmtp_extend_workspace_bytes(B, q_max, ...) bytes or more they are sized
+ * from each sequence's last row (the one that sees every key) and fill the
+ * device.  The two decompositions round differently; each is deterministic.
  */
+size_t wmtp_extend_workspace_bytes(int B, int q_max, int Hq, int Hkv, int d, int64_t S_max, int W,
+                                   int sink, int variant);
 int wmtp_draft_extend_full(const void* q, const void* k, const void* v, const int32_t* lens,
                            const int32_t* n_q, void* out, float* lse, int B, int q_max, int Hq,
                            int Hkv, int d, int64_t S_max, float scale, void* ws, size_t ws_bytes,
@@ -217,8 +226,8 @@ int wmtp_ring_extend(const void* q, const void* k_ring, const void* v_ring, cons
  * and the last W windowed -- and gives the same result, bit for bit, as the
  * dense call over a cache holding the same rows.  Table entries outside
  * [0, pool_rows) read row 0 and raise WMTP_DERR_SLOT_RANGE.
- * Workspace: wmtp_workspace_bytes(WMTP_VARIANT_PAGED_FULL / _WINDOWED, B, Hq,
- * Hkv, d, table_stride, W, sink).
+ * Workspace: wmtp_workspace_bytes(B, Hq, Hkv, d, table_stride, W, sink,
+ * WMTP_VARIANT_PAGED_FULL / _WINDOWED).
  */
 int wmtp_paged_attn_full(const void* q, const void* k_pool, const void* v_pool,
                          const int32_t* req_to_token, const int32_t* lens, void* out, float* lse,
@@ -357,7 +366,7 @@ int wmtp_ring_rollback(int32_t* lens, const int32_t* n_drop, int B, int32_t* err
  * wmtp_tree_attn: q, out [B, width, Hq, d] bf16, lse [B, width, Hq] or NULL.
  *   Candidate c of request b attends the windowed key set (sink + W) of its
  *   own sequence at length S + depth[b].  Workspace:
- *   wmtp_workspace_bytes(WMTP_VARIANT_TREE, B * width, Hq, Hkv, d, 0, W, sink).
+ *   wmtp_workspace_bytes(B * width, Hq, Hkv, d, 0, W, sink, WMTP_VARIANT_TREE).
  * wmtp_tree_reset: depth[b] = 0 for every request (after the verify).  The
  *   accepted tokens' draft rows are then written at their committed
  *   positions by wmtp_ring_append + wmtp_ring_extend (the draft-extend step,
@@ -494,7 +503,7 @@ const char* wmtp_status_string(int status);
 /* ABI version of this header, (major << 16) | minor. */
 int wmtp_abi_version(void);
 
-#define WMTP_ABI_VERSION ((2 << 16) | 1)
+#define WMTP_ABI_VERSION ((2 << 16) | 2)
 
 #ifdef __cplusplus
 }

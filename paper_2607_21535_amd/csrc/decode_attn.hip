@@ -86,6 +86,7 @@ struct SplitArgs {
   const void* v2;
   int64_t rows2;
   int dd;
+  int per_seq;  // item size from each sequence's last row only (see wave_chunk)
 };
 
 struct MergeArgs {
@@ -105,6 +106,7 @@ struct MergeArgs {
   float out_scale;  // value scale of an fp8 cache (1 for bf16)
   int dd;           // Tree: largest speculative depth; fused step: n_max
   int32_t* lens_out;  // fused step: each row's new length
+  int per_seq;        // as in SplitArgs
 };
 
 // Work decomposition, derived the same way by every split and merge
@@ -113,13 +115,18 @@ struct MergeArgs {
 // selected keys per KV head divided by `target`, rounded up to a multiple of
 // kChunkQuantum and clamped to [kChunkQuantum, chunk_cap]; sequence b owns
 // ceil(n_sel(b) / chunk) consecutive items (per query row, see
-// visible_len).  Runs on one whole wave; every lane returns the same value.
-// `first` receives the visible length of row `lane` (0 past the last row),
-// so that a scan over the first 64 rows need not read the lengths again.
+// visible_len).  per_seq (full-context draft-extend with a workspace for
+// it): the total counts only the last new row of each sequence, the one
+// that sees every key, so the multi-row kernel, which reads a sequence's
+// keys once for all its rows, gets about `target` items per KV head however
+// many rows share them (each row still has its own partials).  Runs on one
+// whole wave; every lane returns the same value.  `first` receives the
+// visible length of row `lane` (0 past the last row), so that a scan over
+// the first 64 rows need not read the lengths again.
 template <KeyMap M>
 __device__ int wave_chunk(const int32_t* lens, const int32_t* n_q, int qps, int NV, int64_t len_cap,
                           int W, int sink, int target, int chunk_cap, int32_t* err, bool report, int dd,
-                          int& first) {
+                          bool per_seq, int& first) {
   const int lane = threadIdx.x & (kWave - 1);
   long long total = 0;
   first = 0;
@@ -129,7 +136,11 @@ __device__ int wave_chunk(const int32_t* lens, const int32_t* n_q, int qps, int 
     if (v < NV) {
       const int S = visible_len<M>(lens, n_q, qps, len_cap, err, v, report, b, dd);
       if (base == 0) first = S;
-      total += selected_count<M>(S, W, sink);
+      // per_seq: only the sequence's last new row (n = n_q[b], clamped as
+      // in visible_len) counts; a select rather than a branch
+      const int n = n_q == nullptr ? qps : min(max(n_q[b], 0), qps);
+      const long long keys = selected_count<M>(S, W, sink);
+      total += (!per_seq || v - b * qps == n - 1) ? keys : 0ll;
     }
   }
 #pragma unroll
@@ -152,7 +163,7 @@ __device__ bool locate_item(const SplitArgs& a, int item, int& v_out, int& c_out
     const int lane = threadIdx.x;
     int first;
     const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, NV, a.len_cap, a.W, a.sink, a.target,
-                                    a.chunk_cap, a.err, true, a.dd, first);
+                                    a.chunk_cap, a.err, true, a.dd, a.per_seq != 0, first);
     if (lane == 0) {
       s_v = -1;
       s_chunk = chunk;
@@ -578,7 +589,7 @@ __device__ bool locate_rows_item(const SplitArgs& a, int item, int& b_out, int& 
     const int lane = threadIdx.x;
     int first;
     const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, NV, a.len_cap, a.W, a.sink, a.target,
-                                    a.chunk_cap, a.err, true, a.dd, first);
+                                    a.chunk_cap, a.err, true, a.dd, a.per_seq != 0, first);
     if (lane == 0) {
       s_b = -1;
       s_chunk = chunk;
@@ -904,7 +915,7 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
   if (tid < kWave) {
     int first;
     const int chunk = wave_chunk<M>(a.lens, a.n_q, a.qps, a.B * a.qps, a.len_cap, a.W, a.sink,
-                                    a.target, a.chunk_cap, a.err, false, a.dd, first);
+                                    a.target, a.chunk_cap, a.err, false, a.dd, a.per_seq != 0, first);
     int before = 0, mine = 0;
     for (int base = 0; base <= v; base += kWave) {
       const int vv = base + lane;
@@ -1052,6 +1063,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
     a.target = L.target; a.chunk_cap = L.chunk_cap;
     a.scale_log2 = L.scale * L.k_scale * kLog2e;
     a.k2 = L.k2; a.v2 = L.v2; a.rows2 = L.rows2; a.dd = L.dd;
+    a.per_seq = L.per_seq ? 1 : 0;
     if constexpr (M == KeyMap::Full && (!F8 || D >= 128)) {
       if (L.qps > 1) {
         // Items of the multi-row kernel: sequence b owns ceil(n(b) / chunk)
@@ -1088,6 +1100,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   m.out_scale = L.v_scale;
   m.dd = L.dd;
   m.lens_out = L.lens_out;
+  m.per_seq = L.per_seq ? 1 : 0;
   const unsigned bh = static_cast<unsigned>(NV) * static_cast<unsigned>(L.Hq);
   if (wide)
     hipLaunchKernelGGL((merge_kernel<D, M, kMergeThreads, 64>), dim3(bh, D / 64), dim3(kMergeThreads), 0,
@@ -1156,7 +1169,7 @@ int device_cus() {
   return v;
 }
 
-SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_max) {
+SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_max, int qps) {
   // Aim for one split workgroup per CU (256 on MI355X), with items of at
   // most `chunk_max` keys, so that a long single sequence runs in one
   // balanced round and many or variable-length sequences are cut finely
@@ -1166,7 +1179,9 @@ SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_
   // fewer items also mean fewer partials for the merge.  The kernels pick the
   // item size from the actual lengths; the workspace covers every choice they can
   // make: with per-head target T and chunk in [quantum, cap], the item count
-  // is at most min(B*ceil(n/quantum), max(T + B, B*ceil(n/cap))).
+  // is at most min(B*ceil(n/quantum), max(T + B, B*ceil(n/cap))) for B query
+  // rows.  Items sized per sequence (qps > 1 rows per sequence: the
+  // full-context extend) are up to qps times finer: max(qps*T + B, ...).
   static const int target_env = env_int("WMTP_TARGET_ITEMS", 0);
   static const int chunk_max = std::max(
       kChunkQuantum, env_int("WMTP_CHUNK_MAX", WMTP_CHUNK_MAX_DEFAULT) / kChunkQuantum * kChunkQuantum);
@@ -1183,7 +1198,7 @@ SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_
   if (n_keys_max > 0) {
     const int64_t fine = static_cast<int64_t>(B) * ((n_keys_max + kChunkQuantum - 1) / kChunkQuantum);
     const int64_t coarse = static_cast<int64_t>(B) * ((n_keys_max + cap - 1) / cap);
-    items = std::min(fine, std::max(T + B, coarse));
+    items = std::min(fine, std::max(static_cast<int64_t>(std::max(qps, 1)) * T + B, coarse));
   }
   p.max_items = static_cast<int>(std::min<int64_t>(items, INT32_MAX));
   const size_t rows = static_cast<size_t>(p.max_items) * Hkv * (Hq / Hkv);

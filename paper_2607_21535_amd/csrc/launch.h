@@ -39,6 +39,7 @@ struct AttnLaunch {
   bool step;
   int32_t* lens_out;
   // split plan (from plan_split; full-context variants)
+  bool per_seq;   // items sized from each sequence's last row (full-context extend)
   int target;     // work items per KV head to aim for
   int chunk_cap;  // largest work item, in keys
   int max_items;  // work items per KV head, upper bound over all lengths
@@ -72,8 +73,10 @@ struct SplitPlan {
 };
 
 // Split plan for a validated shape; B counts query rows (sequences x rows per
-// sequence); n_keys_max = most keys one query row attends.
-SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_max);
+// sequence); n_keys_max = most keys one query row attends.  qps > 1: the plan
+// of a full-context extend whose items are sized per sequence (qps rows per
+// sequence), with room for up to qps times more partials.
+SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_max, int qps = 1);
 
 // Windowed calls run in one launch (window_attn.hip): fixed work items of
 // `item_keys` selected keys per query row and KV head, the value columns cut

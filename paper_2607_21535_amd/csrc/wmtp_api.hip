@@ -131,6 +131,7 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   SplitPlan plan{};
   wmtp::WinPlan wp{};
   size_t need = 0;
+  bool per_seq = false;
   if (win) {
     wp = wmtp::plan_window(rows_q, Hq, Hkv, d, W + sink);
     if (!win_plan_fits(wp, rows_q, Hkv)) return WMTP_EUNSUPPORTED;
@@ -139,6 +140,17 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
     plan = wmtp::plan_split(variant, rows_q, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
     if (!plan_fits(plan, Hkv)) return WMTP_EUNSUPPORTED;
     need = plan.bytes;
+    // A full-context extend whose workspace also holds the finer per-sequence
+    // decomposition (wmtp_extend_workspace_bytes) spreads each sequence's
+    // keys over about one workgroup per CU however many rows it has.
+    if (variant == WMTP_VARIANT_FULL && q_max > 1 && check_ws) {
+      const SplitPlan fine = wmtp::plan_split(variant, rows_q, Hq, Hkv, d, keys_max(variant, S_max, W, sink), q_max);
+      if (plan_fits(fine, Hkv) && ws_bytes >= fine.bytes) {
+        plan = fine;
+        need = fine.bytes;
+        per_seq = true;
+      }
+    }
   }
   if (check_ws) {
     if (ws_bytes < need) return WMTP_EWORKSPACE;
@@ -185,6 +197,7 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
   L.scale = scale;
   L.k_scale = k_scale;
   L.v_scale = v_scale;
+  L.per_seq = per_seq;
   L.target = plan.target;
   L.chunk_cap = plan.chunk_cap;
   L.max_items = plan.max_items;
@@ -263,6 +276,16 @@ WMTP_EXPORT size_t wmtp_workspace_bytes(int B, int Hq, int Hkv, int d, int64_t S
       wmtp::plan_split(variant, B, Hq, Hkv, d, keys_max(variant, S_max, W, sink));
   if (!plan_fits(plan, Hkv)) return 0;
   return plan.bytes;
+}
+
+WMTP_EXPORT size_t wmtp_extend_workspace_bytes(int B, int q_max, int Hq, int Hkv, int d, int64_t S_max,
+                                               int W, int sink, int variant) {
+  if (B < 0 || q_max < 1 || q_max > kMaxQueryRows || static_cast<int64_t>(B) * q_max > INT_MAX / 64) return 0;
+  const int rows_q = B * q_max;
+  const size_t coarse = wmtp_workspace_bytes(rows_q, Hq, Hkv, d, S_max, W, sink, variant);
+  if (variant != WMTP_VARIANT_FULL || q_max == 1 || coarse == 0) return coarse;
+  const SplitPlan fine = wmtp::plan_split(variant, rows_q, Hq, Hkv, d, keys_max(variant, S_max, W, sink), q_max);
+  return plan_fits(fine, Hkv) ? std::max(coarse, fine.bytes) : coarse;
 }
 
 WMTP_EXPORT int wmtp_draft_attn_full(const void* q, const void* k, const void* v,

@@ -79,6 +79,7 @@ PROBE_BLOCKS = 512  # WMTP_PROBE_BLOCKS
 
 EXPORTED_SYMBOLS = (
     "wmtp_workspace_bytes",
+    "wmtp_extend_workspace_bytes",
     "wmtp_draft_attn_full",
     "wmtp_draft_attn_windowed",
     "wmtp_draft_attn_windowed_noalloc",
@@ -128,6 +129,7 @@ _SZ = ctypes.c_size_t
 
 _SIGNATURES = {
     "wmtp_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I64, _I, _I, _I]),
+    "wmtp_extend_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, _I64, _I, _I, _I]),
     "wmtp_draft_attn_full": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _F, _P, _SZ, _P, _P]),
     "wmtp_draft_attn_windowed": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _F, _P, _SZ, _P, _P]),
     "wmtp_draft_attn_windowed_noalloc": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I64, _I, _I, _F, _P, _P]),
@@ -185,7 +187,7 @@ class WmtpError(RuntimeError):
 
 # The version of include/wmtp.h these signatures follow, (major << 16) | minor:
 # a library of another major version, or an older minor one, is refused.
-ABI_VERSION = (2 << 16) | 1
+ABI_VERSION = (2 << 16) | 2
 
 
 def lib_path() -> str:
@@ -252,12 +254,21 @@ def workspace_bytes(B, Hq, Hkv, d, S_max=0, W=1, sink=0, variant=VARIANT_FULL) -
     return int(load_library().wmtp_workspace_bytes(B, Hq, Hkv, d, S_max, W, sink, variant))
 
 
-def _workspace(ws, nbytes, device):
-    """The caller's workspace (checked for size), or a new zero-filled one."""
+def extend_workspace_bytes(B, q_max, Hq, Hkv, d, S_max=0, W=1, sink=0, variant=VARIANT_FULL) -> int:
+    """wmtp_extend_workspace_bytes: workspace bytes with which a draft-extend
+    call of B sequences and q_max rows spreads each sequence's keys over the
+    whole device (full context); other variants: as workspace_bytes(B * q_max)."""
+    return int(load_library().wmtp_extend_workspace_bytes(B, q_max, Hq, Hkv, d, S_max, W, sink, variant))
+
+
+def _workspace(ws, nbytes, device, alloc=None):
+    """The caller's workspace (checked for size), or a new zero-filled one of
+    `alloc` bytes (default nbytes)."""
     if ws is None:
-        if nbytes == 0:
+        alloc = nbytes if alloc is None else alloc
+        if alloc == 0:
             return None
-        return torch.zeros(nbytes, dtype=torch.uint8, device=device)
+        return torch.zeros(alloc, dtype=torch.uint8, device=device)
     if ws.numel() * ws.element_size() < nbytes:
         raise WmtpError(EWORKSPACE, "workspace")
     return ws
@@ -398,7 +409,8 @@ def draft_extend_full(q, k, v, lens, n_q=None, out=None, lse=None, scale=None, w
     dev, B, q_max, Hq, d, out = _extend_io(q, k, v, lens, n_q, out, lse)
     S_max, Hkv = k.shape[1], k.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(B * q_max, Hq, Hkv, d, S_max, variant=VARIANT_FULL), dev)
+    ws = _workspace(ws, workspace_bytes(B * q_max, Hq, Hkv, d, S_max, variant=VARIANT_FULL), dev,
+                    extend_workspace_bytes(B, q_max, Hq, Hkv, d, S_max))
     st = load_library().wmtp_draft_extend_full(
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq, Hkv, d,
         S_max, scale, _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))
@@ -642,7 +654,8 @@ def draft_extend_full_fp8(q, k, v, lens, k_scale=1.0, v_scale=1.0, n_q=None, out
     dev, B, q_max, Hq, d, out = _extend_io(q, k, v, lens, n_q, out, lse, fp8=True)
     S_max, Hkv = k.shape[1], k.shape[2]
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ws = _workspace(ws, workspace_bytes(B * q_max, Hq, Hkv, d, S_max, variant=VARIANT_FULL), dev)
+    ws = _workspace(ws, workspace_bytes(B * q_max, Hq, Hkv, d, S_max, variant=VARIANT_FULL), dev,
+                    extend_workspace_bytes(B, q_max, Hq, Hkv, d, S_max))
     st = load_library().wmtp_draft_extend_full_fp8(
         _ptr(q), _ptr(k), _ptr(v), _ptr(lens), _ptr(n_q), _ptr(out), _ptr(lse), B, q_max, Hq, Hkv, d,
         S_max, scale, *_scales(k_scale, v_scale), _ptr(ws), _wsize(ws), _ptr(err), _stream(dev))

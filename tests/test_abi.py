@@ -55,7 +55,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.wmtp_abi_version() == (2 << 16) | 1
+    assert lib.wmtp_abi_version() == (2 << 16) | 2
     # the header, the library and the binding's signatures agree
     with open(os.path.join(ROOT, "include", "wmtp.h")) as f:
         m = re.search(r"#define WMTP_ABI_VERSION \(\(2 << 16\) \| (\d+)\)", f.read())
@@ -80,6 +80,28 @@ def test_workspace_bytes_shapes():
     assert W.workspace_bytes(1, 32, 2, 96, 1000, variant=W.VARIANT_FULL) == 0
     assert W.workspace_bytes(1, 32, 2, 256, 1000, variant=7) == 0
     assert W.workspace_bytes(1, 32, 2, 256, 1000, 0, 4, variant=W.VARIANT_WINDOWED) == 0
+
+
+def test_extend_workspace_bytes():
+    """The full-context extend's per-sequence items need room for up to
+    q_max times more partials; other variants and single rows size as
+    workspace_bytes of B * q_max rows."""
+    for B, q, S in [(1, 8, 1 << 20), (1, 8, 1 << 17), (3, 5, 20000), (2, 1, 5000)]:
+        rows = W.workspace_bytes(B * q, 32, 2, 256, S, variant=W.VARIANT_FULL)
+        ext = W.extend_workspace_bytes(B, q, 32, 2, 256, S)
+        assert ext >= rows > 0
+        assert (ext > rows) == (q > 1)
+        for var, S_, w in [(W.VARIANT_WINDOWED, S, 2048), (W.VARIANT_RING, 2048 + q + 4, 2048)]:
+            assert W.extend_workspace_bytes(B, q, 32, 2, 256, S_, w, 4, variant=var) == \
+                W.workspace_bytes(B * q, 32, 2, 256, S_, w, 4, variant=var)
+    # the finer items are at most q_max * T + rows partials (T = one per CU and KV head)
+    one = W.extend_workspace_bytes(1, 8, 32, 2, 256, 1 << 20)
+    assert one <= 2 * W.workspace_bytes(8 * 8, 32, 2, 256, 1 << 20, variant=W.VARIANT_FULL)
+    # rejected shapes size to 0
+    assert W.extend_workspace_bytes(1, 0, 32, 2, 256, 1000) == 0
+    assert W.extend_workspace_bytes(1, 8, 32, 3, 256, 1000) == 0
+    assert W.extend_workspace_bytes(1, 4097, 32, 2, 256, 1000) == 0
+    assert W.extend_workspace_bytes(0, 8, 32, 2, 256, 1000) == 0
 
 
 def _full(lib, **kw):

@@ -104,9 +104,17 @@ def test_full_extend_many_rows(dev, d, Hq, Hkv, q_max):
     lse = torch.empty(B, q_max, Hq, dtype=torch.float32, device=dev)
     err = G.err_word(dev)
     out = W.draft_extend_full(q, k, v, lt, n_q=nt, lse=lse, err=err)
+    # the same call with only the per-row workspace: items sized from every
+    # row's keys (the coarser decomposition)
+    ws_rows = torch.zeros(W.workspace_bytes(B * q_max, Hq, Hkv, d, S_max, variant=W.VARIANT_FULL),
+                          dtype=torch.uint8, device=dev)
+    assert ws_rows.numel() < W.extend_workspace_bytes(B, q_max, Hq, Hkv, d, S_max)
+    lse_c = torch.empty_like(lse)
+    out_c = W.draft_extend_full(q, k, v, lt, n_q=nt, lse=lse_c, err=err, ws=ws_rows)
     torch.cuda.synchronize()
     o_ref, l_ref, spread = _oracle(q, k, v, lens, n_q, 1.0 / np.sqrt(d), "full")
     G.assert_attn_close(out, o_ref, lse, l_ref, what="extend many rows", spread=spread)
+    G.assert_attn_close(out_c, o_ref, lse_c, l_ref, what="extend many rows, per-row items", spread=spread)
     assert err.item() == 0
 
 
