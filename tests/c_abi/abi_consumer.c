@@ -118,12 +118,17 @@ int main(void) {
   const size_t ws_ext = wmtp_workspace_bytes(B * QMAX, HQ, HKV, D, S_MAX, W, SINK, WMTP_VARIANT_WINDOWED);
   const size_t ws_pool = wmtp_workspace_bytes(B, HQ, HKV, D, S_MAX, W, SINK, WMTP_VARIANT_PAGED_WINDOWED);
   const size_t ws_tree = wmtp_workspace_bytes(B * WIDTH, HQ, HKV, D, 0, W, SINK, WMTP_VARIANT_TREE);
+  /* the full-context extend's per-sequence items need more room than its rows' */
+  const size_t ws_xfull = wmtp_extend_workspace_bytes(B, QMAX, HQ, HKV, D, S_MAX, W, SINK, WMTP_VARIANT_FULL);
+  check(ws_xfull > wmtp_workspace_bytes(B * QMAX, HQ, HKV, D, S_MAX, W, SINK, WMTP_VARIANT_FULL),
+        "wmtp_extend_workspace_bytes (full) exceeds wmtp_workspace_bytes of B * q_max rows");
   check(ws_bytes > 0 && ws_win > 0 && ws_ring > 0 && ws_ext > 0 && ws_pool > 0, "workspace sizes are positive");
   if (ws_win > ws_bytes) ws_bytes = ws_win;
   if (ws_ring > ws_bytes) ws_bytes = ws_ring;
   if (ws_ext > ws_bytes) ws_bytes = ws_ext;
   if (ws_pool > ws_bytes) ws_bytes = ws_pool;
   if (ws_tree > ws_bytes) ws_bytes = ws_tree;
+  if (ws_xfull > ws_bytes) ws_bytes = ws_xfull;
   void* ws = dev_alloc(ws_bytes);
   hip_ok(hipMemset(ws, 0, ws_bytes), "workspace zero-filled once");
   const float scale = 1.0f / sqrtf((float)D);
@@ -202,6 +207,15 @@ int main(void) {
   check(st == WMTP_OK, "wmtp_draft_extend_windowed returns OK");
   hip_ok(hipDeviceSynchronize(), "extend");
   check_rows(out3, lse3, sel_ext, B * QMAX, 0x3F80, "windowed extend");
+  /* The same rows over the full context (row t sees lens - n + t + 1 keys). */
+  int sel_xfull[B * QMAX];
+  for (int b = 0; b < B; ++b)
+    for (int t = 0; t < QMAX; ++t) sel_xfull[b * QMAX + t] = t < n_q_h[b] ? lens_h[b] - n_q_h[b] + t + 1 : 0;
+  st = wmtp_draft_extend_full(q3, k, v, lens, n_q, out3, lse3, B, QMAX, HQ, HKV, D, S_MAX, scale, ws, ws_bytes, err,
+                              NULL);
+  check(st == WMTP_OK, "wmtp_draft_extend_full returns OK");
+  hip_ok(hipDeviceSynchronize(), "full extend");
+  check_rows(out3, lse3, sel_xfull, B * QMAX, 0x3F80, "full extend");
 
   /* fp8 cache: K codes 0, V codes 0x38 (E4M3 1.0), value scale 2 -> output 2. */
   const size_t row8 = (size_t)HKV * D;
