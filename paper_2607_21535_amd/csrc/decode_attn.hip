@@ -637,6 +637,27 @@ __device__ bool locate_rows_item(const SplitArgs& a, int item, int& b_out, int& 
   return b_out >= 0;
 }
 
+// Instruction order of a run of N LDS operand reads, each feeding R MFMAs:
+// the first kAhead reads go out before any of the run's MFMAs and every
+// later read follows the MFMAs of the operand read kAhead before it, so
+// kAhead reads are in flight while the MFMAs run (left to itself the
+// scheduler kept one or two).  Measured on the multi-row kernel: kAhead 5
+// took 8 rows at 1M from 506-520 to 487-490 us (8 and 12 gained less, 12
+// lost ground at 3 rows).
+template <int N, int R>
+__device__ __forceinline__ void pipeline_lds_reads() {
+  constexpr int kAhead = N < 5 ? N : 5;
+  constexpr int kDsRead = 0x100, kMfma = 0x008;  // sched_group_barrier instruction classes
+#pragma unroll
+  for (int i = 0; i < kAhead; ++i) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+#pragma unroll
+  for (int i = kAhead; i < N; ++i) {
+    __builtin_amdgcn_sched_group_barrier(kMfma, R, 0);
+    __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(kMfma, R * kAhead, 0);
+}
+
 // F8: the cache holds E4M3 codes; a step's codes are widened to bf16 when
 // they are stored into LDS (the same layouts as for a bf16 cache), so the
 // compute is the same; the key scale is folded into the logit scale and the
@@ -825,6 +846,7 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
               sc[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                   __builtin_bit_cast(bf16x8, sk[((u0 + u) * kTileKeys + col) * kPitch + 4 * kk + grp]), qf[kk],
                   sc[u], 0, 0, 0);
+          pipeline_lds_reads<KCH * NT, 1>();
           bf16x4 pop[NT];
           st.template weigh<NT, true>(sc, js, j_end, sl2, grp, pop);
           // O^T += V^T . P^T over tile pairs: output tile sg * SEG + e takes
@@ -842,6 +864,7 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
                 st.acc[sg * SEG + e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), pp,
                                                                                 st.acc[sg * SEG + e], 0, 0, 0);
               }
+            pipeline_lds_reads<NSEG * SEG, 1>();
           }
         }
       }
