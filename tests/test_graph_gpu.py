@@ -124,8 +124,10 @@ def test_graph_extend_dense_and_ring(wpath):
     kr = torch.zeros((B, sink + R_w, Hkv, d), dtype=torch.bfloat16, device=dev)
     vr = torch.zeros_like(kr)
     lens, lens_r = G.lens_tensor(S0, dev), G.lens_tensor(S0, dev)
-    outs = [torch.empty_like(q) for _ in range(3)]
+    outs = [torch.empty_like(q) for _ in range(4)]
     ws = torch.zeros(W.workspace_bytes(B * qm, Hq, Hkv, d, 500, variant=W.VARIANT_FULL), dtype=torch.uint8, device=dev)
+    # the full-context extend with items sized per sequence (its own workspace)
+    ws_x = torch.zeros(W.extend_workspace_bytes(B, qm, Hq, Hkv, d, 500), dtype=torch.uint8, device=dev)
     ws_w = torch.zeros(W.workspace_bytes(B * qm, Hq, Hkv, d, 500, Wn, sink, variant=W.VARIANT_WINDOWED),
                        dtype=torch.uint8, device=dev)
 
@@ -140,6 +142,7 @@ def test_graph_extend_dense_and_ring(wpath):
     def body():
         W.cache_append(k, v, kn, vn, n_new, lens)
         W.draft_extend_full(q, k, v, lens, n_q=n_new, out=outs[0], ws=ws)
+        W.draft_extend_full(q, k, v, lens, n_q=n_new, out=outs[3], ws=ws_x)
         W.draft_extend_windowed(q, k, v, lens, Wn, sink, n_q=n_new, out=outs[1], ws=ws_w)
         W.ring_append(kr, vr, kn, vn, n_new, lens_r, sink, R_w)
         W.ring_extend(q, kr, vr, lens_r, Wn, sink, R_w, n_q=n_new, out=outs[2], ws=ws_w)
