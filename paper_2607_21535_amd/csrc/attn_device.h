@@ -97,6 +97,38 @@ __device__ __forceinline__ T stream_load(const E* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const T*>(p));
 }
 
+// Maximum and sum of x over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (one
+// query head of an MFMA tile), as with shuffles by lane ^ 16 and then
+// lane ^ 32, but without their LDS permutes and waits: v_permlane16_swap
+// exchanges lanes 16..31 and 48..63 of its first register with lanes 0..15
+// and 32..47 of its second, v_permlane32_swap lanes 32..63 of the first with
+// lanes 0..31 of the second, so with x in both registers each lane then holds
+// x of itself and of its partner, in one VALU op.  (The compiler's builtins
+// for these swaps returned the first register twice in this toolchain, so
+// they are written as inline assembly; the s_nop covers the wait a swap needs
+// after a VALU write of its operands.)  The sum adds the same pairs in the
+// same order as the shuffles, so its bits are theirs.
+__device__ __forceinline__ void swap_rows16(float& a, float& b) {
+  asm("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void swap_rows32(float& a, float& b) {
+  asm("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ float max_across_rows(float x) {
+  float a = x, b = x;
+  swap_rows16(a, b);
+  float c = fmaxf(a, b), e = c;
+  swap_rows32(c, e);
+  return fmaxf(c, e);
+}
+__device__ __forceinline__ float sum_across_rows(float x) {
+  float a = x, b = x;
+  swap_rows16(a, b);
+  float c = a + b, e = c;
+  swap_rows32(c, e);
+  return c + e;
+}
+
 // Registers of one 16-key tile on one lane.  kx holds 16-byte units
 // 64 i + lane of the tile's K rows, key-major (8 bf16 values or 16 fp8 codes
 // each); vx holds the lane's VEC values (or codes) of keys 4*grp + i as words.
@@ -158,9 +190,7 @@ struct OnlineHeads {
     for (int u = 0; u < NT; ++u)
 #pragma unroll
       for (int i = 0; i < 4; ++i) mt = fmaxf(mt, sv[u][i]);
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m, mt);
+    const float m_new = fmaxf(m, max_across_rows(mt));
     if (__any(m_new > m)) {
       const float alpha = __builtin_amdgcn_exp2f(m - m_new);
       l *= alpha;
@@ -180,6 +210,68 @@ struct OnlineHeads {
         const float p1 = __builtin_amdgcn_exp2f(sv[u][2 * i + 1] - m);
         pb[i] = pack_bf16x2(p0, p1);
         l += bf16_lo(pb[i]) + bf16_hi(pb[i]);
+        z += p0 + p1;
+      }
+      pop[u] = __builtin_bit_cast(bf16x4, u32x2{pb[0], pb[1]});
+    }
+  }
+
+  // weigh with fewer vector instructions, for the multi-row kernel (whose
+  // time is set by its compute waves).  Requires sl2 > 0 (the kernel puts
+  // the sign of the scale into its queries, exactly, and stands in the
+  // smallest normal float for a zero scale: every weight is then exp2 of a
+  // number within |s| 2^-126 of 0, i.e. 1 to fp32 precision, as for the
+  // scale 0, and masked keys stay at exp2(-inf) = 0 where -inf * 0 would be
+  // NaN): the maximum is then
+  // taken over the raw logits (rounding is monotone, so it scales to the
+  // maximum of the scaled ones) and the scale is folded into the exponent,
+  // exp2(fma(s, sl2, -m)); the maxima across the four lanes of a head use
+  // gfx950's permlane swaps (one VALU op each instead of an LDS permute and
+  // its wait); the sum of the rounded weights is a bf16 dot product with
+  // (1, 1) per weight pair.  The weights and sums may differ from weigh's in
+  // the last bit.
+  template <int NT>
+  __device__ __forceinline__ void weigh_lean(const floatx4 (&s)[NT], int jt, int j_end, float sl2, int grp,
+                                             bf16x4 (&pop)[NT]) {
+    const bool tail = jt + kTileKeys * NT > j_end;  // wave-uniform: the group reaches the row's end
+    float sv[NT][4];
+#pragma unroll
+    for (int u = 0; u < NT; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sv[u][i] = s[u][i];
+    if (tail) {
+#pragma unroll
+      for (int u = 0; u < NT; ++u)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (jt + kTileKeys * u + 4 * grp + i >= j_end) sv[u][i] = neg_inf();
+    }
+    float mt = neg_inf();
+#pragma unroll
+    for (int u = 0; u < NT; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mt = fmaxf(mt, sv[u][i]);
+    // Key jt is visible, so mt is finite after the exchange.
+    const float m_new = fmaxf(m, max_across_rows(mt) * sl2);
+    if (__any(m_new > m)) {
+      const float alpha = __builtin_amdgcn_exp2f(m - m_new);
+      l *= alpha;
+      z *= alpha;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] *= alpha;
+    }
+    m = m_new;
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3f803f80u);
+#pragma unroll
+    for (int u = 0; u < NT; ++u) {
+      uint32_t pb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[u][2 * i], sl2, -m));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[u][2 * i + 1], sl2, -m));
+        pb[i] = pack_bf16x2(p0, p1);
+        l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pb[i]), ones, l, false);
         z += p0 + p1;
       }
       pop[u] = __builtin_bit_cast(bf16x4, u32x2{pb[0], pb[1]});

@@ -483,10 +483,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // ---- combine the four waves: (m, l) per head, then O in wave order ----
   float l_run = st.l, z_run = st.z;
   const float m_run = st.m;
-  l_run += __shfl_xor(l_run, 16);
-  l_run += __shfl_xor(l_run, 32);
-  z_run += __shfl_xor(z_run, 16);
-  z_run += __shfl_xor(z_run, 32);
+  l_run = sum_across_rows(l_run);
+  z_run = sum_across_rows(z_run);
   __shared__ float s_m[kWaves][16];
   __shared__ float s_l[kWaves][16];
   __shared__ float s_z[kWaves][16];
@@ -676,7 +674,6 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
   // conflicts on gfx950.
   constexpr int kPitch = kUnits + 2;
   constexpr int kLUnits = F8 ? D / 16 : kUnits;  // 16-byte units per row as loaded (codes or bf16)
-  constexpr int kPer = 16 / static_cast<int>(sizeof(KT));  // elements per loaded unit
   constexpr int kLoads = kRowStep * kLUnits / kRowThreads;  // K (and V) units per thread and step
   static_assert(kLoads == 1 || kLoads == 2 || kLoads == 4, "a thread's keys must sit in one 4-key run");
   static_assert(kRowStep * kUnits % kRowThreads == 0, "step must tile the workgroup");
@@ -732,22 +729,39 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
   // Thread tid holds loaded unit tid % kLUnits of the kLoads consecutive keys
   // kLoads * (tid / kLUnits) + i of a step (a run inside one 4-key group of a
   // tile); the lanes of a load instruction cover whole rows of several keys.
-  // Keys past j1 read row j0 (masked out of every row's softmax).
+  // A load addresses the step's first row (wave-uniform) plus a fixed 32-bit
+  // byte offset per thread and key; keys past j1 read the step's first row
+  // (masked out of every row's softmax).
   const int my_unit = tid % kLUnits;
   const int my_key0 = kLoads * (tid / kLUnits);
+  const uint32_t row_bytes = static_cast<uint32_t>(rs) * sizeof(KT);  // one token row, all KV heads
+  uint32_t my_off[kLoads];
+#pragma unroll
+  for (int i = 0; i < kLoads; ++i) my_off[i] = (my_key0 + i) * row_bytes + my_unit * 16u;
   // Where this thread's keys and value columns land in the transposed V:
   // k' of its first key, and the row of value column 8 my_unit + x.
   const int my_kq = ((my_key0 >> 5) << 5) + ((my_key0 & 15) >> 2) * 8 + ((my_key0 >> 4) & 1) * 4 + (my_key0 & 3);
   auto vt_row = [](int dd) { return ((dd % SEG) * NSEG + dd / (16 * SEG)) * 16 + (dd / SEG) % 16; };
   u32x4 rk[kLoads], rv[kLoads];
   auto load = [&](int s) {
-    const int js = j0 + s * kRowStep + my_key0;
+    const int js = j0 + s * kRowStep;
+    const int64_t step_off = static_cast<int64_t>(js) * row_bytes;
+    const char* ks = reinterpret_cast<const char*>(kbase) + step_off;
+    const char* vs = reinterpret_cast<const char*>(vbase) + step_off;
+    const int left = j1 - js;  // keys of the chunk from this step on (wave-uniform)
+    if (left >= kRowStep) {
 #pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      const int j = js + i;
-      const int64_t off = static_cast<int64_t>(j < j1 ? j : j0) * rs + my_unit * kPer;
-      rk[i] = stream_load<u32x4>(kbase + off);
-      rv[i] = stream_load<u32x4>(vbase + off);
+      for (int i = 0; i < kLoads; ++i) {
+        rk[i] = stream_load<u32x4>(ks + my_off[i]);
+        rv[i] = stream_load<u32x4>(vs + my_off[i]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < kLoads; ++i) {
+        const uint32_t off = my_key0 + i < left ? my_off[i] : my_unit * 16u;
+        rk[i] = stream_load<u32x4>(ks + off);
+        rv[i] = stream_load<u32x4>(vs + off);
+      }
     }
   };
   auto stash = [&](int buf) {
@@ -797,7 +811,11 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
       }
     }
   };
-  const float sl2 = a.scale_log2;
+  // weigh_lean takes a positive scale: a negative one is applied as its
+  // magnitude with the queries negated (exact in bf16), zero as the smallest
+  // normal float.
+  const float sl2 = fmaxf(fabsf(a.scale_log2), __FLT_MIN__);
+  const uint32_t q_sign = a.scale_log2 < 0.f ? 0x80008000u : 0u;
 
   for (int t0 = 0; t0 < n; t0 += kRowWaves) {
     const int t = t0 + wave;
@@ -815,7 +833,7 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
 #pragma unroll
       for (int kk = 0; kk < KCH; ++kk) {
         u32x4 w = live ? *reinterpret_cast<const u32x4*>(qp + kk * 32 + grp * 8) : u32x4{0u, 0u, 0u, 0u};
-        qf[kk] = __builtin_bit_cast(bf16x8, w);
+        qf[kk] = __builtin_bit_cast(bf16x8, w ^ q_sign);
       }
     }
 
@@ -848,7 +866,7 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
                   sc[u], 0, 0, 0);
           pipeline_lds_reads<KCH * NT, 1>();
           bf16x4 pop[NT];
-          st.template weigh<NT, true>(sc, js, j_end, sl2, grp, pop);
+          st.template weigh_lean<NT>(sc, js, j_end, sl2, grp, pop);
           // O^T += V^T . P^T over tile pairs: output tile sg * SEG + e takes
           // the transposed V unit of value column 16 SEG sg + SEG col + e,
           // keys 8 grp .. 8 grp + 7 of the pair.
@@ -880,10 +898,8 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
 #pragma unroll
       for (int off = kWave / 2; off > 0; off >>= 1) later += __shfl_xor(later, off);
       float l = st.l, z = st.z;
-      l += __shfl_xor(l, 16);
-      l += __shfl_xor(l, 32);
-      z += __shfl_xor(z, 16);
-      z += __shfl_xor(z, 32);
+      l = sum_across_rows(l);
+      z = sum_across_rows(z);
       const int64_t pidx = static_cast<int64_t>(before_last - later + c) * a.Hkv + g;
       if (col < a.G) {
         if (grp == 0) {

@@ -401,10 +401,8 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
     // ---- combine the four waves: (m, l, z) per head, O pairwise ----
     float l_run = st.l, z_run = st.z;
     const float m_run = st.m;
-    l_run += __shfl_xor(l_run, 16);
-    l_run += __shfl_xor(l_run, 32);
-    z_run += __shfl_xor(z_run, 16);
-    z_run += __shfl_xor(z_run, 32);
+    l_run = sum_across_rows(l_run);
+    z_run = sum_across_rows(z_run);
     if (grp == 0) {
       s_m[wave][col] = m_run;
       s_l[wave][col] = l_run;

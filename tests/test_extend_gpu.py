@@ -87,6 +87,32 @@ def test_extend_vs_oracle(dev, d, Hq, Hkv, q_max, wpath):
     assert torch.equal(orr, ow)
 
 
+@pytest.mark.parametrize("scale", [-1.0 / 16, 0.0, 0.5])
+def test_full_extend_any_scale(dev, scale):
+    """The multi-row kernel folds the logit scale into its exponent and needs
+    it positive: a negative scale goes into the queries' sign, a zero one is
+    replaced by the smallest normal float.  Negative, zero and large scales
+    against the oracle (the zero scale averages the visible values), with
+    rows ending inside a 64-key step, where keys are masked."""
+    d, Hq, Hkv, q_max = 256, 32, 2, 8
+    lens = [q_max, 77, 3000, 9000 + 13]
+    n_q = [q_max, 5, q_max, 3]
+    B = len(lens)
+    S_max = max(lens) + 2
+    G.say(f"full extend scale={scale} lens={lens} n_q={n_q}")
+    q = I.normal_bf16((B, q_max, Hq, d), 71, dev)
+    k = I.normal_bf16((B, S_max, Hkv, d), 72, dev)
+    v = I.normal_bf16((B, S_max, Hkv, d), 73, dev)
+    lt, nt = G.lens_tensor(lens, dev), G.lens_tensor(n_q, dev)
+    err = G.err_word(dev)
+    lse = torch.empty(B, q_max, Hq, dtype=torch.float32, device=dev)
+    out = W.draft_extend_full(q, k, v, lt, n_q=nt, lse=lse, scale=scale, err=err)
+    torch.cuda.synchronize()
+    o_ref, l_ref, spread = _oracle(q, k, v, lens, n_q, scale, "full")
+    G.assert_attn_close(out, o_ref, lse, l_ref, what=f"full extend scale {scale}", spread=spread)
+    assert err.item() == 0
+
+
 @pytest.mark.parametrize("d,Hq,Hkv", [(128, 12, 2), (256, 32, 2)])
 @pytest.mark.parametrize("q_max", [12, 20])
 def test_full_extend_many_rows(dev, d, Hq, Hkv, q_max):
