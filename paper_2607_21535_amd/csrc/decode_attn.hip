@@ -1034,9 +1034,30 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
     }
     Mx = m;
   } else {
+    // The partials of a slot's first kPre items are loaded before the
+    // largest maximum is known (they do not depend on it), so the two
+    // rounds of loads overlap; items past those (rows with more than
+    // kPre * NS items) are loaded in the loop below.  The loads are
+    // unconditional (a slot past the row's last item re-reads that item and
+    // ignores it): a load under a branch made the compiler wait for it there.
+    constexpr int kPre = NS >= 32 ? 2 : 8;
+    float pmv[kPre], plv[kPre], pzv[kPre];
+    floatx4 pov[kPre];
+    // (The maxima first: the wait for them then leaves the rest in flight.)
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) pmv[i] = a.pm[prow(min(slot + i * NS, n - 1))];
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      const int64_t pr = prow(min(slot + i * NS, n - 1));
+      pov[i] = *reinterpret_cast<const floatx4*>(a.po + pr * D + d0);
+      plv[i] = a.pl[pr];
+      pzv[i] = a.pz[pr];
+    }
     // Largest partial maximum.
     float mx = neg_inf();
-    for (int c = tid; c < n; c += NT) mx = fmaxf(mx, a.pm[prow(c)]);
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) mx = fmaxf(mx, slot + i * NS < n ? pmv[i] : neg_inf());
+    for (int c = slot + kPre * NS; c < n; c += NS) mx = fmaxf(mx, a.pm[prow(c)]);
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
     if (lane == 0) s_red[wave] = mx;
@@ -1045,10 +1066,20 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
 #pragma unroll
     for (int w = 1; w < NT / kWave; ++w) Mx = fmaxf(Mx, s_red[w]);
 
+    // Items in order c = slot, slot + NS, ...
     floatx4 o = {0.f, 0.f, 0.f, 0.f};
     float L = 0.f, Z = 0.f;
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      if (slot + i * NS < n) {
+        const float w = __builtin_amdgcn_exp2f(pmv[i] - Mx);
+        o += w * pov[i];
+        L += w * plv[i];
+        Z += w * pzv[i];
+      }
+    }
 #pragma unroll 8
-    for (int c = slot; c < n; c += NS) {
+    for (int c = slot + kPre * NS; c < n; c += NS) {
       const int64_t pr = prow(c);
       const float w = __builtin_amdgcn_exp2f(a.pm[pr] - Mx);
       const floatx4 v = *reinterpret_cast<const floatx4*>(a.po + pr * D + d0);
