@@ -1057,7 +1057,7 @@ __global__ __launch_bounds__(NT) void merge_kernel(MergeArgs a) {
     float mx = neg_inf();
 #pragma unroll
     for (int i = 0; i < kPre; ++i) mx = fmaxf(mx, slot + i * NS < n ? pmv[i] : neg_inf());
-    for (int c = slot + kPre * NS; c < n; c += NS) mx = fmaxf(mx, a.pm[prow(c)]);
+    for (int c = kPre * NS + tid; c < n; c += NT) mx = fmaxf(mx, a.pm[prow(c)]);  // the other items
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
     if (lane == 0) s_red[wave] = mx;
