@@ -86,7 +86,11 @@ typedef enum {
  * Workspace (device bytes) that one attention call of the given variant and
  * shape needs for its split-K partial results (per work item and query head:
  * the running maximum, two softmax denominators and the unnormalised output
- * row, in fp32) and its work counters, sized for the current device.
+ * row, in fp32) and its work counters, sized for the current device.  Small
+ * calls (at most four query rows x KV heads; windowed, or full context over
+ * at most 16384 cached rows per sequence at d = 256, 4096 below) run as one
+ * launch whose last work item per row merges the others; their workspace
+ * holds those items' records instead.
  * B counts query rows: the batch for the single-row calls, B * q_max for the
  * extend calls.  S_max is the dense cache capacity (ignored for the ring); W
  * and sink are ignored for the full variant.  Returns 0 for arguments the

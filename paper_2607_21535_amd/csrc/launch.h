@@ -85,6 +85,7 @@ SplitPlan plan_split(int variant, int B, int Hq, int Hkv, int d, int64_t n_keys_
 constexpr int kWinSlice = 64;          // value columns per slice when sliced
 constexpr int kWinOneLaunchRows = 4;   // query rows x KV heads up to which the one-launch kernel runs
 constexpr int kWinMaxItemKeys = 1024;  // largest item (a paged item's pool rows live in LDS)
+constexpr int64_t kWinFullMaxKeys = 16384;  // full-context capacity up to which the one-launch kernel runs (d = 256; a quarter below)
 
 struct WinPlan {
   int item_keys;  // selected keys per work item (multiple of kChunkQuantum)
@@ -109,6 +110,7 @@ WinPlan plan_window(int NV, int Hq, int Hkv, int d, int keys);
 // kernel (many rows: the merge is spread over one workgroup per row and
 // head).  Depends only on the shape, like the plans.
 bool use_window_kernel(int NV, int Hkv);
+bool use_window_kernel_full(int NV, int Hkv, int d, int64_t S_max);
 
 hipError_t launch_window(const AttnLaunch& a, hipStream_t stream);
 

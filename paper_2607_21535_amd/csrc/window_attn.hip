@@ -639,8 +639,10 @@ template <int D>
 hipError_t launch_d(const AttnLaunch& L, hipStream_t st) {
   if (L.kv_fp8) {
     switch (L.variant) {
+      case WMTP_VARIANT_FULL: return launch_slices<D, KeyMap::Full, true>(L, st);
       case WMTP_VARIANT_WINDOWED: return launch_slices<D, KeyMap::Window, true>(L, st);
       case WMTP_VARIANT_RING: return launch_slices<D, KeyMap::Ring, true>(L, st);
+      case WMTP_VARIANT_PAGED_FULL: return launch_slices<D, KeyMap::PagedFull, true>(L, st);
       case WMTP_VARIANT_PAGED_WINDOWED: return launch_slices<D, KeyMap::PagedWindow, true>(L, st);
       default: return hipErrorInvalidValue;  // no fp8 tree or fused-step kernels
     }
@@ -653,8 +655,10 @@ hipError_t launch_d(const AttnLaunch& L, hipStream_t st) {
     }
   }
   switch (L.variant) {
+    case WMTP_VARIANT_FULL: return launch_slices<D, KeyMap::Full, false>(L, st);
     case WMTP_VARIANT_WINDOWED: return launch_slices<D, KeyMap::Window, false>(L, st);
     case WMTP_VARIANT_RING: return launch_slices<D, KeyMap::Ring, false>(L, st);
+    case WMTP_VARIANT_PAGED_FULL: return launch_slices<D, KeyMap::PagedFull, false>(L, st);
     case WMTP_VARIANT_PAGED_WINDOWED: return launch_slices<D, KeyMap::PagedWindow, false>(L, st);
     case WMTP_VARIANT_TREE: return launch_slices<D, KeyMap::Tree, false>(L, st);
     default: return hipErrorInvalidValue;
@@ -736,6 +740,24 @@ WinPlan plan_window(int NV, int Hq, int Hkv, int d, int keys) {
   p.off_pl = p.off_pz = p.off_po = p.off_pm;  // (one array of records)
   p.bytes = p.off_pm + records * rec_bytes;
   return p;
+}
+
+bool use_window_kernel_full(int NV, int Hkv, int d, int64_t S_max) {
+  // Short full contexts are launch-bound like windowed calls and take the
+  // one-launch kernel under the same row limit, up to a capacity measured on
+  // MI355X (graph-replayed calls, one sequence, Hkv = 2; split + merge / one
+  // launch): d = 256, Hq = 32: 1K 11.1 / 8.1 us, 4K 12.5 / 10.3, 8K 14.4 /
+  // 13.1, 16K 16.9 / 16.3, 32K 21.3 / 40.2; d = 128, Hq = 16: 1K 8.9 / 6.7,
+  // 4K 9.6 / 8.7, 8K 10.3 / 10.6 (the best item size), 16K 11.1 / 15.1.
+  // WMTP_WIN_FULL_MAX_KEYS overrides the capacity limit (0: never), read at
+  // every call.
+  int64_t max_keys = d >= 256 ? kWinFullMaxKeys : kWinFullMaxKeys / 4;
+  if (const char* e = std::getenv("WMTP_WIN_FULL_MAX_KEYS"); e != nullptr && *e != '\0') {
+    char* end = nullptr;
+    const long long x = std::strtoll(e, &end, 10);
+    if (end != e && x >= 0) max_keys = x;
+  }
+  return S_max > 0 && S_max <= max_keys && use_window_kernel(NV, Hkv);
 }
 
 bool use_window_kernel(int NV, int Hkv) {

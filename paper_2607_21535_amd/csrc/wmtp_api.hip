@@ -54,6 +54,22 @@ bool paged_variant(int variant) {
   return variant == WMTP_VARIANT_PAGED_FULL || variant == WMTP_VARIANT_PAGED_WINDOWED;
 }
 
+// Whether a call takes the one-launch kernel (split, ticket and merge in
+// one launch): windowed calls of at most kWinOneLaunchRows query rows x KV
+// heads, and full-context calls of that size over a short cache (up to
+// kWinFullMaxKeys rows per sequence at d = 256, a quarter of that below:
+// launch-bound like the windowed ones).  The keys it plans for: the window,
+// or the capacity.
+bool one_launch(int variant, int rows_q, int Hkv, int d, int64_t S_max) {
+  if (windowed_variant(variant)) return wmtp::use_window_kernel(rows_q, Hkv);
+  if (variant == WMTP_VARIANT_FULL || variant == WMTP_VARIANT_PAGED_FULL)
+    return wmtp::use_window_kernel_full(rows_q, Hkv, d, S_max);
+  return false;
+}
+int one_launch_keys(int variant, int64_t S_max, int W, int sink) {
+  return windowed_variant(variant) ? W + sink : static_cast<int>(S_max);
+}
+
 // A per-tensor scale of an fp8 cache: finite and positive.
 bool valid_scale(float s) { return std::isfinite(s) && s > 0.0f; }
 
@@ -127,13 +143,13 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
     return WMTP_EINVAL;
 
   const int rows_q = B * q_max;
-  const bool win = windowed_variant(variant) && wmtp::use_window_kernel(rows_q, Hkv);
+  const bool win = one_launch(variant, rows_q, Hkv, d, S_max);
   SplitPlan plan{};
   wmtp::WinPlan wp{};
   size_t need = 0;
   bool per_seq = false;
   if (win) {
-    wp = wmtp::plan_window(rows_q, Hq, Hkv, d, W + sink);
+    wp = wmtp::plan_window(rows_q, Hq, Hkv, d, one_launch_keys(variant, S_max, W, sink));
     if (!win_plan_fits(wp, rows_q, Hkv)) return WMTP_EUNSUPPORTED;
     need = wp.bytes;
   } else {
@@ -267,8 +283,8 @@ WMTP_EXPORT size_t wmtp_workspace_bytes(int B, int Hq, int Hkv, int d, int64_t S
   if (check_heads(B, Hq, Hkv, d) != WMTP_OK || B == 0) return 0;
   if (windowed_variant(variant) && check_window(W, sink) != WMTP_OK) return 0;
   if (!windowed_variant(variant) && S_max < 0) return 0;
-  if (windowed_variant(variant) && wmtp::use_window_kernel(B, Hkv)) {
-    const wmtp::WinPlan wp = wmtp::plan_window(B, Hq, Hkv, d, W + sink);
+  if (one_launch(variant, B, Hkv, d, S_max)) {
+    const wmtp::WinPlan wp = wmtp::plan_window(B, Hq, Hkv, d, one_launch_keys(variant, S_max, W, sink));
     if (!win_plan_fits(wp, B, Hkv)) return 0;
     return wp.bytes;
   }
