@@ -157,6 +157,30 @@ def test_full_specific_checks(lib):
 
 
 @fake_pointers
+@pytest.mark.parametrize("d,Hq,cap", [(256, 32, 16384), (128, 16, 4096), (64, 8, 4096)])
+def test_full_one_launch_workspace(lib, monkeypatch, d, Hq, cap):
+    """Full-context calls of at most four query rows x KV heads over a cache
+    of at most `cap` rows take the one-launch kernel: their workspace holds
+    its records (sized otherwise than the split partials), a byte less is
+    refused, and one row more of capacity (or the override
+    WMTP_WIN_FULL_MAX_KEYS=0) gives the split layout."""
+    monkeypatch.delenv("WMTP_WIN_FULL_MAX_KEYS", raising=False)
+    monkeypatch.delenv("WMTP_WIN_ONE_LAUNCH_ROWS", raising=False)
+    one = W.workspace_bytes(1, Hq, 2, d, cap, variant=W.VARIANT_FULL)
+    assert _full(lib, Hq=Hq, d=d, S_max=cap, ws_bytes=one - 1) == W.EWORKSPACE
+    monkeypatch.setenv("WMTP_WIN_FULL_MAX_KEYS", "0")
+    split = W.workspace_bytes(1, Hq, 2, d, cap, variant=W.VARIANT_FULL)
+    assert split > 0 and split != one
+    monkeypatch.delenv("WMTP_WIN_FULL_MAX_KEYS")
+    assert W.workspace_bytes(1, Hq, 2, d, cap + 1, variant=W.VARIANT_FULL) != one
+    # three sequences (six rows x KV heads) keep split + merge at any capacity
+    monkeypatch.setenv("WMTP_WIN_FULL_MAX_KEYS", "0")
+    split3 = W.workspace_bytes(3, Hq, 2, d, cap, variant=W.VARIANT_FULL)
+    monkeypatch.delenv("WMTP_WIN_FULL_MAX_KEYS")
+    assert W.workspace_bytes(3, Hq, 2, d, cap, variant=W.VARIANT_FULL) == split3
+
+
+@fake_pointers
 @pytest.mark.parametrize("call", [_win, _ring])
 def test_window_argument_checks(lib, call):
     assert call(lib, W=0) == W.EINVAL
