@@ -839,12 +839,15 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
 
     OnlineHeads<D, false> st;
     st.init();
+    // A thread issues the next step's loads as soon as it has stored the
+    // current ones (before the barrier), so they have the wait at the
+    // barrier as well as a step of compute to arrive in.
     load(0);
     stash(0);
+    if (n_steps > 1) load(1);
     __syncthreads();
     for (int s = 0; s < n_steps; ++s) {
       const int buf = s & 1;
-      if (s + 1 < n_steps) load(s + 1);
       if (active) {
         const u32x4* sk = s_k[buf];
         const u32x4* svt = s_vt[buf];
@@ -886,7 +889,10 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
           }
         }
       }
-      if (s + 1 < n_steps) stash(buf ^ 1);
+      if (s + 1 < n_steps) {
+        stash(buf ^ 1);
+        if (s + 2 < n_steps) load(s + 2);
+      }
       __syncthreads();
     }
 
