@@ -217,19 +217,16 @@ struct OnlineHeads {
   }
 
   // weigh with fewer vector instructions, for the multi-row kernel (whose
-  // time is set by its compute waves).  Requires sl2 > 0 (the kernel puts
-  // the sign of the scale into its queries, exactly, and stands in the
-  // smallest normal float for a zero scale: every weight is then exp2 of a
-  // number within |s| 2^-126 of 0, i.e. 1 to fp32 precision, as for the
-  // scale 0, and masked keys stay at exp2(-inf) = 0 where -inf * 0 would be
-  // NaN): the maximum is then
-  // taken over the raw logits (rounding is monotone, so it scales to the
-  // maximum of the scaled ones) and the scale is folded into the exponent,
-  // exp2(fma(s, sl2, -m)); the maxima across the four lanes of a head use
-  // gfx950's permlane swaps (one VALU op each instead of an LDS permute and
-  // its wait); the sum of the rounded weights is a bf16 dot product with
-  // (1, 1) per weight pair.  The weights and sums may differ from weigh's in
-  // the last bit.
+  // time is set by its compute waves): the maximum is taken over the raw
+  // logits (rounding is monotone, so it scales to the maximum of the scaled
+  // ones), the scale is folded into the exponent, exp2(fma(s, sl2, -m)), and
+  // the sum of the rounded weights is a bf16 dot product with (1, 1) per
+  // weight pair.  Requires sl2 > 0: the kernel puts the sign of the scale
+  // into its queries (exact) and stands in the smallest normal float for a
+  // zero scale (every weight is then exp2 of a number within |s| 2^-126 of 0,
+  // i.e. 1 to fp32 precision, as for the scale 0, and a masked key keeps
+  // exp2(-inf) = 0 where -inf * 0 would be NaN).  The weights and sums may
+  // differ from weigh's in the last bit.
   template <int NT>
   __device__ __forceinline__ void weigh_lean(const floatx4 (&s)[NT], int jt, int j_end, float sl2, int grp,
                                              bf16x4 (&pop)[NT]) {

@@ -675,6 +675,7 @@ __global__ __launch_bounds__(kRowThreads) void rows_split_kernel(SplitArgs a) {
   constexpr int kPitch = kUnits + 2;
   constexpr int kLUnits = F8 ? D / 16 : kUnits;  // 16-byte units per row as loaded (codes or bf16)
   constexpr int kLoads = kRowStep * kLUnits / kRowThreads;  // K (and V) units per thread and step
+  static_assert(kRowStep == 64, "rows_kernel_fits assumes 64-key steps");
   static_assert(kLoads == 1 || kLoads == 2 || kLoads == 4, "a thread's keys must sit in one 4-key run");
   static_assert(kRowStep * kUnits % kRowThreads == 0, "step must tile the workgroup");
   // V is staged transposed, in the order of the PV product's operand: one
@@ -1141,7 +1142,7 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
     a.k2 = L.k2; a.v2 = L.v2; a.rows2 = L.rows2; a.dd = L.dd;
     a.per_seq = L.per_seq ? 1 : 0;
     if constexpr (M == KeyMap::Full && (!F8 || D >= 128)) {
-      if (L.qps > 1) {
+      if (L.qps > 1 && rows_kernel_fits(L.Hkv, L.d, F8)) {
         // Items of the multi-row kernel: sequence b owns ceil(n(b) / chunk)
         // of them, n(b) its last row's length; with the chunk of the per-row
         // decomposition (total over rows / T, clamped to [quantum, cap]) that

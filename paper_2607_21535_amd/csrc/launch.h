@@ -110,6 +110,13 @@ WinPlan plan_window(int NV, int Hq, int Hkv, int d, int keys);
 // kernel (many rows: the merge is spread over one workgroup per row and
 // head).  Depends only on the shape, like the plans.
 bool use_window_kernel(int NV, int Hkv);
+
+// The multi-row extend kernel addresses a 64-key step with 32-bit byte
+// offsets from the step's first token row (all KV heads): 64 rows must span
+// less than 4 GiB.  Larger shapes take the per-row split kernel.
+inline bool rows_kernel_fits(int Hkv, int d, bool fp8) {
+  return 64LL * Hkv * d * (fp8 ? 1 : 2) < (1LL << 32);
+}
 bool use_window_kernel_full(int NV, int Hkv, int d, int64_t S_max);
 
 hipError_t launch_window(const AttnLaunch& a, hipStream_t stream);

@@ -159,7 +159,7 @@ int attention_common(int variant, const void* q, const void* k, const void* v,
     // A full-context extend whose workspace also holds the finer per-sequence
     // decomposition (wmtp_extend_workspace_bytes) spreads each sequence's
     // keys over about one workgroup per CU however many rows it has.
-    if (variant == WMTP_VARIANT_FULL && q_max > 1 && check_ws) {
+    if (variant == WMTP_VARIANT_FULL && q_max > 1 && check_ws && wmtp::rows_kernel_fits(Hkv, d, fp8)) {
       const SplitPlan fine = wmtp::plan_split(variant, rows_q, Hq, Hkv, d, keys_max(variant, S_max, W, sink), q_max);
       if (plan_fits(fine, Hkv) && ws_bytes >= fine.bytes) {
         plan = fine;

@@ -198,3 +198,37 @@ def test_extend_s1m_draft_depth8(dev):
         o1, l1 = A.attend_sequence(qb[0, t], G.HostRows(k[0]), G.HostRows(v[0]), L, wl.scale, None)
         e = G.assert_attn_close(of[0, t], o1, lse_f[0, t], l1, f"extend 1M full row {t}")
         G.say(f"extend 1M full row {t} err {e}")
+
+
+def test_full_extend_many_kv_heads_takes_the_per_row_kernel(dev):
+    """With 64 token rows of all KV heads spanning 4 GiB or more (here
+    Hkv = 131072 at d = 256, G = 1) the multi-row kernel's 32-bit offsets
+    would not reach; the call takes the per-row split kernel instead.  Its
+    rows against a float32 reference computed here (elementwise products, no
+    batched matmul) over the causal keys of each row, to the parity bar's
+    elementwise bound (tests/_gpu.py; with two or three keys per row the
+    outputs reach |o| ~ 5, where rounding to bf16 alone moves them by up to
+    2^-8 |o|)."""
+    Hkv = Hq = 131072
+    d, q_max, S_max = 256, 2, 4
+    lens, n_q = [3], [2]
+    q = I.normal_bf16((1, q_max, Hq, d), 81, dev)
+    k = I.normal_bf16((1, S_max, Hkv, d), 82, dev)
+    v = I.normal_bf16((1, S_max, Hkv, d), 83, dev)
+    lt, nt = G.lens_tensor(lens, dev), G.lens_tensor(n_q, dev)
+    err = G.err_word(dev)
+    out = W.draft_extend_full(q, k, v, lt, n_q=nt, err=err)
+    torch.cuda.synchronize()
+    assert err.item() == 0
+    scale = 1.0 / np.sqrt(d)
+    for t in range(q_max):
+        L = lens[0] - n_q[0] + t + 1
+        qt = q[0, t].float()                                     # [H, d]
+        kt, vt = k[0, :L].float(), v[0, :L].float()              # [L, H, d]
+        s = (qt[None] * kt).sum(-1) * scale                      # [L, H]
+        p = torch.softmax(s, dim=0)
+        ref = (p[..., None] * vt).sum(0)                         # [H, d]
+        spread = (p[..., None] * (vt - ref[None]).abs()).sum(0)  # sum_p w_p |v_p - o|
+        bound = G.elementwise_bound(ref.double().cpu().numpy(), spread.double().cpu().numpy())
+        err_t = (out[0, t].float() - ref).abs().double().cpu().numpy()
+        assert (err_t <= bound).all(), (t, float(err_t.max()), float((err_t - bound).max()))
