@@ -1163,11 +1163,16 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
     }
   }
   // The merge shape: 1024-thread workgroups on 64-wide slices when a row has
-  // many items and their grid fits one workgroup per CU; else one 256-thread
-  // workgroup per row and head (a tree of 4 speculation candidates at
-  // Hq = 32, 512 wide workgroups: 22.4 -> 20.8 us per draft step).
+  // many items and their grid fits one workgroup per CU; for such rows
+  // whose wide grid does not fit, 512-thread workgroups on 128-wide slices
+  // (sixteen item slots: a row's first 128 items in one round of loads)
+  // while two of them per CU hold the grid; else one 256-thread workgroup
+  // per row and head (a tree of 4 speculation candidates at Hq = 32, 512
+  // wide workgroups: 22.4 -> 20.8 us per draft step).
   const int64_t NV = static_cast<int64_t>(L.B) * L.qps;
-  const bool wide = L.max_items >= 32 * NV && NV * L.Hq * (D / 64) <= static_cast<int64_t>(device_cus());
+  const bool many = L.max_items >= 32 * NV;
+  const bool wide = many && NV * L.Hq * (D / 64) <= static_cast<int64_t>(device_cus());
+  const bool mid = many && !wide && D >= 128 && NV * L.Hq * (D / 128) <= 2 * static_cast<int64_t>(device_cus());
   MergeArgs m;
   m.lens = L.lens; m.n_q = L.n_q; m.qps = L.qps; m.pm = L.pm; m.pl = L.pl; m.pz = L.pz; m.po = L.po;
   m.out = L.out; m.lse = L.lse; m.err = L.err;
@@ -1179,11 +1184,15 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   m.lens_out = L.lens_out;
   m.per_seq = L.per_seq ? 1 : 0;
   const unsigned bh = static_cast<unsigned>(NV) * static_cast<unsigned>(L.Hq);
-  if (wide)
+  if (wide) {
     hipLaunchKernelGGL((merge_kernel<D, M, kMergeThreads, 64>), dim3(bh, D / 64), dim3(kMergeThreads), 0,
                        st, m);
-  else
+  } else if (mid) {
+    if constexpr (D >= 128)
+      hipLaunchKernelGGL((merge_kernel<D, M, 512, 128>), dim3(bh, D / 128), dim3(512), 0, st, m);
+  } else {
     hipLaunchKernelGGL((merge_kernel<D, M, 256, D>), dim3(bh, 1), dim3(256), 0, st, m);
+  }
   return hipGetLastError();
 }
 
