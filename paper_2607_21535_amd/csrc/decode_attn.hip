@@ -1163,16 +1163,18 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
     }
   }
   // The merge shape: 1024-thread workgroups on 64-wide slices when a row has
-  // many items and their grid fits one workgroup per CU; for such rows
-  // whose wide grid does not fit, 512-thread workgroups on 128-wide slices
-  // (sixteen item slots: a row's first 128 items in one round of loads)
-  // while two of them per CU hold the grid; else one 256-thread workgroup
+  // many items and their grid fits one workgroup per CU; for full-context
+  // rows (O(S) items each) whose wide grid does not fit, 512-thread
+  // workgroups on 128-wide slices (sixteen item slots: a row's first 128
+  // items in one round of loads) while two of them per CU hold the grid (a
+  // tree of 4 candidates took 4.6 -> 5.1 us on it); else one 256-thread workgroup
   // per row and head (a tree of 4 speculation candidates at Hq = 32, 512
   // wide workgroups: 22.4 -> 20.8 us per draft step).
   const int64_t NV = static_cast<int64_t>(L.B) * L.qps;
   const bool many = L.max_items >= 32 * NV;
   const bool wide = many && NV * L.Hq * (D / 64) <= static_cast<int64_t>(device_cus());
-  const bool mid = many && !wide && D >= 128 && NV * L.Hq * (D / 128) <= 2 * static_cast<int64_t>(device_cus());
+  const bool mid = many && !wide && !is_windowed(M) && D >= 128 &&
+                   NV * L.Hq * (D / 128) <= 2 * static_cast<int64_t>(device_cus());
   MergeArgs m;
   m.lens = L.lens; m.n_q = L.n_q; m.qps = L.qps; m.pm = L.pm; m.pl = L.pl; m.pz = L.pz; m.po = L.po;
   m.out = L.out; m.lse = L.lse; m.err = L.err;
