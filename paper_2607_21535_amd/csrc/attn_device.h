@@ -12,14 +12,19 @@
 
 namespace wmtp {
 
-__device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap, int32_t* err,
-                                        bool report) {
-  int S = lens[b];
+// A length read from a device array, clamped to [0, cap] (flagged when out
+// of range).
+__device__ __forceinline__ int check_len(int S, int64_t cap, int32_t* err, bool report) {
   if (S < 0 || static_cast<int64_t>(S) > cap) {
     if (report) raise_error(err, WMTP_DERR_LEN_RANGE);
     S = S < 0 ? 0 : static_cast<int>(cap);
   }
   return S;
+}
+
+__device__ __forceinline__ int read_len(const int32_t* lens, int b, int64_t cap, int32_t* err,
+                                        bool report) {
+  return check_len(lens[b], cap, err, report);
 }
 
 // Tail maps.  Tree (speculation candidates): query row v = b * qps + t is
@@ -34,12 +39,15 @@ __device__ __forceinline__ int tail_len(const int32_t* lens, const int32_t* extr
                                         int b, int32_t* err, bool report, int& s_commit) {
   constexpr bool kDense = is_step(M) && !is_ring(M);
   const int64_t lim = kDense ? (cap < INT_MAX - dd ? cap : INT_MAX - dd) : INT_MAX - dd;
+  // Both values are read before either is checked: a read placed after an
+  // error report would wait for the first one (the report may write memory
+  // the second read could alias).
   int S = lens[b];
+  int i = extra[b];
   if (S < 0 || S > lim) {
     if (report) raise_error(err, WMTP_DERR_LEN_RANGE);
     S = S < 0 ? 0 : static_cast<int>(lim);
   }
-  int i = extra[b];
   if (i < 0 || i > dd) {
     if (report) raise_error(err, WMTP_DERR_NNEW_RANGE);
     i = i < 0 ? 0 : dd;
@@ -72,10 +80,11 @@ __device__ __forceinline__ int visible_len(const int32_t* lens, const int32_t* n
   const int b = qps == 1 ? v : v / qps;
   const int t = v - b * qps;
   b_out = b;
-  const int S = read_len(lens, b, cap, err, report);
-  int n = qps;
+  // Both values are read before either is checked (as in tail_len).
+  const int S_read = lens[b];
+  int n = n_q != nullptr ? n_q[b] : qps;
+  const int S = check_len(S_read, cap, err, report);
   if (n_q != nullptr) {
-    n = n_q[b];
     if (n < 0 || n > qps) {
       if (report) raise_error(err, WMTP_DERR_NNEW_RANGE);
       n = n < 0 ? 0 : qps;
