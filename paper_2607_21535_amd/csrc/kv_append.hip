@@ -42,12 +42,14 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
   const int64_t cap = RING ? static_cast<int64_t>(INT_MAX) : a.rows;
   const bool report = threadIdx.x == 0;
 
+  // Both counts are read before either is checked: a read placed after an
+  // error report would wait for the first one.
   int L0 = a.lens[b];
+  int n = a.n_new[b];
   if (L0 < 0 || L0 > cap) {
     if (report) raise_error(a.err, WMTP_DERR_LEN_RANGE);
     L0 = L0 < 0 ? 0 : static_cast<int>(cap);
   }
-  int n = a.n_new[b];
   if (n < 0 || n > a.n_max) {
     if (report) raise_error(a.err, WMTP_DERR_NNEW_RANGE);
     n = n < 0 ? 0 : a.n_max;
