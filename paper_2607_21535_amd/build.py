@@ -40,6 +40,16 @@ COMMON_FLAGS = [
 ]
 
 
+# Per-source flags.  The one-launch windowed kernel takes the values its
+# first loads depend on (length arrays, queries, item and head counts) as
+# its ten leading scalar arguments; gfx950 preloads them into scalar
+# registers at wave launch instead of each wave fetching them from the
+# kernel-argument segment first.
+SOURCE_FLAGS = {
+    "window_attn.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=10"],
+}
+
+
 def hipcc() -> str:
     cand = os.environ.get("HIPCC") or shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     return cand
@@ -69,7 +79,7 @@ def build(verbose: bool = False, extra_flags=None) -> str:
     for src in SOURCES:
         obj = os.path.join(BUILD_DIR, src.replace(".hip", ".o"))
         objs.append(obj)
-        cmds.append([cc, *flags, "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([cc, *flags, *SOURCE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj])
     with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 1)) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))
     tmp = LIB_PATH + ".tmp"

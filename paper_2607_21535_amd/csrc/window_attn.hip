@@ -108,7 +108,8 @@ __device__ __forceinline__ void coherent_store16(__amdgpu_buffer_rsrc_t r, int b
 constexpr int win_waves(int) { return 4; }
 
 template <int D, int DS, KeyMap M, bool F8>
-__global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a) {
+__global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(const int32_t* lens, const int32_t* n_q, const uint16_t* q, int NI, int n_items,
+                                                                   int Hkv, int qps, int G, int Hq, int dd, WinArgs a) {
   constexpr int NW = win_waves(DS);
   constexpr int NT = NW * kWave;
   using KT = std::conditional_t<F8, uint8_t, uint16_t>;  // one cached K/V element
@@ -133,20 +134,19 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
   const int id = blockIdx.x;
   const int s = (id >> 3) % NSL;
   const int it = ((id >> 3) / NSL) * 8 + (id & 7);
-  if (it >= a.NI) return;  // padding of the last group of eight: no item, no ticket
-  const int c = it % a.n_items;
-  const int vg = it / a.n_items;  // query row x KV heads + KV head
-  const int g = vg % a.Hkv;
-  const int v = vg / a.Hkv;
-  const int b = a.qps == 1 ? v : v / a.qps;
-  const int G = a.G;
+  if (it >= NI) return;  // padding of the last group of eight: no item, no ticket
+  const int c = it % n_items;
+  const int vg = it / n_items;  // query row x KV heads + KV head
+  const int g = vg % Hkv;
+  const int v = vg / Hkv;
+  const int b = qps == 1 ? v : v / qps;
 
   // Q^T operand (as in the split-K kernel): lane (grp, col) holds at step kk
   // the 8 d values of head col that the key operand holds.
   bf16x8 qf[KCH];
   {
     const bool live = col < G;
-    const uint16_t* qp = a.q + (static_cast<int64_t>(v) * a.Hq + g * G + (live ? col : 0)) * D;
+    const uint16_t* qp = q + (static_cast<int64_t>(v) * Hq + g * G + (live ? col : 0)) * D;
 #pragma unroll
     for (int kk = 0; kk < KCH; ++kk) {
       const int d0 = F8 ? ((kk >> 1) * 4 + grp) * 16 + (kk & 1) * 8 : kk * 32 + grp * 8;
@@ -161,10 +161,10 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
   // the first one's error report).
   int S, S_c_len = 0;
   if constexpr (has_tail(M)) {
-    S = tail_len<M>(a.lens, a.n_q, a.dd, a.len_cap, b, a.err, report && v == b * a.qps, S_c_len);
+    S = tail_len<M>(lens, n_q, dd, a.len_cap, b, a.err, report && v == b * qps, S_c_len);
   } else {
     int b_unused;
-    S = visible_len<M>(a.lens, a.n_q, a.qps, a.len_cap, a.err, v, report, b_unused, a.dd);
+    S = visible_len<M>(lens, n_q, qps, a.len_cap, a.err, v, report, b_unused, dd);
   }
   S = __builtin_amdgcn_readfirstlane(S);
   const int n_sel = selected_count<M>(S, a.W, a.sink);
@@ -184,19 +184,19 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
     S_c = __builtin_amdgcn_readfirstlane(S_c_len);
     bool tail = true;
     if constexpr (M == KeyMap::Tree) {
-      const int cand = v - b * a.qps;
+      const int cand = v - b * qps;
       tail = cand != 0;  // candidate 0 lives in the ring, as a chain writes it
-      tbase = (cand - 1) * a.dd;
+      tbase = (cand - 1) * dd;
     }
     // The first virtual index whose position is >= S_c (positions grow with j).
     if (tail) j_c = S_c < a.sink ? S_c : max(a.sink, S_c - map.shift);
   }
-  const int64_t rs = static_cast<int64_t>(a.Hkv) * D;  // elements between rows
+  const int64_t rs = static_cast<int64_t>(Hkv) * D;  // elements between rows
   const int64_t seq_rows = is_paged(M) ? 0 : static_cast<int64_t>(b) * a.rows;
-  const int64_t seq_off = (seq_rows * a.Hkv + g) * D;
+  const int64_t seq_off = (seq_rows * Hkv + g) * D;
   const KT* kbase = static_cast<const KT*>(a.k) + seq_off;
   const KT* vbase = static_cast<const KT*>(a.v) + seq_off;
-  [[maybe_unused]] const int64_t off2 = (static_cast<int64_t>(b) * a.rows2 * a.Hkv + g) * D;
+  [[maybe_unused]] const int64_t off2 = (static_cast<int64_t>(b) * a.rows2 * Hkv + g) * D;
   [[maybe_unused]] const KT* kbase2 = has_tail(M) ? static_cast<const KT*>(a.k2) + off2 : nullptr;
   [[maybe_unused]] const KT* vbase2 = has_tail(M) ? static_cast<const KT*>(a.v2) + off2 : nullptr;
   // Second-buffer row of virtual index j >= j_c.
@@ -464,7 +464,7 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
           }
     }
     __syncthreads();
-    const __amdgpu_buffer_rsrc_t rr = record_rsrc(a.rec + ((static_cast<int64_t>(vg) * NSL + s) * a.n_items + c) * kRec);
+    const __amdgpu_buffer_rsrc_t rr = record_rsrc(a.rec + ((static_cast<int64_t>(vg) * NSL + s) * n_items + c) * kRec);
     for (int i = tid; i < kRec / 4; i += NT)
       coherent_store16(rr, i * 16, reinterpret_cast<const u32x4*>(s_rec)[i]);
     __builtin_amdgcn_s_waitcnt(0);  // the stores are complete at the point of coherence
@@ -499,7 +499,7 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
   __syncthreads();
   if (tid == 0) {
     const int old = __hip_atomic_fetch_add(ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int last = old == a.n_items - 1;
+    const int last = old == n_items - 1;
     if (last) __hip_atomic_store(ticket, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     s_last = last;
   }
@@ -521,7 +521,7 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
   constexpr int CPT = (kMaxGroup * Q4 + NT - 1) / NT;  // columns per thread
   constexpr int NB = 32 / CPT;                                       // items per batch
   const int n_c = ceil_div_i(n_sel, a.item_keys);
-  float* gbase = a.rec + (static_cast<int64_t>(vg) * NSL + s) * a.n_items * kRec;
+  float* gbase = a.rec + (static_cast<int64_t>(vg) * NSL + s) * n_items * kRec;
   const __amdgpu_buffer_rsrc_t rg = record_rsrc(gbase);
   float Mrun[CPT], L[CPT], Z[CPT];
   floatx4 O[CPT];
@@ -593,10 +593,10 @@ __global__ __launch_bounds__(win_waves(DS) * kWave) void window_kernel(WinArgs a
 #pragma unroll
     for (int i = 0; i < 4; ++i) r[i] = n_c > 0 ? O[x][i] / L[x] * a.out_scale : 0.f;
     const int h = g * G + hl;
-    *reinterpret_cast<u32x2*>(a.out + (static_cast<int64_t>(v) * a.Hq + h) * D + s * DS + 4 * q4) =
+    *reinterpret_cast<u32x2*>(a.out + (static_cast<int64_t>(v) * Hq + h) * D + s * DS + 4 * q4) =
         u32x2{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])};
     if (a.lse != nullptr && s == 0 && q4 == 0)
-      a.lse[static_cast<int64_t>(v) * a.Hq + h] = n_c > 0 ? (Mrun[x] + log2f(Z[x])) * kLn2 : neg_inf();
+      a.lse[static_cast<int64_t>(v) * Hq + h] = n_c > 0 ? (Mrun[x] + log2f(Z[x])) * kLn2 : neg_inf();
   }
   store_copy();
   if constexpr (is_step(M)) {
@@ -623,7 +623,8 @@ hipError_t launch_typed(const AttnLaunch& L, hipStream_t st) {
   a.rec = L.pm; a.tickets = L.tickets;
   const int64_t groups = (NI + 7) / 8;
   const dim3 grid(static_cast<unsigned>(groups * (D / DS) * 8));
-  hipLaunchKernelGGL((window_kernel<D, DS, M, F8>), grid, dim3(win_waves(DS) * kWave), 0, st, a);
+  hipLaunchKernelGGL((window_kernel<D, DS, M, F8>), grid, dim3(win_waves(DS) * kWave), 0, st, a.lens, a.n_q, a.q,
+                     a.NI, a.n_items, a.Hkv, a.qps, a.G, a.Hq, a.dd, a);
   return hipGetLastError();
 }
 
