@@ -8,7 +8,10 @@ windows and sinks of any size.
   bit, and the oracle's paged attention within the elementwise bound of
   tests/_gpu.py;
 * fp8 full, windowed and ring attention against the oracle over the
-  dequantized rows, ring == windowed bit for bit.
+  dequantized rows, ring == windowed bit for bit;
+* fp8 draft-extends (ragged new-row counts, empty sequences): full and
+  windowed against the oracle, the ring extend (ring of W + q_max - 1 rows)
+  == the windowed extend bit for bit.
 
 Both windowed paths (one launch, split + merge) run every case.
 """
@@ -17,6 +20,7 @@ import numpy as np
 import pytest
 import torch
 
+from oracle import attention as A
 from oracle import fp8 as F
 from oracle import paged as Pg
 from oracle import ring as R
@@ -175,3 +179,54 @@ def test_random_fp8_cache_vs_oracle(dev, seed, wpath):
     assert torch.equal(outs["ring"][0], outs["windowed"][0]), f"random fp8 {seed}: ring != windowed"
     assert torch.equal(outs["ring"][1], outs["windowed"][1]), f"random fp8 {seed}: ring lse != windowed"
     assert err.item() == 0, f"random fp8 {seed}: device error word {err.item():#x}"
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_random_fp8_extend_vs_oracle(dev, seed, wpath):
+    d, Hkv, Gq, B, W_, sink, lens = _case(300 + seed)
+    rng = np.random.default_rng(9000 + seed)
+    q_max = int(rng.integers(1, 9))
+    n_q = [min(int(rng.integers(1, q_max + 1)), S) for S in lens]
+    Hq = Hkv * Gq
+    S_max = max(lens) + 3
+    scale = 1.0 / np.sqrt(d)
+    ks, vs = 0.875, 1.125
+    G.say(f"random fp8 extend {seed}: d={d} Hq={Hq} Hkv={Hkv} W={W_} sink={sink} lens={lens} n_q={n_q} "
+          f"path={wpath}")
+    q = I.normal_bf16((B, q_max, Hq, d), 500 + seed, dev)
+    k8 = I.normal_fp8((B, S_max, Hkv, d), 501 + seed, dev)
+    v8 = I.normal_fp8((B, S_max, Hkv, d), 502 + seed, dev)
+    lt, nt = G.lens_tensor(lens, dev), G.lens_tensor(n_q, dev)
+    err = G.err_word(dev)
+    qb = I.bf16_bits(q)
+    rows = [(F.DequantizedRows(_HostCodes(k8[b]), ks), F.DequantizedRows(_HostCodes(v8[b]), vs)) for b in range(B)]
+    outs = {}
+    for variant in ("full", "windowed"):
+        lse = torch.empty(B, q_max, Hq, dtype=torch.float32, device=dev)
+        if variant == "full":
+            out = W.draft_extend_full_fp8(q, k8, v8, lt, ks, vs, n_q=nt, lse=lse, err=err)
+        else:
+            out = W.draft_extend_windowed_fp8(q, k8, v8, lt, W_, sink, ks, vs, n_q=nt, lse=lse, err=err)
+        torch.cuda.synchronize()
+        outs[variant] = (out, lse)
+        o_ref, l_ref, spread = [], [], []
+        for b in range(B):
+            if n_q[b] == 0:  # an empty sequence: every row is padding
+                o_ref.append(np.zeros((q_max, Hq, d)))
+                l_ref.append(np.full((q_max, Hq), -np.inf))
+                spread.append(np.zeros((q_max, Hq, d)))
+                continue
+            o, l = A.attend_extend(qb[b], *rows[b], lens[b], n_q[b], scale, variant, W_, sink)
+            o_ref.append(o)
+            l_ref.append(l)
+            spread.append(A.extend_spread(qb[b], *rows[b], lens[b], n_q[b], scale, variant, W_, sink))
+        G.assert_attn_close(out, np.stack(o_ref), lse, np.stack(l_ref), what=f"random fp8 extend {seed} {variant}",
+                            spread=np.stack(spread))
+    R_w = W_ + q_max - 1
+    kr, vr = _ring_from_dense(k8, lens, sink, R_w), _ring_from_dense(v8, lens, sink, R_w)
+    lse_r = torch.empty(B, q_max, Hq, dtype=torch.float32, device=dev)
+    orr = W.ring_extend_fp8(q, kr, vr, lt, W_, sink, R_w, ks, vs, n_q=nt, lse=lse_r, err=err)
+    torch.cuda.synchronize()
+    assert torch.equal(orr, outs["windowed"][0]), f"random fp8 extend {seed}: ring != windowed"
+    assert torch.equal(lse_r, outs["windowed"][1]), f"random fp8 extend {seed}: ring lse != windowed"
+    assert err.item() == 0, f"random fp8 extend {seed}: device error word {err.item():#x}"
