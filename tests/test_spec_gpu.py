@@ -9,6 +9,8 @@
   oracle after each draft step, then the verify: depth reset, the accepted
   candidate's rows plus a bonus row appended and attended by the
   draft-extend (ring_extend) -- against the oracle, over many rounds;
+* the tree rounds over seeded random shapes (widths 1-6, depths 1-8,
+  windows down to one key, sinks from none, G 1-16);
 * a width-1 tree equals the chain path bit for bit;
 * a request at the largest depth is flagged and left unchanged.
 """
@@ -118,19 +120,46 @@ def _tree_state(dev, B, width, dd, Hkv, d, sink, R_w):
 
 @pytest.mark.parametrize("d,Hq,Hkv,width,dd", [(128, 16, 2, 3, 4), (256, 32, 2, 4, 3), (64, 6, 2, 2, 7)])
 def test_tree_candidates_and_verify(dev, d, Hq, Hkv, width, dd, wpath):
-    B, Wn, sink = 3, 64, 4
+    _tree_rounds(dev, d, Hq, Hkv, width, dd, 64, 4, [2, 66, 300], 20, width * 10 + dd)
+
+
+def _random_tree_case(seed):
+    rng = np.random.default_rng(8000 + seed)
+    d = int(rng.choice([64, 128, 256]))
+    Hkv = int(rng.choice([1, 2, 4]))
+    Gq = int(rng.integers(1, 17))
+    width = int(rng.integers(1, 7))
+    dd = int(rng.integers(1, 9))
+    Wn = int(rng.choice([1, 2, 5, 64, 129]))
+    sink = int(rng.choice([0, 1, 4, 7]))
+    B = int(rng.integers(1, 5))
+    S0 = [int(rng.choice([1, 2, sink + 1, sink + Wn, sink + Wn + 3, 250])) for _ in range(B)]
+    return d, Hkv * Gq, Hkv, width, dd, Wn, sink, S0
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_tree_random_shapes(dev, seed, wpath):
+    """The tree rounds over seeded random shapes: widths 1-6, depths 1-8,
+    windows down to one key, sinks from none, G from 1 to 16."""
+    d, Hq, Hkv, width, dd, Wn, sink, S0 = _random_tree_case(seed)
+    G.say(f"random tree {seed}: d={d} Hq={Hq} Hkv={Hkv} width={width} depth_max={dd} W={Wn} sink={sink} S0={S0}")
+    _tree_rounds(dev, d, Hq, Hkv, width, dd, Wn, sink, S0, 8, 77 + seed)
+
+
+def _tree_rounds(dev, d, Hq, Hkv, width, dd, Wn, sink, S0, n_rounds, seed):
+    B = len(S0)
     R_w = Wn + dd
     scale = 1.0 / np.sqrt(d)
     rows = Rows(dev, Hkv, d)
-    rng = np.random.default_rng(width * 10 + dd)
+    rng = np.random.default_rng(seed)
     kr, vr, kbr, vbr = _tree_state(dev, B, width, dd, Hkv, d, sink, R_w)
     lens = G.lens_tensor([0] * B, dev)
     depth = G.lens_tensor([0] * B, dev)
     err = G.err_word(dev)
     seqs = [P.SpecSequences(width) for _ in range(B)]
-    _prefill(dev, rows, kr, vr, lens, seqs, [2, 66, 300], sink, R_w)
+    _prefill(dev, rows, kr, vr, lens, seqs, S0, sink, R_w)
     lse = torch.empty((B, width, Hq), dtype=torch.float32, device=dev)
-    for rnd in range(20):
+    for rnd in range(n_rounds):
         G.say(f"tree d={d} width={width} dd={dd} round {rnd}")
         n_steps = int(rng.integers(1, dd + 1))
         for i in range(n_steps):
