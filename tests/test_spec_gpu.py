@@ -9,8 +9,8 @@
   oracle after each draft step, then the verify: depth reset, the accepted
   candidate's rows plus a bonus row appended and attended by the
   draft-extend (ring_extend) -- against the oracle, over many rounds;
-* the tree rounds over seeded random shapes (widths 1-6, depths 1-8,
-  windows down to one key, sinks from none, G 1-16);
+* the chain and tree rounds over seeded random shapes (gamma 1-8, widths
+  1-6, depths 1-8, windows down to one key, sinks from none, G 1-16);
 * a width-1 tree equals the chain path bit for bit;
 * a request at the largest depth is flagged and left unchanged.
 """
@@ -65,20 +65,41 @@ def _prefill(dev, rows, kr, vr, lens, seqs, S0, sink, R_w):
 
 @pytest.mark.parametrize("d,Hq,Hkv", [(128, 16, 2), (256, 32, 2)])
 def test_chain_speculate_rollback(dev, d, Hq, Hkv, wpath):
-    B, Wn, sink, gamma = 4, 64, 4, 5
+    _chain_rounds(dev, d, Hq, Hkv, 64, 4, 5, [0, 3, 70, 250], 30, d)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_chain_random_shapes(dev, seed, wpath):
+    """The chain rounds over seeded random shapes: gamma 1-8, windows down to
+    one key, sinks from none, G from 1 to 16."""
+    rng = np.random.default_rng(8500 + seed)
+    d = int(rng.choice([64, 128, 256]))
+    Hkv = int(rng.choice([1, 2, 4]))
+    Hq = Hkv * int(rng.integers(1, 17))
+    gamma = int(rng.integers(1, 9))
+    Wn = int(rng.choice([1, 2, 5, 64, 129]))
+    sink = int(rng.choice([0, 1, 4, 7]))
+    S0 = [int(rng.choice([0, 1, sink + 1, sink + Wn, sink + Wn + 3, 250])) for _ in range(int(rng.integers(1, 5)))]
+    S0[-1] = max(S0[-1], 1)  # at least one prompt row drawn
+    G.say(f"random chain {seed}: d={d} Hq={Hq} Hkv={Hkv} gamma={gamma} W={Wn} sink={sink} S0={S0}")
+    _chain_rounds(dev, d, Hq, Hkv, Wn, sink, gamma, S0, 10, 55 + seed)
+
+
+def _chain_rounds(dev, d, Hq, Hkv, Wn, sink, gamma, S0, n_rounds, seed):
+    B = len(S0)
     R_w = Wn + gamma
     scale = 1.0 / np.sqrt(d)
     rows = Rows(dev, Hkv, d)
-    rng = np.random.default_rng(d)
+    rng = np.random.default_rng(seed)
     kr = torch.zeros((B, sink + R_w, Hkv, d), dtype=torch.bfloat16, device=dev)
     vr = torch.zeros_like(kr)
     lens = G.lens_tensor([0] * B, dev)
     err = G.err_word(dev)
     seqs = [P.SpecSequences(1) for _ in range(B)]
-    _prefill(dev, rows, kr, vr, lens, seqs, [0, 3, 70, 250], sink, R_w)
+    _prefill(dev, rows, kr, vr, lens, seqs, S0, sink, R_w)
     ones = G.lens_tensor([1] * B, dev)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
-    for rnd in range(30):
+    for rnd in range(n_rounds):
         G.say(f"chain d={d} round {rnd}")
         for j in range(gamma):
             k, v, kb, vb = rows.draw(B, 1)
